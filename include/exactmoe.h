@@ -1,0 +1,256 @@
+/*
+ * exactmoe.h -- C ABI of the MI355X (gfx950) fused W4A16 routed-expert layer.
+ *
+ * The layer follows "Every Expert Counts: ExactMoE for Memory-Efficient W4A16
+ * Inference":
+ *   Sec. 3.1, Eq. 1  router logits z = W_r h and top-k selection S_t;
+ *   Sec. 3.1, Eq. 2  y_t = sum_{e in S_t} p_{t,e} W_d,e [phi(W_g,e h) * W_u,e h];
+ *   Sec. 3.2, Eq. 3  symmetric group-128 INT4 weights with FP16 scales;
+ *   Sec. 3.3         per-layer slot cache (global-to-slot map, LRU, events);
+ *   Sec. 3.4         grouped execution in waves of at most C experts.
+ *
+ * Conventions for every call:
+ *   - Return value is an emoe_status (0 = success, < 0 = error).  Nothing is
+ *     enqueued when an argument check fails; emoe_last_error() then holds a
+ *     message for the calling thread.  HIP failures map to EMOE_EHIP.
+ *   - "device" pointers are HIP device memory, "host" pointers are ordinary
+ *     host memory, "pinned" pointers are page-locked host memory
+ *     (hipHostMalloc).  The caller owns every buffer passed in; the library
+ *     owns only the opaque emoe_cache object and what it creates.
+ *   - bf16 values travel as uint16_t bit patterns.  Matrices are row-major in
+ *     nn.Linear order: a projection W[N][K] maps K inputs to N outputs.
+ *   - All device work is enqueued on the stream argument (0 = the null
+ *     stream) and is asynchronous unless the call says otherwise.
+ */
+#ifndef EXACTMOE_H
+#define EXACTMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum emoe_status {
+  EMOE_OK = 0,
+  EMOE_EINVAL = -1,     /* null pointer, bad flag, short buffer, non-pinned host bank */
+  EMOE_ESHAPE = -2,     /* d_model or d_ff not a multiple of 128, bad top_k / expert count */
+  EMOE_ERANGE = -3,     /* a group scale max|W|/7 overflows FP16 */
+  EMOE_ECAPACITY = -4,  /* capacity C outside [top_k, n_experts] */
+  EMOE_EHIP = -5,       /* a HIP runtime call failed */
+  EMOE_ESTATE = -6      /* call not valid for this cache (e.g. no slot bank attached) */
+};
+
+/* Quantization group along the input dimension (Sec. 3.2). */
+#define EMOE_GROUP 128
+/* Largest supported expert count per layer. */
+#define EMOE_MAX_EXPERTS 256
+
+/* Execution path of the expert projections.  AUTO takes the MFMA grouped GEMM
+ * when the call averages at least EMOE_MFMA_MIN_PAIRS_PER_EXPERT token-expert
+ * pairs per expert, else the VALU weight-streaming GEMV.  The choice is made
+ * once per call from (tokens, top_k, n_experts), so every wave of a call uses
+ * the same arithmetic. */
+enum emoe_path { EMOE_PATH_AUTO = 0, EMOE_PATH_GEMV = 1, EMOE_PATH_MFMA = 2 };
+#define EMOE_MFMA_MIN_PAIRS_PER_EXPERT 32
+
+typedef struct emoe_dims {
+  int32_t d_model;    /* hidden size d; multiple of 128 */
+  int32_t d_ff;       /* expert intermediate size f; multiple of 128 */
+  int32_t n_experts;  /* E, 1..EMOE_MAX_EXPERTS */
+  int32_t top_k;      /* k, 1..E */
+} emoe_dims;
+
+/* Counters of Sec. 4.2 / Sec. 5.3 (cache events, transferred bytes, grouped
+ * GEMM calls, sequential expert calls).  Calls that take an emoe_stats*
+ * ADD to it; pass NULL to skip. */
+typedef struct emoe_stats {
+  int64_t layer_calls;         /* moe_forward / moe_forward_sequential calls */
+  int64_t waves;               /* waves executed */
+  int64_t hits;                /* wave experts found resident (C < E only) */
+  int64_t misses;              /* wave experts copied from the host bank */
+  int64_t h2d_bytes;           /* bytes copied host bank -> slot bank */
+  int64_t grouped_gemm_calls;  /* grouped projection launches (2 per wave) */
+  int64_t seq_expert_calls;    /* per-expert launches of the sequential path */
+  int64_t kernel_launches;     /* every kernel launch made by the call */
+} emoe_stats;
+
+/* Byte offsets of the per-call arrays inside a forward workspace. */
+typedef struct emoe_ws_layout {
+  size_t logits;        /* f32   [T][E]   router logits z (Eq. 1) */
+  size_t topk_ids;      /* i32   [T][k]   selected experts, rank order */
+  size_t topk_w;        /* f32   [T][k]   mixture weights p */
+  size_t counts;        /* i32   [E]      pairs per expert */
+  size_t offsets;       /* i32   [E+1]    exclusive prefix sum of counts */
+  size_t sorted_pairs;  /* i32   [T*k]    pair ids pi = t*k+j grouped by expert */
+  size_t active;        /* i32   [E]      active experts, ascending */
+  size_t n_active;      /* i32   [1]      number of active experts */
+  size_t tile_offsets;  /* i32   [E+1]    MFMA row-tile prefix sum */
+  size_t act;           /* bf16  [T*k][d_ff]    phi(g)*u per pair, grouped order */
+  size_t pair_out;      /* f32   [T*k][d_model] expert output per pair id */
+  size_t total;         /* bytes needed */
+} emoe_ws_layout;
+
+typedef struct emoe_cache emoe_cache; /* opaque; owned by the library */
+
+/* ---------------------------------------------------------------- basics */
+const char* emoe_status_string(int32_t status);
+/* Message of the last failing call on this thread ("" if none). */
+const char* emoe_last_error(void);
+/* EMOE_OK if the shape is supported, else EMOE_ESHAPE / EMOE_EINVAL. */
+int32_t emoe_check_dims(const emoe_dims* dims);
+
+/* Bytes of one packed expert record: 3*f*d/2 code bytes + 3*f*d/64 scale
+ * bytes, i.e. Eq. 4's 4/8 + 16/(128*8) bytes per weight with no padding
+ * (3,244,032 B at d = 2048, f = 1024).  0 for unsupported dims. */
+size_t emoe_expert_record_bytes(const emoe_dims* dims);
+
+/* Workspace of emoe_moe_forward for up to max_tokens tokens. */
+int32_t emoe_workspace_layout(const emoe_dims* dims, int32_t max_tokens, emoe_ws_layout* out);
+size_t emoe_workspace_bytes(const emoe_dims* dims, int32_t max_tokens);
+
+/* ---------------------------------------------------------------- offline conversion */
+/* Sec. 3.2, Eq. 3: quantize n experts and pack them into records.
+ *   w_gate, w_up: device bf16 [n][d_ff][d_model];  w_down: device bf16 [n][d_model][d_ff].
+ *   records: device, n * emoe_expert_record_bytes bytes, written in expert order.
+ * Per (row, 128-wide input group): s = fp32(max|W|)/7 (IEEE divide),
+ * q = clip(round_half_even(W/s), -8, 7) from the fp32 s, stored scale =
+ * fp16(s) (round to nearest even); an all-zero group, or one whose FP16
+ * scale underflows to zero, stores s = 0 and q = 0.
+ * Synchronizes `stream` to report EMOE_ERANGE when a scale overflows FP16
+ * (the records are then incomplete). */
+int32_t emoe_quantize_experts(const emoe_dims* dims, int32_t n,
+                              const uint16_t* w_gate, const uint16_t* w_up,
+                              const uint16_t* w_down, void* records, hipStream_t stream);
+
+/* Host-side decode of one packed record (host memory) into plain arrays:
+ *   q_gate, q_up int8 [d_ff][d_model], s_gate, s_up fp16 bits [d_ff][d_model/128];
+ *   q_down int8 [d_model][d_ff], s_down fp16 bits [d_model][d_ff/128].
+ * Any output pointer may be NULL to skip it. */
+int32_t emoe_unpack_expert(const emoe_dims* dims, const void* record,
+                           int8_t* q_gate, uint16_t* s_gate, int8_t* q_up, uint16_t* s_up,
+                           int8_t* q_down, uint16_t* s_down);
+/* Inverse of emoe_unpack_expert (host memory).  Codes must lie in [-8, 7]. */
+int32_t emoe_pack_expert(const emoe_dims* dims, const int8_t* q_gate, const uint16_t* s_gate,
+                         const int8_t* q_up, const uint16_t* s_up, const int8_t* q_down,
+                         const uint16_t* s_down, void* record);
+
+/* ---------------------------------------------------------------- routing and grouping */
+/* Sec. 3.1, Eq. 1 and the grouping of Fig. 1, on the device:
+ *   z[t][e] = fp32( sum_i h[t][i] * w_router[e][i] ) with an fp64 sum
+ *     (or z = logits_override, device f32 [T][E], when non-NULL);
+ *   topk_ids[t][j]: the k largest logits, rank j ordered by logit descending,
+ *     ties to the lower expert id;
+ *   topk_w[t][j]: softmax weights of the selected experts; renormalize != 0
+ *     divides by the sum over the selected experts, 0 by the sum over all E;
+ *   counts[e], offsets[E+1] (exclusive scan), sorted_pairs[T*k] (pair ids
+ *     pi = t*k+j stably sorted by expert), active[<=E] (ascending experts with
+ *     counts > 0) and n_active[1].
+ * h: device bf16 [T][d_model]; w_router: device bf16 [E][d_model] (may be
+ * NULL when logits_override is given); logits: device f32 [T][E] output (may
+ * be NULL with an override).  Logits must not be NaN.  T may be 0. */
+int32_t emoe_route(const emoe_dims* dims, int32_t tokens, const uint16_t* h,
+                   const uint16_t* w_router, const float* logits_override, int32_t renormalize,
+                   float* logits, int32_t* topk_ids, float* topk_w, int32_t* counts,
+                   int32_t* offsets, int32_t* sorted_pairs, int32_t* active, int32_t* n_active,
+                   hipStream_t stream);
+
+/* ---------------------------------------------------------------- slot cache (Sec. 3.3) */
+/* Create the per-layer cache with C = capacity slots, top_k <= C <= E.
+ *   slot_bank: device, C * record_bytes (caller-owned), or NULL;
+ *   host_bank: pinned, E * record_bytes holding this layer's records in
+ *              expert order (caller-owned), or NULL.
+ * With both NULL the cache only plans (emoe_plan_waves / emoe_build_slot_map).
+ * With a slot bank and C = E, emoe_cache_preload_all makes every expert
+ * resident (its record already in slot e, or copied from the host bank).
+ * With a slot bank and C < E a host bank is required; the cache creates one
+ * copy stream (default priority) and one completion event per slot. */
+int32_t emoe_cache_create(const emoe_dims* dims, int32_t capacity, void* slot_bank,
+                          const void* host_bank, emoe_cache** out);
+int32_t emoe_cache_destroy(emoe_cache* cache);
+/* C = E only: identity map, no replacement and no hit accounting afterwards.
+ * Copies the host bank into the slot bank on `stream` when a host bank is
+ * attached; otherwise the slot bank must already hold expert e in slot e. */
+int32_t emoe_cache_preload_all(emoe_cache* cache, hipStream_t stream);
+/* Snapshot: slot_of_expert[E] (-1 absent), expert_of_slot[C] (-1 empty),
+ * stamp_of_slot[C] (-1 never used).  Any pointer may be NULL. */
+int32_t emoe_cache_state(const emoe_cache* cache, int32_t* slot_of_expert,
+                         int32_t* expert_of_slot, int64_t* stamp_of_slot);
+
+/* Sec. 3.4: split the active set into waves of at most C experts.
+ * counts: host [E].  Order: experts resident now (ascending id), then the
+ * others (ascending id), cut into chunks of C.  Outputs (host):
+ * wave_experts[<=E], wave_offsets[<=E+1] (wave w = wave_experts[off[w]..off[w+1])),
+ * n_waves.  Does not change the cache. */
+int32_t emoe_plan_waves(const emoe_cache* cache, const int32_t* counts,
+                        int32_t* wave_experts, int32_t* wave_offsets, int32_t* n_waves);
+
+/* Sec. 3.3 / Sec. 3.4 steps 1-2: resolve one wave (n distinct experts, n <= C).
+ * Resident experts are hits and are protected; each missing expert, in
+ * ascending id order, takes the unprotected slot with the smallest
+ * (stamp, slot index) -- empty slots first -- evicting its occupant.  Every
+ * slot the wave uses is stamped with a clock that ticks once per wave.
+ * Outputs (host): slot_map[E] (-1 = inactive sentinel), fill_expert[n],
+ * fill_slot[n], n_fill.  Updates the cache and adds hits/misses/h2d_bytes. */
+int32_t emoe_build_slot_map(emoe_cache* cache, const int32_t* wave_experts, int32_t n,
+                            int32_t* slot_map, int32_t* fill_expert, int32_t* fill_slot,
+                            int32_t* n_fill, emoe_stats* stats);
+
+/* Host-bank slot fill (Sec. 3.3): copy each listed record from the pinned host
+ * bank to its slot with hipMemcpyAsync on the cache's copy stream, each copy
+ * first waiting for the slot's completion event; `stream` is then made to
+ * wait for the copies.  No host synchronization. */
+int32_t emoe_fill_slots(emoe_cache* cache, const int32_t* fill_expert, const int32_t* fill_slot,
+                        int32_t n_fill, hipStream_t stream);
+
+/* ---------------------------------------------------------------- the layer */
+/* Sec. 3.1 Eq. 1-2 executed as in Sec. 3.4: route and group, then for each
+ * wave resolve/fill its slots, run one grouped gate/up+SwiGLU launch and one
+ * grouped down launch over the whole token matrix, and record slot completion
+ * events; finally add the k weighted expert outputs of every token in rank
+ * order (weights are never renormalized per wave).
+ *   h: device bf16 [T][d_model];  y: device bf16 [T][d_model];
+ *   w_router: device bf16 [E][d_model] (NULL allowed with logits_override);
+ *   workspace: device, >= emoe_workspace_bytes(dims, T) bytes;
+ *   path: an emoe_path value.
+ * With a fully resident cache (C = E after preload) the call never blocks the
+ * host.  Otherwise it copies counts[E] to the host once (one batched expert-id
+ * transfer) and synchronizes `stream` to plan the waves.  If a fill fails the
+ * cache map is restored to its state before that wave. */
+int32_t emoe_moe_forward(emoe_cache* cache, int32_t tokens, const uint16_t* h,
+                         const uint16_t* w_router, const float* logits_override,
+                         int32_t renormalize, int32_t path, uint16_t* y, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream, emoe_stats* stats);
+
+/* Sequential W4 reference path (Sec. 3.4, Sec. 5.3): same routing, cache
+ * handling and arithmetic, but one gate/up and one down launch per active
+ * expert instead of per wave.  Output is bit-identical to emoe_moe_forward
+ * with the same path. */
+int32_t emoe_moe_forward_sequential(emoe_cache* cache, int32_t tokens, const uint16_t* h,
+                                    const uint16_t* w_router, const float* logits_override,
+                                    int32_t renormalize, int32_t path, uint16_t* y,
+                                    void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream, emoe_stats* stats);
+
+/* ---------------------------------------------------------------- kernel timing */
+/* Kernels launched by the layer calls, as reported by emoe_profile_end. */
+enum emoe_kernel {
+  EMOE_K_ROUTER = 0, EMOE_K_TOPK = 1, EMOE_K_GROUP = 2, EMOE_K_GATEUP_GEMV = 3,
+  EMOE_K_DOWN_GEMV = 4, EMOE_K_GATEUP_MFMA = 5, EMOE_K_DOWN_MFMA = 6, EMOE_K_COMBINE = 7
+};
+/* Start recording a HIP event pair around each kernel that emoe_route,
+ * emoe_moe_forward and emoe_moe_forward_sequential launch from this thread,
+ * on the stream the kernel is launched on, for up to max_kernels launches.
+ * Creates the events (host call, not for use under graph capture). */
+int32_t emoe_profile_begin(int32_t max_kernels);
+/* Stop recording, wait for the recorded events and return, in launch order,
+ * each kernel's kind (emoe_kernel) and duration in milliseconds; n_out =
+ * number of kernels recorded (at most max_out are written).  Frees the events. */
+int32_t emoe_profile_end(int32_t* kinds, float* ms, int32_t max_out, int32_t* n_out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EXACTMOE_H */

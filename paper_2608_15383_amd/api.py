@@ -1,0 +1,185 @@
+"""Thin Python binding of libexactmoe.so with the C ABI's names.
+
+PyTorch only supplies device memory, pinned host memory and streams; every
+step of the layer runs in the HIP library.  Tensors holding bf16 data may be
+torch.bfloat16 or int16/uint16 bit patterns; they are passed by data_ptr().
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+import numpy as np
+
+from . import _lib
+from ._lib import (Dims, Stats, WsLayout, check, lib, EMOE_PATH_AUTO, EMOE_PATH_GEMV,
+                   EMOE_PATH_MFMA, ExactMoEError)
+
+
+def _ptr(t) -> int | None:
+    if t is None:
+        return None
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def dims(d_model: int, d_ff: int, n_experts: int, top_k: int) -> Dims:
+    return Dims(d_model, d_ff, n_experts, top_k)
+
+
+def check_dims(dm: Dims) -> None:
+    check(lib().emoe_check_dims(C.byref(dm)))
+
+
+def expert_record_bytes(dm: Dims) -> int:
+    return int(lib().emoe_expert_record_bytes(C.byref(dm)))
+
+
+def workspace_layout(dm: Dims, max_tokens: int) -> WsLayout:
+    out = WsLayout()
+    check(lib().emoe_workspace_layout(C.byref(dm), max_tokens, C.byref(out)))
+    return out
+
+
+def workspace_bytes(dm: Dims, max_tokens: int) -> int:
+    return int(lib().emoe_workspace_bytes(C.byref(dm), max_tokens))
+
+
+def quantize_experts(dm: Dims, w_gate, w_up, w_down, records, stream=None) -> None:
+    """emoe_quantize_experts: device bf16 weights -> device packed records."""
+    n = w_gate.shape[0]
+    check(lib().emoe_quantize_experts(C.byref(dm), n, _ptr(w_gate), _ptr(w_up), _ptr(w_down),
+                                      _ptr(records), _stream(stream)))
+
+
+def unpack_expert(dm: Dims, record: np.ndarray) -> dict:
+    """emoe_unpack_expert on a host copy of one record (numpy uint8)."""
+    d, f = dm.d_model, dm.d_ff
+    out = dict(q_gate=np.empty((f, d), np.int8), s_gate=np.empty((f, d // 128), np.uint16),
+               q_up=np.empty((f, d), np.int8), s_up=np.empty((f, d // 128), np.uint16),
+               q_down=np.empty((d, f), np.int8), s_down=np.empty((d, f // 128), np.uint16))
+    rec = np.ascontiguousarray(record, dtype=np.uint8)
+    check(lib().emoe_unpack_expert(C.byref(dm), rec.ctypes.data, *[out[k].ctypes.data for k in
+                                   ("q_gate", "s_gate", "q_up", "s_up", "q_down", "s_down")]))
+    return out
+
+
+def pack_expert(dm: Dims, q_gate, s_gate, q_up, s_up, q_down, s_down) -> np.ndarray:
+    """emoe_pack_expert: plain codes/scales (host) -> one packed record (numpy uint8)."""
+    rec = np.zeros(expert_record_bytes(dm), np.uint8)
+    arrs = [np.ascontiguousarray(a) for a in (q_gate, s_gate, q_up, s_up, q_down, s_down)]
+    check(lib().emoe_pack_expert(C.byref(dm), *[a.ctypes.data for a in arrs], rec.ctypes.data))
+    return rec
+
+
+def route(dm: Dims, tokens: int, h, w_router, logits_override, renormalize: bool, logits,
+          topk_ids, topk_w, counts, offsets, sorted_pairs, active, n_active, stream=None) -> None:
+    """emoe_route: Eq. 1 logits, top-k, mixture weights and grouping on the device."""
+    check(lib().emoe_route(C.byref(dm), tokens, _ptr(h), _ptr(w_router), _ptr(logits_override),
+                           int(bool(renormalize)), _ptr(logits), _ptr(topk_ids), _ptr(topk_w),
+                           _ptr(counts), _ptr(offsets), _ptr(sorted_pairs), _ptr(active),
+                           _ptr(n_active), _stream(stream)))
+
+
+class Cache:
+    """emoe_cache_*: one layer's slot cache (Sec. 3.3)."""
+
+    def __init__(self, dm: Dims, capacity: int, slot_bank=None, host_bank=None):
+        self.dims = dm
+        self.capacity = capacity
+        self._keep = (slot_bank, host_bank)
+        handle = C.c_void_p()
+        check(lib().emoe_cache_create(C.byref(dm), capacity, _ptr(slot_bank), _ptr(host_bank),
+                                      C.byref(handle)))
+        self.handle = handle
+
+    def close(self) -> None:
+        if self.handle:
+            lib().emoe_cache_destroy(self.handle)
+            self.handle = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def preload_all(self, stream=None) -> None:
+        check(lib().emoe_cache_preload_all(self.handle, _stream(stream)))
+
+    def state(self):
+        e, c = self.dims.n_experts, self.capacity
+        so, eo, st = np.empty(e, np.int32), np.empty(c, np.int32), np.empty(c, np.int64)
+        check(lib().emoe_cache_state(self.handle, so.ctypes.data, eo.ctypes.data, st.ctypes.data))
+        return so, eo, st
+
+    def plan_waves(self, counts) -> list[list[int]]:
+        e = self.dims.n_experts
+        cnt = np.ascontiguousarray(counts, np.int32)
+        we, wo, nw = np.empty(e, np.int32), np.empty(e + 1, np.int32), C.c_int32()
+        check(lib().emoe_plan_waves(self.handle, cnt.ctypes.data, we.ctypes.data, wo.ctypes.data,
+                                    C.byref(nw)))
+        return [we[wo[i]:wo[i + 1]].tolist() for i in range(nw.value)]
+
+    def build_slot_map(self, wave, stats: Stats | None = None):
+        e = self.dims.n_experts
+        w = np.ascontiguousarray(wave, np.int32)
+        sm = np.empty(e, np.int32)
+        fe, fs = np.empty(max(len(w), 1), np.int32), np.empty(max(len(w), 1), np.int32)
+        nf = C.c_int32()
+        check(lib().emoe_build_slot_map(self.handle, w.ctypes.data, len(w), sm.ctypes.data,
+                                        fe.ctypes.data, fs.ctypes.data, C.byref(nf),
+                                        C.byref(stats) if stats is not None else None))
+        return sm, list(zip(fe[:nf.value].tolist(), fs[:nf.value].tolist()))
+
+    def fill_slots(self, fills, stream=None) -> None:
+        fe = np.array([a for a, _ in fills], np.int32)
+        fs = np.array([b for _, b in fills], np.int32)
+        check(lib().emoe_fill_slots(self.handle, fe.ctypes.data, fs.ctypes.data, len(fills),
+                                    _stream(stream)))
+
+
+def moe_forward(cache: Cache, h, w_router, y, workspace, logits_override=None,
+                renormalize: bool = True, path: int = EMOE_PATH_AUTO, stats: Stats | None = None,
+                stream=None, sequential: bool = False) -> None:
+    """emoe_moe_forward (or emoe_moe_forward_sequential): y = the MoE layer of Eq. 2."""
+    fn = lib().emoe_moe_forward_sequential if sequential else lib().emoe_moe_forward
+    tokens = h.shape[0]
+    nbytes = workspace.numel() * workspace.element_size()
+    check(fn(cache.handle, tokens, _ptr(h), _ptr(w_router), _ptr(logits_override),
+             int(bool(renormalize)), path, _ptr(y), _ptr(workspace), nbytes, _stream(stream),
+             C.byref(stats) if stats is not None else None))
+
+
+def moe_forward_sequential(cache: Cache, h, w_router, y, workspace, **kw) -> None:
+    moe_forward(cache, h, w_router, y, workspace, sequential=True, **kw)
+
+
+def profile_begin(max_kernels: int) -> None:
+    """emoe_profile_begin: time each kernel the layer calls launch from this thread."""
+    check(lib().emoe_profile_begin(max_kernels))
+
+
+def profile_end(max_out: int = 1 << 16) -> list[tuple[str, float]]:
+    """emoe_profile_end: [(kernel name, milliseconds)] in launch order."""
+    kinds = np.empty(max_out, np.int32)
+    ms = np.empty(max_out, np.float32)
+    n = C.c_int32()
+    check(lib().emoe_profile_end(kinds.ctypes.data, ms.ctypes.data, max_out, C.byref(n)))
+    m = min(n.value, max_out)
+    return [(_lib.KERNEL_NAMES[k], float(t)) for k, t in zip(kinds[:m], ms[:m])]
+
+
+__all__ = ["Dims", "Stats", "WsLayout", "ExactMoEError", "EMOE_PATH_AUTO", "EMOE_PATH_GEMV",
+           "EMOE_PATH_MFMA", "dims", "check_dims", "expert_record_bytes", "workspace_layout",
+           "workspace_bytes", "quantize_experts", "unpack_expert", "pack_expert", "route", "Cache",
+           "moe_forward", "moe_forward_sequential", "profile_begin", "profile_end", "lib"]

@@ -1,0 +1,751 @@
+// Host runtime and C ABI of libexactmoe.so: argument checks, the workspace
+// layout, the per-layer slot cache with LRU replacement and event-ordered
+// slot reuse (Sec. 3.3), wave planning and the per-wave execution loop of
+// Sec. 3.4, and the sequential per-expert comparison path.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "common.h"
+
+using namespace emoe;
+
+// ------------------------------------------------------------------ errors
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int32_t fail(int32_t status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int32_t hip_fail(hipError_t e, const char* what) {
+  return fail(EMOE_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define EMOE_HIP(call)                                  \
+  do {                                                  \
+    hipError_t e_ = (call);                             \
+    if (e_ != hipSuccess) return hip_fail(e_, #call);   \
+  } while (0)
+
+size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Optional per-thread kernel timing (emoe_profile_begin / emoe_profile_end).
+struct Profiler {
+  bool on = false;
+  int max = 0;
+  std::vector<hipEvent_t> start, stop;
+  std::vector<int32_t> kind;
+  int used = 0;
+};
+thread_local Profiler g_prof;
+
+hipError_t timed_launch(int32_t kind, hipStream_t stream, hipError_t (*fn)(void*), void* ctx) {
+  Profiler& p = g_prof;
+  const bool rec = p.on && p.used < p.max;
+  if (rec) {
+    hipError_t e = hipEventRecord(p.start[p.used], stream);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = fn(ctx);
+  if (e != hipSuccess || !rec) return e;
+  e = hipEventRecord(p.stop[p.used], stream);
+  p.kind[p.used++] = kind;
+  return e;
+}
+
+// EMOE_LAUNCH(kind, stream, expr): run the launcher expression `expr`, with a
+// timing event pair around it while profiling is on; return on failure.
+#define EMOE_LAUNCH(kind, stream, expr)                                              \
+  do {                                                                               \
+    auto fn_ = [&]() -> hipError_t { return (expr); };                               \
+    hipError_t e_ = timed_launch((kind), (stream),                                   \
+                                 [](void* c) { return (*static_cast<decltype(fn_)*>(c))(); }, \
+                                 &fn_);                                              \
+    if (e_ != hipSuccess) return hip_fail(e_, #expr);                                \
+  } while (0)
+
+}  // namespace
+
+// ------------------------------------------------------------------ cache object
+struct emoe_cache {
+  emoe_dims dims;
+  int32_t capacity = 0;
+  int64_t record_bytes = 0;
+  uint8_t* slot_bank = nullptr;
+  const uint8_t* host_bank = nullptr;
+  bool resident_all = false;
+  std::vector<int32_t> slot_of;     // [E]
+  std::vector<int32_t> expert_of;   // [C]
+  std::vector<int64_t> stamp;       // [C]
+  int64_t clock = 0;
+  int device = -1;
+  hipStream_t copy_stream = nullptr;
+  std::vector<hipEvent_t> release;  // [C] completion of the last wave using the slot
+  hipEvent_t ready = nullptr;       // completion of the last batch of fills
+  int32_t* counts_host = nullptr;   // pinned [E]: the batched expert-id transfer
+};
+
+namespace {
+
+int32_t check_dims(const emoe_dims* d) {
+  if (!d) return fail(EMOE_EINVAL, "dims is NULL");
+  if (d->d_model <= 0 || d->d_ff <= 0 || d->d_model % EMOE_GROUP || d->d_ff % EMOE_GROUP)
+    return fail(EMOE_ESHAPE, "d_model=%d and d_ff=%d must be positive multiples of %d",
+                d->d_model, d->d_ff, EMOE_GROUP);
+  if (d->n_experts < 1 || d->n_experts > EMOE_MAX_EXPERTS)
+    return fail(EMOE_ESHAPE, "n_experts=%d outside [1, %d]", d->n_experts, EMOE_MAX_EXPERTS);
+  if (d->top_k < 1 || d->top_k > d->n_experts)
+    return fail(EMOE_ESHAPE, "top_k=%d outside [1, n_experts=%d]", d->top_k, d->n_experts);
+  return EMOE_OK;
+}
+
+emoe_ws_layout make_layout(const emoe_dims& d, int32_t T) {
+  emoe_ws_layout L{};
+  const size_t E = d.n_experts, k = d.top_k, P = (size_t)T * k;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align_up(bytes);
+    return at;
+  };
+  L.logits = take((size_t)T * E * 4);
+  L.topk_ids = take(P * 4);
+  L.topk_w = take(P * 4);
+  L.counts = take(E * 4);
+  L.offsets = take((E + 1) * 4);
+  L.sorted_pairs = take(P * 4);
+  L.active = take(E * 4);
+  L.n_active = take(4);
+  L.tile_offsets = take((E + 1) * 4);
+  L.act = take(P * (size_t)d.d_ff * 2);
+  L.pair_out = take(P * (size_t)d.d_model * 4);
+  L.total = off;
+  return L;
+}
+
+// Per-device scratch flag of the quantizer (allocated once per device).
+std::mutex g_flag_mu;
+int32_t* g_range_flag[64] = {};
+
+int32_t range_flag_for_current_device(int32_t** out) {
+  int dev = 0;
+  EMOE_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return fail(EMOE_EINVAL, "device index %d unsupported", dev);
+  std::lock_guard<std::mutex> lk(g_flag_mu);
+  if (!g_range_flag[dev]) EMOE_HIP(hipMalloc(&g_range_flag[dev], 256));
+  *out = g_range_flag[dev];
+  return EMOE_OK;
+}
+
+void add_stats(emoe_stats* s, const emoe_stats& d) {
+  if (!s) return;
+  s->layer_calls += d.layer_calls;
+  s->waves += d.waves;
+  s->hits += d.hits;
+  s->misses += d.misses;
+  s->h2d_bytes += d.h2d_bytes;
+  s->grouped_gemm_calls += d.grouped_gemm_calls;
+  s->seq_expert_calls += d.seq_expert_calls;
+  s->kernel_launches += d.kernel_launches;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* emoe_status_string(int32_t st) {
+  switch (st) {
+    case EMOE_OK: return "ok";
+    case EMOE_EINVAL: return "invalid argument";
+    case EMOE_ESHAPE: return "unsupported shape";
+    case EMOE_ERANGE: return "scale out of FP16 range";
+    case EMOE_ECAPACITY: return "capacity outside [top_k, n_experts]";
+    case EMOE_EHIP: return "HIP runtime error";
+    case EMOE_ESTATE: return "call not valid for this cache";
+    default: return "unknown status";
+  }
+}
+
+const char* emoe_last_error(void) { return g_last_error; }
+
+int32_t emoe_check_dims(const emoe_dims* dims) { return check_dims(dims); }
+
+size_t emoe_expert_record_bytes(const emoe_dims* dims) {
+  if (check_dims(dims) != EMOE_OK) return 0;
+  return (size_t)record_layout(dims->d_model, dims->d_ff).bytes;
+}
+
+int32_t emoe_workspace_layout(const emoe_dims* dims, int32_t max_tokens, emoe_ws_layout* out) {
+  int32_t st = check_dims(dims);
+  if (st) return st;
+  if (max_tokens < 0 || !out) return fail(EMOE_EINVAL, "bad max_tokens or NULL output");
+  *out = make_layout(*dims, max_tokens);
+  return EMOE_OK;
+}
+
+size_t emoe_workspace_bytes(const emoe_dims* dims, int32_t max_tokens) {
+  if (check_dims(dims) != EMOE_OK || max_tokens < 0) return 0;
+  return make_layout(*dims, max_tokens).total;
+}
+
+// ------------------------------------------------------------------ quantization
+int32_t emoe_quantize_experts(const emoe_dims* dims, int32_t n, const uint16_t* w_gate,
+                              const uint16_t* w_up, const uint16_t* w_down, void* records,
+                              hipStream_t stream) {
+  int32_t st = check_dims(dims);
+  if (st) return st;
+  if (n < 0 || n > 65535) return fail(EMOE_EINVAL, "n=%d experts out of range", n);
+  if (n == 0) return EMOE_OK;
+  if (!w_gate || !w_up || !w_down || !records) return fail(EMOE_EINVAL, "NULL buffer");
+  int32_t* flag = nullptr;
+  if ((st = range_flag_for_current_device(&flag))) return st;
+  EMOE_HIP(hipMemsetAsync(flag, 0, sizeof(int32_t), stream));
+  EMOE_HIP(launch_quantize(dims->d_model, dims->d_ff, n, w_gate, w_up, w_down,
+                           static_cast<uint8_t*>(records), flag, stream));
+  int32_t host_flag = 0;
+  EMOE_HIP(hipMemcpyAsync(&host_flag, flag, sizeof host_flag, hipMemcpyDeviceToHost, stream));
+  EMOE_HIP(hipStreamSynchronize(stream));
+  if (host_flag) return fail(EMOE_ERANGE, "a group scale max|W|/7 overflows FP16");
+  return EMOE_OK;
+}
+
+int32_t emoe_unpack_expert(const emoe_dims* dims, const void* record, int8_t* q_gate,
+                           uint16_t* s_gate, int8_t* q_up, uint16_t* s_up, int8_t* q_down,
+                           uint16_t* s_down) {
+  int32_t st = check_dims(dims);
+  if (st) return st;
+  if (!record) return fail(EMOE_EINVAL, "record is NULL");
+  const int d = dims->d_model, f = dims->d_ff;
+  const RecordLayout L = record_layout(d, f);
+  const uint8_t* rec = static_cast<const uint8_t*>(record);
+  // Decode one matrix (N x K codes at `codes`, fp16 [N][K/128] at `sc`) into
+  // row-major outputs; `row_of(n)` maps the stored row to the output row or -1.
+  auto decode = [&](int N, int K, int64_t codes_off, int64_t sc_off, auto row_of, int8_t* q,
+                    uint16_t* s) {
+    const int G = K / kGroup;
+    for (int rb = 0; rb < N / kTileRows; ++rb)
+      for (int g = 0; g < G; ++g) {
+        const uint8_t* tile = rec + codes_off + ((int64_t)rb * G + g) * kTileBytes;
+        for (int l = 0; l < 64; ++l) {
+          const int out_row = row_of(rb * kTileRows + (l & 15));
+          if (out_row < 0 || !q) continue;
+          for (int i = 0; i < 4; ++i) {
+            uint32_t dw;
+            std::memcpy(&dw, tile + 16 * l + 4 * i, 4);
+            for (int r = 0; r < 8; ++r) {
+              const int kk = g * kGroup + 32 * i + 8 * (l >> 4) + r;
+              const uint32_t u = (dw >> (4 * (r >> 1) + 16 * (r & 1))) & 0xfu;
+              q[(int64_t)out_row * K + kk] = (int8_t)((int)u - 8);
+            }
+          }
+        }
+      }
+    if (s) {
+      const uint16_t* sp = reinterpret_cast<const uint16_t*>(rec + sc_off);
+      for (int n = 0; n < N; ++n) {
+        const int out_row = row_of(n);
+        if (out_row < 0) continue;
+        std::memcpy(s + (int64_t)out_row * G, sp + (int64_t)n * G, G * 2);
+      }
+    }
+  };
+  // W13 stored row n -> gate row (block parity 0) or up row (parity 1).
+  auto gate_row = [](int n) { return ((n >> 4) & 1) ? -1 : ((n >> 5) << 4) + (n & 15); };
+  auto up_row = [](int n) { return ((n >> 4) & 1) ? ((n >> 5) << 4) + (n & 15) : -1; };
+  auto same_row = [](int n) { return n; };
+  decode(2 * f, d, L.w13_codes, L.w13_scales, gate_row, q_gate, s_gate);
+  decode(2 * f, d, L.w13_codes, L.w13_scales, up_row, q_up, s_up);
+  decode(d, f, L.w2_codes, L.w2_scales, same_row, q_down, s_down);
+  return EMOE_OK;
+}
+
+int32_t emoe_pack_expert(const emoe_dims* dims, const int8_t* q_gate, const uint16_t* s_gate,
+                         const int8_t* q_up, const uint16_t* s_up, const int8_t* q_down,
+                         const uint16_t* s_down, void* record) {
+  int32_t st = check_dims(dims);
+  if (st) return st;
+  if (!q_gate || !s_gate || !q_up || !s_up || !q_down || !s_down || !record)
+    return fail(EMOE_EINVAL, "NULL buffer");
+  const int d = dims->d_model, f = dims->d_ff;
+  const RecordLayout L = record_layout(d, f);
+  uint8_t* rec = static_cast<uint8_t*>(record);
+  auto encode = [&](int N, int K, int64_t codes_off, int64_t sc_off, auto src_of) -> int32_t {
+    const int G = K / kGroup;
+    for (int rb = 0; rb < N / kTileRows; ++rb)
+      for (int g = 0; g < G; ++g) {
+        uint8_t* tile = rec + codes_off + ((int64_t)rb * G + g) * kTileBytes;
+        for (int l = 0; l < 64; ++l) {
+          const int8_t* qrow;
+          const uint16_t* srow;
+          src_of(rb * kTileRows + (l & 15), qrow, srow);
+          for (int i = 0; i < 4; ++i) {
+            uint32_t dw = 0;
+            for (int r = 0; r < 8; ++r) {
+              const int v = qrow[g * kGroup + 32 * i + 8 * (l >> 4) + r];
+              if (v < -8 || v > 7) return fail(EMOE_ERANGE, "code %d outside [-8, 7]", v);
+              dw |= (uint32_t)(v + 8) << (4 * (r >> 1) + 16 * (r & 1));
+            }
+            std::memcpy(tile + 16 * l + 4 * i, &dw, 4);
+          }
+        }
+      }
+    uint16_t* sp = reinterpret_cast<uint16_t*>(rec + sc_off);
+    for (int n = 0; n < N; ++n) {
+      const int8_t* qrow;
+      const uint16_t* srow;
+      src_of(n, qrow, srow);
+      std::memcpy(sp + (int64_t)n * G, srow, G * 2);
+    }
+    return EMOE_OK;
+  };
+  const int Gd = d / kGroup, Gf = f / kGroup;
+  auto w13_src = [&](int n, const int8_t*& qrow, const uint16_t*& srow) {
+    const int row = ((n >> 5) << 4) + (n & 15);
+    const bool up = (n >> 4) & 1;
+    qrow = (up ? q_up : q_gate) + (int64_t)row * d;
+    srow = (up ? s_up : s_gate) + (int64_t)row * Gd;
+  };
+  auto w2_src = [&](int n, const int8_t*& qrow, const uint16_t*& srow) {
+    qrow = q_down + (int64_t)n * f;
+    srow = s_down + (int64_t)n * Gf;
+  };
+  if ((st = encode(2 * f, d, L.w13_codes, L.w13_scales, w13_src))) return st;
+  return encode(d, f, L.w2_codes, L.w2_scales, w2_src);
+}
+
+// ------------------------------------------------------------------ routing
+int32_t emoe_route(const emoe_dims* dims, int32_t T, const uint16_t* h, const uint16_t* w_router,
+                   const float* logits_override, int32_t renormalize, float* logits,
+                   int32_t* topk_ids, float* topk_w, int32_t* counts, int32_t* offsets,
+                   int32_t* sorted_pairs, int32_t* active, int32_t* n_active, hipStream_t stream) {
+  int32_t st = check_dims(dims);
+  if (st) return st;
+  if (T < 0) return fail(EMOE_EINVAL, "tokens=%d < 0", T);
+  if (!counts || !offsets || !active || !n_active) return fail(EMOE_EINVAL, "NULL output");
+  if (T > 0) {
+    if (!topk_ids || !topk_w || !sorted_pairs) return fail(EMOE_EINVAL, "NULL output");
+    if (!logits_override && (!h || !w_router || !logits))
+      return fail(EMOE_EINVAL, "h, w_router and logits are required without logits_override");
+  }
+  const int E = dims->n_experts, k = dims->top_k;
+  const float* z = logits_override ? logits_override : logits;
+  if (T > 0 && !logits_override)
+    EMOE_LAUNCH(EMOE_K_ROUTER, stream,
+                launch_router_logits(T, E, dims->d_model, h, w_router, logits, stream));
+  if (T > 0)
+    EMOE_LAUNCH(EMOE_K_TOPK, stream, launch_topk(T, E, k, renormalize, z, topk_ids, topk_w, stream));
+  EMOE_LAUNCH(EMOE_K_GROUP, stream,
+              launch_group(T * k, E, topk_ids, counts, offsets, sorted_pairs, active, n_active,
+                           nullptr, stream));
+  return EMOE_OK;
+}
+
+// ------------------------------------------------------------------ cache
+int32_t emoe_cache_create(const emoe_dims* dims, int32_t capacity, void* slot_bank,
+                          const void* host_bank, emoe_cache** out) {
+  int32_t st = check_dims(dims);
+  if (st) return st;
+  if (!out) return fail(EMOE_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (capacity < dims->top_k || capacity > dims->n_experts)
+    return fail(EMOE_ECAPACITY, "capacity %d outside [top_k=%d, n_experts=%d]", capacity,
+                dims->top_k, dims->n_experts);
+  if (!slot_bank && host_bank) return fail(EMOE_EINVAL, "a host bank needs a slot bank");
+  if (slot_bank && !host_bank && capacity != dims->n_experts)
+    return fail(EMOE_EINVAL, "C < E needs a pinned host bank to fill slots from");
+  if (host_bank) {
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, host_bank) != hipSuccess || attr.type != hipMemoryTypeHost) {
+      (void)hipGetLastError();
+      return fail(EMOE_EINVAL, "host_bank is not pinned host memory (use hipHostMalloc)");
+    }
+  }
+  emoe_cache* c = new (std::nothrow) emoe_cache();
+  if (!c) return fail(EMOE_EINVAL, "out of host memory");
+  c->dims = *dims;
+  c->capacity = capacity;
+  c->record_bytes = record_layout(dims->d_model, dims->d_ff).bytes;
+  c->slot_bank = static_cast<uint8_t*>(slot_bank);
+  c->host_bank = static_cast<const uint8_t*>(host_bank);
+  c->slot_of.assign(dims->n_experts, -1);
+  c->expert_of.assign(capacity, -1);
+  c->stamp.assign(capacity, -1);
+  if (slot_bank) {
+    hipError_t e = hipGetDevice(&c->device);
+    if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&c->counts_host),
+                                           sizeof(int32_t) * dims->n_experts, hipHostMallocDefault);
+    if (e == hipSuccess && host_bank) {
+      e = hipStreamCreateWithFlags(&c->copy_stream, hipStreamNonBlocking);
+      if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ready, hipEventDisableTiming);
+      c->release.assign(capacity, nullptr);
+      for (int s = 0; s < capacity && e == hipSuccess; ++s)
+        e = hipEventCreateWithFlags(&c->release[s], hipEventDisableTiming);
+    }
+    if (e != hipSuccess) {
+      emoe_cache_destroy(c);
+      return hip_fail(e, "cache resources");
+    }
+  }
+  *out = c;
+  return EMOE_OK;
+}
+
+int32_t emoe_cache_destroy(emoe_cache* c) {
+  if (!c) return EMOE_OK;
+  if (c->copy_stream) (void)hipStreamSynchronize(c->copy_stream);
+  for (hipEvent_t ev : c->release)
+    if (ev) (void)hipEventDestroy(ev);
+  if (c->ready) (void)hipEventDestroy(c->ready);
+  if (c->copy_stream) (void)hipStreamDestroy(c->copy_stream);
+  if (c->counts_host) (void)hipHostFree(c->counts_host);
+  delete c;
+  return EMOE_OK;
+}
+
+int32_t emoe_cache_preload_all(emoe_cache* c, hipStream_t stream) {
+  if (!c) return fail(EMOE_EINVAL, "cache is NULL");
+  if (c->capacity != c->dims.n_experts)
+    return fail(EMOE_ESTATE, "full residency needs capacity == n_experts");
+  if (!c->slot_bank) return fail(EMOE_ESTATE, "no slot bank attached");
+  if (c->host_bank)
+    EMOE_HIP(hipMemcpyAsync(c->slot_bank, c->host_bank,
+                            (size_t)c->record_bytes * c->capacity, hipMemcpyHostToDevice, stream));
+  for (int e = 0; e < c->dims.n_experts; ++e) {
+    c->slot_of[e] = e;
+    c->expert_of[e] = e;
+  }
+  c->resident_all = true;
+  return EMOE_OK;
+}
+
+int32_t emoe_cache_state(const emoe_cache* c, int32_t* slot_of_expert, int32_t* expert_of_slot,
+                         int64_t* stamp_of_slot) {
+  if (!c) return fail(EMOE_EINVAL, "cache is NULL");
+  if (slot_of_expert) std::copy(c->slot_of.begin(), c->slot_of.end(), slot_of_expert);
+  if (expert_of_slot) std::copy(c->expert_of.begin(), c->expert_of.end(), expert_of_slot);
+  if (stamp_of_slot) std::copy(c->stamp.begin(), c->stamp.end(), stamp_of_slot);
+  return EMOE_OK;
+}
+
+int32_t emoe_plan_waves(const emoe_cache* c, const int32_t* counts, int32_t* wave_experts,
+                        int32_t* wave_offsets, int32_t* n_waves) {
+  if (!c || !counts || !wave_experts || !wave_offsets || !n_waves)
+    return fail(EMOE_EINVAL, "NULL argument");
+  const int E = c->dims.n_experts;
+  int n = 0;
+  for (int pass = 0; pass < 2; ++pass)  // resident first, then the rest
+    for (int e = 0; e < E; ++e) {
+      if (counts[e] < 0) return fail(EMOE_EINVAL, "counts[%d] < 0", e);
+      if (counts[e] > 0 && ((c->slot_of[e] >= 0) == (pass == 0))) wave_experts[n++] = e;
+    }
+  int w = 0;
+  for (int at = 0; at < n; at += c->capacity) wave_offsets[w++] = at;
+  wave_offsets[w] = n;
+  *n_waves = w;
+  return EMOE_OK;
+}
+
+int32_t emoe_build_slot_map(emoe_cache* c, const int32_t* wave, int32_t n, int32_t* slot_map,
+                            int32_t* fill_expert, int32_t* fill_slot, int32_t* n_fill,
+                            emoe_stats* stats) {
+  if (!c || (n > 0 && !wave) || !slot_map || !n_fill) return fail(EMOE_EINVAL, "NULL argument");
+  const int E = c->dims.n_experts, C = c->capacity;
+  if (n < 0 || n > C) return fail(EMOE_ECAPACITY, "wave of %d experts exceeds capacity %d", n, C);
+  std::vector<char> seen(E, 0);
+  for (int i = 0; i < n; ++i) {
+    if (wave[i] < 0 || wave[i] >= E) return fail(EMOE_EINVAL, "expert %d out of range", wave[i]);
+    if (seen[wave[i]]++) return fail(EMOE_EINVAL, "expert %d repeated in a wave", wave[i]);
+  }
+  std::fill(slot_map, slot_map + E, -1);
+  *n_fill = 0;
+  if (c->resident_all) {
+    for (int i = 0; i < n; ++i) slot_map[wave[i]] = wave[i];
+    return EMOE_OK;
+  }
+  if (n > 0 && (!fill_expert || !fill_slot)) return fail(EMOE_EINVAL, "NULL fill list");
+  emoe_stats d{};
+  c->clock += 1;
+  std::vector<char> prot(C, 0);
+  for (int i = 0; i < n; ++i) {
+    const int s = c->slot_of[wave[i]];
+    if (s >= 0) {
+      d.hits += 1;
+      prot[s] = 1;
+      c->stamp[s] = c->clock;
+    }
+  }
+  std::vector<int32_t> missing;
+  for (int i = 0; i < n; ++i)
+    if (c->slot_of[wave[i]] < 0) missing.push_back(wave[i]);
+  std::sort(missing.begin(), missing.end());
+  for (int e : missing) {
+    int victim = -1;
+    for (int s = 0; s < C; ++s) {
+      if (prot[s]) continue;
+      if (victim < 0 || c->stamp[s] < c->stamp[victim]) victim = s;
+    }
+    const int old = c->expert_of[victim];
+    if (old >= 0) c->slot_of[old] = -1;
+    c->expert_of[victim] = e;
+    c->slot_of[e] = victim;
+    c->stamp[victim] = c->clock;
+    prot[victim] = 1;
+    fill_expert[*n_fill] = e;
+    fill_slot[*n_fill] = victim;
+    *n_fill += 1;
+    d.misses += 1;
+    d.h2d_bytes += c->record_bytes;
+  }
+  for (int i = 0; i < n; ++i) slot_map[wave[i]] = c->slot_of[wave[i]];
+  add_stats(stats, d);
+  return EMOE_OK;
+}
+
+int32_t emoe_fill_slots(emoe_cache* c, const int32_t* fill_expert, const int32_t* fill_slot,
+                        int32_t n_fill, hipStream_t stream) {
+  if (!c) return fail(EMOE_EINVAL, "cache is NULL");
+  if (n_fill == 0) return EMOE_OK;
+  if (n_fill < 0 || !fill_expert || !fill_slot) return fail(EMOE_EINVAL, "bad fill list");
+  if (!c->slot_bank || !c->host_bank || !c->copy_stream)
+    return fail(EMOE_ESTATE, "cache has no slot bank / host bank");
+  for (int i = 0; i < n_fill; ++i) {
+    const int e = fill_expert[i], s = fill_slot[i];
+    if (e < 0 || e >= c->dims.n_experts || s < 0 || s >= c->capacity)
+      return fail(EMOE_EINVAL, "fill (%d -> %d) out of range", e, s);
+  }
+  for (int i = 0; i < n_fill; ++i) {
+    const int e = fill_expert[i], s = fill_slot[i];
+    EMOE_HIP(hipStreamWaitEvent(c->copy_stream, c->release[s], 0));
+    EMOE_HIP(hipMemcpyAsync(c->slot_bank + (int64_t)s * c->record_bytes,
+                            c->host_bank + (int64_t)e * c->record_bytes, c->record_bytes,
+                            hipMemcpyHostToDevice, c->copy_stream));
+  }
+  EMOE_HIP(hipEventRecord(c->ready, c->copy_stream));
+  EMOE_HIP(hipStreamWaitEvent(stream, c->ready, 0));
+  return EMOE_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------------------ forward
+namespace {
+
+struct CacheSnapshot {
+  std::vector<int32_t> slot_of, expert_of;
+  std::vector<int64_t> stamp;
+  int64_t clock;
+};
+
+int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t* w_router,
+                     const float* logits_override, int32_t renormalize, int32_t path, uint16_t* y,
+                     void* workspace, size_t ws_bytes, hipStream_t stream, emoe_stats* stats,
+                     bool sequential) {
+  if (!c) return fail(EMOE_EINVAL, "cache is NULL");
+  if (!c->slot_bank) return fail(EMOE_ESTATE, "no slot bank attached");
+  if (!c->resident_all && !c->host_bank)
+    return fail(EMOE_ESTATE, "cache is neither fully resident nor backed by a host bank");
+  const emoe_dims& D = c->dims;
+  if (T < 0) return fail(EMOE_EINVAL, "tokens=%d < 0", T);
+  if (path < EMOE_PATH_AUTO || path > EMOE_PATH_MFMA) return fail(EMOE_EINVAL, "bad path %d", path);
+  emoe_stats ds{};
+  ds.layer_calls = 1;
+  if (T == 0) {
+    add_stats(stats, ds);
+    return EMOE_OK;
+  }
+  if (!h || !y || !workspace) return fail(EMOE_EINVAL, "NULL h, y or workspace");
+  if (!w_router && !logits_override) return fail(EMOE_EINVAL, "need w_router or logits_override");
+  const emoe_ws_layout L = make_layout(D, T);
+  if (ws_bytes < L.total)
+    return fail(EMOE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, L.total);
+  const int E = D.n_experts, k = D.top_k, d = D.d_model, f = D.d_ff;
+  const int P = T * k;
+  if (path == EMOE_PATH_AUTO)
+    path = (P >= EMOE_MFMA_MIN_PAIRS_PER_EXPERT * E) ? EMOE_PATH_MFMA : EMOE_PATH_GEMV;
+
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  float* logits = reinterpret_cast<float*>(ws + L.logits);
+  int32_t* ids = reinterpret_cast<int32_t*>(ws + L.topk_ids);
+  float* wts = reinterpret_cast<float*>(ws + L.topk_w);
+  int32_t* counts = reinterpret_cast<int32_t*>(ws + L.counts);
+  int32_t* offsets = reinterpret_cast<int32_t*>(ws + L.offsets);
+  int32_t* sorted = reinterpret_cast<int32_t*>(ws + L.sorted_pairs);
+  int32_t* active = reinterpret_cast<int32_t*>(ws + L.active);
+  int32_t* n_active = reinterpret_cast<int32_t*>(ws + L.n_active);
+  int32_t* tiles = reinterpret_cast<int32_t*>(ws + L.tile_offsets);
+  uint16_t* act = reinterpret_cast<uint16_t*>(ws + L.act);
+  float* pair_out = reinterpret_cast<float*>(ws + L.pair_out);
+
+  // Route (Eq. 1) and group by expert.
+  const float* z = logits_override ? logits_override : logits;
+  if (!logits_override) {
+    EMOE_LAUNCH(EMOE_K_ROUTER, stream, launch_router_logits(T, E, d, h, w_router, logits, stream));
+    ds.kernel_launches += 1;
+  }
+  EMOE_LAUNCH(EMOE_K_TOPK, stream, launch_topk(T, E, k, renormalize, z, ids, wts, stream));
+  EMOE_LAUNCH(EMOE_K_GROUP, stream,
+              launch_group(P, E, ids, counts, offsets, sorted, active, n_active, tiles, stream));
+  ds.kernel_launches += 2;
+  const GroupView gv{sorted, offsets, active, n_active, tiles};
+
+  auto run_wave = [&](const WaveArg& wa) -> int32_t {
+    if (path == EMOE_PATH_MFMA) {
+      EMOE_LAUNCH(EMOE_K_GATEUP_MFMA, stream,
+                  launch_gateup_mfma(d, f, k, P, E, h, gv, wa, c->slot_bank, c->record_bytes, act, stream));
+      EMOE_LAUNCH(EMOE_K_DOWN_MFMA, stream,
+                  launch_down_mfma(d, f, k, P, E, act, gv, wa, c->slot_bank, c->record_bytes, pair_out, stream));
+    } else {
+      EMOE_LAUNCH(EMOE_K_GATEUP_GEMV, stream,
+                  launch_gateup_gemv(d, f, k, P, E, h, gv, wa, c->slot_bank, c->record_bytes, act, stream));
+      EMOE_LAUNCH(EMOE_K_DOWN_GEMV, stream,
+                  launch_down_gemv(d, f, k, P, E, act, gv, wa, c->slot_bank, c->record_bytes, pair_out, stream));
+    }
+    ds.kernel_launches += 2;
+    return EMOE_OK;
+  };
+
+  int32_t st;
+  if (c->resident_all && !sequential) {
+    // Full residency (Sec. 3.3): identity map, no expert-id transfer.
+    WaveArg wa;
+    wa.n = -1;
+    if ((st = run_wave(wa))) return st;
+    ds.waves = 1;
+    ds.grouped_gemm_calls = 2;
+  } else {
+    // One batched expert-id transfer per layer (Sec. 1), then the waves of Sec. 3.4.
+    EMOE_HIP(hipMemcpyAsync(c->counts_host, counts, sizeof(int32_t) * E, hipMemcpyDeviceToHost, stream));
+    EMOE_HIP(hipStreamSynchronize(stream));
+    std::vector<int32_t> wexp(E), woff(E + 1), smap(E), fexp(E), fslot(E);
+    int32_t n_waves = 0;
+    if ((st = emoe_plan_waves(c, c->counts_host, wexp.data(), woff.data(), &n_waves))) return st;
+    for (int w = 0; w < n_waves; ++w) {
+      const int n = woff[w + 1] - woff[w];
+      const int32_t* we = wexp.data() + woff[w];
+      CacheSnapshot snap{c->slot_of, c->expert_of, c->stamp, c->clock};
+      emoe_stats wstats{};
+      int32_t n_fill = 0;
+      if ((st = emoe_build_slot_map(c, we, n, smap.data(), fexp.data(), fslot.data(), &n_fill, &wstats)))
+        return st;
+      if (!c->resident_all) {
+        st = emoe_fill_slots(c, fexp.data(), fslot.data(), n_fill, stream);
+        if (st) {
+          c->slot_of = snap.slot_of;
+          c->expert_of = snap.expert_of;
+          c->stamp = snap.stamp;
+          c->clock = snap.clock;
+          return st;
+        }
+      }
+      ds.hits += wstats.hits;
+      ds.misses += wstats.misses;
+      ds.h2d_bytes += wstats.h2d_bytes;
+      WaveArg wa;
+      wa.n = n;
+      for (int e = 0; e < E; ++e) wa.slot_of[e] = (int16_t)smap[e];
+      for (int i = 0; i < n; ++i) wa.expert[i] = (int16_t)we[i];
+      if (sequential) {
+        for (int i = 0; i < n; ++i) {
+          WaveArg one;
+          one.n = 1;
+          one.expert[0] = (int16_t)we[i];
+          for (int e = 0; e < E; ++e) one.slot_of[e] = -1;
+          one.slot_of[we[i]] = (int16_t)smap[we[i]];
+          if ((st = run_wave(one))) return st;
+          ds.seq_expert_calls += 1;
+        }
+      } else {
+        if ((st = run_wave(wa))) return st;
+        ds.grouped_gemm_calls += 2;
+      }
+      ds.waves += 1;
+      if (!c->resident_all)
+        for (int i = 0; i < n; ++i) EMOE_HIP(hipEventRecord(c->release[smap[we[i]]], stream));
+    }
+  }
+  EMOE_LAUNCH(EMOE_K_COMBINE, stream, launch_combine(T, d, k, wts, pair_out, y, stream));
+  ds.kernel_launches += 1;
+  add_stats(stats, ds);
+  return EMOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t emoe_moe_forward(emoe_cache* cache, int32_t tokens, const uint16_t* h,
+                         const uint16_t* w_router, const float* logits_override,
+                         int32_t renormalize, int32_t path, uint16_t* y, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream, emoe_stats* stats) {
+  return forward_impl(cache, tokens, h, w_router, logits_override, renormalize, path, y, workspace,
+                      workspace_bytes, stream, stats, false);
+}
+
+int32_t emoe_moe_forward_sequential(emoe_cache* cache, int32_t tokens, const uint16_t* h,
+                                    const uint16_t* w_router, const float* logits_override,
+                                    int32_t renormalize, int32_t path, uint16_t* y,
+                                    void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream, emoe_stats* stats) {
+  return forward_impl(cache, tokens, h, w_router, logits_override, renormalize, path, y, workspace,
+                      workspace_bytes, stream, stats, true);
+}
+
+int32_t emoe_profile_begin(int32_t max_kernels) {
+  if (max_kernels <= 0 || max_kernels > (1 << 20)) return fail(EMOE_EINVAL, "bad max_kernels");
+  Profiler& p = g_prof;
+  if (p.on) return fail(EMOE_ESTATE, "profiling already active on this thread");
+  p.start.assign(max_kernels, nullptr);
+  p.stop.assign(max_kernels, nullptr);
+  p.kind.assign(max_kernels, -1);
+  p.max = max_kernels;
+  p.used = 0;
+  for (int i = 0; i < max_kernels; ++i) {
+    hipError_t e = hipEventCreate(&p.start[i]);
+    if (e == hipSuccess) e = hipEventCreate(&p.stop[i]);
+    if (e != hipSuccess) {
+      for (hipEvent_t ev : p.start) if (ev) (void)hipEventDestroy(ev);
+      for (hipEvent_t ev : p.stop) if (ev) (void)hipEventDestroy(ev);
+      p = Profiler();
+      return hip_fail(e, "hipEventCreate");
+    }
+  }
+  p.on = true;
+  return EMOE_OK;
+}
+
+int32_t emoe_profile_end(int32_t* kinds, float* ms, int32_t max_out, int32_t* n_out) {
+  Profiler& p = g_prof;
+  if (!p.on) return fail(EMOE_ESTATE, "profiling not active on this thread");
+  int32_t st = EMOE_OK;
+  const int n = p.used;
+  for (int i = 0; i < n && st == EMOE_OK; ++i) {
+    hipError_t e = hipEventSynchronize(p.stop[i]);
+    float t = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, p.start[i], p.stop[i]);
+    if (e != hipSuccess) {
+      st = hip_fail(e, "kernel timing events");
+      break;
+    }
+    if (i < max_out) {
+      if (kinds) kinds[i] = p.kind[i];
+      if (ms) ms[i] = t;
+    }
+  }
+  if (n_out) *n_out = n;
+  for (hipEvent_t ev : p.start) (void)hipEventDestroy(ev);
+  for (hipEvent_t ev : p.stop) (void)hipEventDestroy(ev);
+  p = Profiler();
+  return st;
+}
+
+}  // extern "C"

@@ -1,0 +1,160 @@
+// Internal definitions shared by the gfx950 kernels and the host runtime of
+// libexactmoe.so: the packed record layout, the wave descriptor passed to the
+// grouped kernels, small device helpers and the kernel launchers.
+#pragma once
+
+#include <hip/hip_fp16.h>
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "exactmoe.h"
+
+namespace emoe {
+
+constexpr int kGroup = EMOE_GROUP;  // quantization group along K (Sec. 3.2)
+constexpr int kTileRows = 16;       // output rows per packed tile
+constexpr int kTileBytes = 1024;    // codes of one 16 x 128 tile (4 bits each)
+constexpr int kMaxWave = EMOE_MAX_EXPERTS;
+constexpr int kMfmaRows = 64;       // token rows per MFMA row-tile
+
+// ---------------------------------------------------------------------------
+// Packed expert record (our CDNA4 layout; the paper packs its own GPU's format
+// offline once, Sec. 3.2, and keeps the identical bytes in host and GPU
+// memory, Sec. 3.3).
+//
+//   [W13 codes][W13 scales][W2 codes][W2 scales]
+//
+// W13 holds gate and up (each d_ff x d_model) as 2*d_ff rows interleaved per
+// 16-row block: row-block 2b is gate rows 16b..16b+15, row-block 2b+1 is up
+// rows 16b..16b+15, so one workgroup sees matching gate and up outputs.
+// W2 is down (d_model x d_ff).
+//
+// Codes of a matrix with N rows and K inputs: (N/16) x (K/128) tiles of
+// 1024 B, tile (rb, g) at byte (rb*(K/128) + g)*1024.  Inside a tile, lane l
+// of a wavefront owns the 16 bytes at 16*l: output row n = 16*rb + l%16 and
+// the four dwords i = 0..3 hold inputs k = 128*g + 32*i + 8*(l/16) + r,
+// r = 0..7, with r even in bits 4*(r/2)..+3 and r odd in bits 16+4*(r/2)..+3.
+// A 4-bit code is u = q + 8 (offset binary).  One wavefront load of a tile is
+// therefore fully coalesced, each dword expands to four bf16 pairs (k, k+1)
+// that line up with bf16 activations in memory, and the four dwords are the
+// B operands of four v_mfma_f32_16x16x32_bf16 steps.
+// Scales: fp16 [N][K/128] row-major after the codes.
+// ---------------------------------------------------------------------------
+struct RecordLayout {
+  int64_t w13_codes, w13_scales, w2_codes, w2_scales, bytes;
+};
+
+__host__ __device__ inline RecordLayout record_layout(int d, int f) {
+  RecordLayout r;
+  const int64_t fd = (int64_t)f * d;
+  r.w13_codes = 0;
+  r.w13_scales = fd;                   // 2f*d codes at 4 bits
+  r.w2_codes = fd + fd / 32;           // + 2f * (d/128) fp16 scales
+  r.w2_scales = r.w2_codes + fd / 2;   // + d*f codes at 4 bits
+  r.bytes = r.w2_scales + fd / 64;     // + d * (f/128) fp16 scales
+  return r;
+}
+
+// Experts of one wave (Sec. 3.4 step 2).  n < 0: every active expert of the
+// call, resident in the slot of the same index (full residency, Sec. 3.3);
+// the kernels then read the device-side active list.  n >= 0: the wave's
+// experts expert[0..n) and the global-to-slot map slot_of[E], -1 being the
+// inactive sentinel for every expert outside the wave.
+struct WaveArg {
+  int32_t n;
+  int16_t expert[kMaxWave];
+  int16_t slot_of[kMaxWave];
+};
+
+// Device-side views used by the grouped projection kernels.
+struct GroupView {
+  const int32_t* sorted_pairs;  // [P] pair ids grouped by expert
+  const int32_t* offsets;       // [E+1]
+  const int32_t* active;        // [E]
+  const int32_t* n_active;      // [1]
+  const int32_t* tile_offsets;  // [E+1] MFMA row-tile prefix sum (MFMA path)
+};
+
+// ---------------------------------------------------------------------------
+// Device helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;  // NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ float half_bits_to_f32(uint16_t b) {
+  return __half2float(__ushort_as_half(b));
+}
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
+
+// Resolve the wave-local expert index w to (expert, slot); false if unused.
+__device__ __forceinline__ bool resolve_wave_expert(const WaveArg& wave, const GroupView& gv,
+                                                    int w, int& expert, int& slot) {
+  if (wave.n < 0) {
+    if (w >= *gv.n_active) return false;
+    expert = gv.active[w];
+    slot = expert;
+  } else {
+    if (w >= wave.n) return false;
+    expert = wave.expert[w];
+    slot = wave.slot_of[expert];
+  }
+  return true;
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (return the launch status; arguments are validated by the caller)
+// ---------------------------------------------------------------------------
+hipError_t launch_quantize(int d, int f, int n_experts, const uint16_t* w_gate,
+                           const uint16_t* w_up, const uint16_t* w_down, uint8_t* records,
+                           int32_t* range_flag, hipStream_t stream);
+
+hipError_t launch_router_logits(int tokens, int n_experts, int d, const uint16_t* h,
+                                const uint16_t* w_router, float* logits, hipStream_t stream);
+
+hipError_t launch_topk(int tokens, int n_experts, int top_k, int renormalize, const float* logits,
+                       int32_t* topk_ids, float* topk_w, hipStream_t stream);
+
+hipError_t launch_group(int pairs, int n_experts, const int32_t* topk_ids, int32_t* counts,
+                        int32_t* offsets, int32_t* sorted_pairs, int32_t* active,
+                        int32_t* n_active, int32_t* tile_offsets, hipStream_t stream);
+
+// Number of wave-local expert indices a grouped launch must cover.
+inline int grid_experts(const WaveArg& wave, int n_experts, int pairs) {
+  if (wave.n >= 0) return wave.n;
+  return pairs < n_experts ? pairs : n_experts;
+}
+
+hipError_t launch_gateup_gemv(int d, int f, int top_k, int pairs, int n_experts,
+                              const uint16_t* h, const GroupView& gv, const WaveArg& wave,
+                              const uint8_t* slot_bank, int64_t record_bytes, uint16_t* act,
+                              hipStream_t stream);
+
+hipError_t launch_down_gemv(int d, int f, int top_k, int pairs, int n_experts,
+                            const uint16_t* act, const GroupView& gv, const WaveArg& wave,
+                            const uint8_t* slot_bank, int64_t record_bytes, float* pair_out,
+                            hipStream_t stream);
+
+hipError_t launch_gateup_mfma(int d, int f, int top_k, int pairs, int n_experts,
+                              const uint16_t* h, const GroupView& gv, const WaveArg& wave,
+                              const uint8_t* slot_bank, int64_t record_bytes, uint16_t* act,
+                              hipStream_t stream);
+
+hipError_t launch_down_mfma(int d, int f, int top_k, int pairs, int n_experts,
+                            const uint16_t* act, const GroupView& gv, const WaveArg& wave,
+                            const uint8_t* slot_bank, int64_t record_bytes, float* pair_out,
+                            hipStream_t stream);
+
+hipError_t launch_combine(int tokens, int d, int top_k, const float* topk_w,
+                          const float* pair_out, uint16_t* y, hipStream_t stream);
+
+}  // namespace emoe

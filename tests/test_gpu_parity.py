@@ -1,0 +1,316 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Integer results (codes, scales, top-k ids, grouping, slot maps, counters) are
+compared bit for bit; layer outputs within max|err| <= 2e-2 * max|ref|; a
+multi-wave call must equal the single-wave call bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2608_15383_amd import api
+from paper_2608_15383_amd._lib import EMOE_ERANGE, ExactMoEError
+from paper_2608_15383_amd.inputs import (LayerInputs, LayerShape, OLMOE, TINY, bf16_bits_to_f32,
+                                          f32_to_bf16_bits, make_layer, spread_logits)
+from tests._gpu import TOL, Layer, LazyExperts, dev, host_bits, quantize, rel_err
+
+pytestmark = pytest.mark.gpu
+
+GEMV, MFMA = api.EMOE_PATH_GEMV, api.EMOE_PATH_MFMA
+
+
+def dims_of(shape: LayerShape):
+    return api.dims(shape.d_model, shape.d_ff, shape.n_experts, shape.top_k)
+
+
+def oracle_y(lay, experts, k, logits=None, tokens=None, renormalize=True):
+    h = lay.f32("h")
+    r = O.route(h, lay.f32("w_router"), k, renormalize, logits)
+    return O.moe_forward(h, experts, r, tokens=tokens), r
+
+
+def assert_close(y, ref, label=""):
+    mx, mean = rel_err(y, ref)
+    print(f"{label}: max|err|/max|ref| = {mx:.3e}, mean rel = {mean:.3e}", flush=True)
+    assert mx <= TOL, (label, mx)
+
+
+# ------------------------------------------------------------------ quantization
+def _check_codes(dm, lay, bank, experts):
+    rec_bytes = api.expert_record_bytes(dm)
+    host = bank.cpu().numpy()
+    for i, e in enumerate(experts):
+        got = api.unpack_expert(dm, host[i * rec_bytes:(i + 1) * rec_bytes])
+        for name, w in (("gate", lay.w_gate[e]), ("up", lay.w_up[e]), ("down", lay.w_down[e])):
+            q, s = O.quantize_matrix(bf16_bits_to_f32(w))
+            assert np.array_equal(got["q_" + name], q), (e, name)
+            assert np.array_equal(got["s_" + name], s.view(np.uint16)), (e, name)
+
+
+def test_quantize_bit_exact_with_special_groups():
+    dm = dims_of(TINY)
+    lay = make_layer(TINY, 4, seed=0)
+    g = bf16_bits_to_f32(lay.w_gate).copy()
+    g[0, 0, :128] = 0.0                                   # zero group
+    g[0, 1, :128] = 0.0
+    g[0, 1, 77] = -0.3125                                 # single nonzero
+    g[0, 2, :128] = 0.0
+    g[0, 2, :15] = [2.0 ** -7 * j for j in range(-7, 8)]  # ramp
+    g[0, 3, :128] = 0.0
+    g[0, 3, 0] = 7 * 2 ** -6                              # half-way quotients
+    g[0, 3, 1:8] = [(2 * m + 1) / 2 * 2 ** -6 for m in range(7)]
+    g[1, 0, :128] = 0.0
+    g[1, 0, 5] = 2.0 ** -126                              # scale underflows FP16
+    g[1, 1, :128] *= 1e-4                                 # subnormal FP16 scales
+    lay.w_gate = f32_to_bf16_bits(g)
+    bank = quantize(dm, lay)
+    _check_codes(dm, lay, bank, range(TINY.n_experts))
+
+
+def test_quantize_bit_exact_olmoe_shape():
+    lay = make_layer(OLMOE, 1, seed=5, n_experts_drawn=2)
+    dm = dims_of(OLMOE)
+    bank = quantize(dm, lay)
+    _check_codes(dm, lay, bank, [0, 1])
+
+
+def test_quantize_scale_overflow_is_an_error():
+    lay = make_layer(TINY, 1, seed=0, n_experts_drawn=1)
+    w = bf16_bits_to_f32(lay.w_down).copy()
+    w[0, 3, 7] = 1.0e6
+    lay.w_down = f32_to_bf16_bits(w)
+    with pytest.raises(ExactMoEError) as ei:
+        quantize(dims_of(TINY), lay)
+    assert ei.value.status == EMOE_ERANGE
+
+
+# ------------------------------------------------------------------ routing
+def _route(dm, h_bits, wr_bits, logits=None, renormalize=True):
+    t, e, k = h_bits.shape[0], dm.n_experts, dm.top_k
+    i32 = dict(dtype=torch.int32, device="cuda:0")
+    out = dict(logits=torch.zeros((max(t, 1), e), dtype=torch.float32, device="cuda:0"),
+               ids=torch.zeros(max(t * k, 1), **i32), w=torch.zeros(max(t * k, 1), dtype=torch.float32,
+                                                                    device="cuda:0"),
+               counts=torch.zeros(e, **i32), offsets=torch.zeros(e + 1, **i32),
+               sorted=torch.zeros(max(t * k, 1), **i32), active=torch.zeros(e, **i32),
+               n_active=torch.zeros(1, **i32))
+    lo = None if logits is None else dev(np.asarray(logits, np.float32))
+    api.route(dm, t, dev(h_bits), dev(wr_bits), lo, renormalize, out["logits"], out["ids"],
+              out["w"], out["counts"], out["offsets"], out["sorted"], out["active"], out["n_active"])
+    torch.cuda.synchronize()
+    return {k_: v.cpu().numpy() for k_, v in out.items()}
+
+
+def _check_route(dm, got, h, wr, logits=None, renormalize=True):
+    t, k = h.shape[0], dm.top_k
+    r = O.route(bf16_bits_to_f32(h), bf16_bits_to_f32(wr), k, renormalize, logits)
+    if logits is None:
+        assert np.array_equal(got["logits"][:t].view(np.uint32), r.logits.view(np.uint32))
+    assert np.array_equal(got["ids"][:t * k].reshape(t, k), r.ids)
+    ulp = np.abs(got["w"][:t * k].view(np.int32).astype(np.int64)
+                 - r.weights.reshape(-1).view(np.int32).astype(np.int64))
+    assert ulp.max(initial=0) <= 4
+    gr = O.group_by_expert(r.ids, dm.n_experts)
+    assert np.array_equal(got["counts"], gr.counts)
+    assert np.array_equal(got["offsets"], gr.offsets)
+    assert np.array_equal(got["sorted"][:t * k], gr.sorted_pairs)
+    assert got["n_active"][0] == len(gr.active)
+    assert np.array_equal(got["active"][:len(gr.active)], gr.active)
+
+
+@pytest.mark.parametrize("shape,tokens", [(TINY, 16), (OLMOE, 1), (OLMOE, 16), (OLMOE, 2048),
+                                          (LayerShape(384, 128, 200, 6), 37)])
+def test_route_and_grouping_bit_exact(shape, tokens):
+    lay = make_layer(shape, tokens, seed=7, n_experts_drawn=0)
+    dm = dims_of(shape)
+    got = _route(dm, lay.h, lay.w_router)
+    _check_route(dm, got, lay.h, lay.w_router)
+
+
+def test_route_override_ties_and_no_renormalize():
+    dm = api.dims(256, 128, 16, 4)
+    rng = np.random.default_rng(3)
+    z = rng.integers(-2, 3, size=(50, 16)).astype(np.float32)   # many exact ties
+    z[3] = -0.0
+    z[4, ::2] = 0.0
+    lay = make_layer(LayerShape(256, 128, 16, 4), 50, seed=3, n_experts_drawn=0)
+    for renorm in (True, False):
+        got = _route(dm, lay.h, lay.w_router, logits=z, renormalize=renorm)
+        _check_route(dm, got, lay.h, lay.w_router, logits=z, renormalize=renorm)
+
+
+def test_route_zero_tokens():
+    dm = dims_of(TINY)
+    lay = make_layer(TINY, 0, seed=1, n_experts_drawn=0)
+    got = _route(dm, lay.h, lay.w_router)
+    assert got["counts"].sum() == 0 and got["n_active"][0] == 0 and np.all(got["offsets"] == 0)
+
+
+# ------------------------------------------------------------------ layer, small shapes
+@pytest.mark.parametrize("path", [GEMV, MFMA])
+def test_forward_tiny_config(path):
+    lay = make_layer(TINY, 16, seed=0)
+    layer = Layer(dims_of(TINY), lay, 16)
+    y = layer.forward(lay.h, path=path)
+    ref, r = oracle_y(lay, LazyExperts(lay), TINY.top_k)
+    assert_close(y, ref, f"tiny path={path}")
+    po = layer.ws_array("pair_out", 16 * 2 * 256, np.float32).reshape(32, 256)
+    assert_close(po, O.pair_outputs(lay.f32("h"), LazyExperts(lay), r, range(32)), "tiny pairs")
+
+
+@pytest.mark.parametrize("shape,tokens", [(LayerShape(384, 256, 6, 3), 7),
+                                          (LayerShape(256, 384, 1, 1), 5),
+                                          (LayerShape(128, 128, 4, 4), 9),
+                                          (LayerShape(640, 128, 12, 2), 70)])
+@pytest.mark.parametrize("path", [GEMV, MFMA])
+def test_forward_ragged_and_degenerate_shapes(shape, tokens, path):
+    lay = make_layer(shape, tokens, seed=11)
+    layer = Layer(dims_of(shape), lay, tokens)
+    y = layer.forward(lay.h, path=path)
+    ref, _ = oracle_y(lay, LazyExperts(lay), shape.top_k)
+    assert_close(y, ref, f"{shape} T={tokens} path={path}")
+
+
+@pytest.mark.parametrize("path", [GEMV, MFMA])
+def test_token_group_sizes_1_to_128(path):
+    """Token-group sizes 1..128 routed to one expert (the paper's kernel-test range)."""
+    shape = LayerShape(256, 256, 4, 1)
+    lay = make_layer(shape, 128, seed=13)
+    layer = Layer(dims_of(shape), lay, 128)
+    experts = LazyExperts(lay)
+    for m in (1, 2, 3, 15, 16, 17, 63, 64, 65, 127, 128):
+        z = np.zeros((128, 4), np.float32)
+        z[:, 0] = 1.0
+        z[:m, 0] = 0.0
+        z[:m, 2] = 1.0                    # the first m tokens go to expert 2
+        y = layer.forward(lay.h, logits=z, path=path)
+        ref, _ = oracle_y(lay, experts, 1, logits=z)
+        assert_close(y, ref, f"group size {m} path={path}")
+
+
+def test_zero_tokens_forward():
+    lay = make_layer(TINY, 0, seed=0)
+    layer = Layer(dims_of(TINY), lay, 1)
+    st = api.Stats()
+    h = torch.zeros((0, 256), dtype=torch.int16, device="cuda:0")
+    api.moe_forward(layer.cache, h, layer.wr, torch.empty_like(h), layer.ws, stats=st)
+    assert st.layer_calls == 1 and st.kernel_launches == 0
+
+
+# ------------------------------------------------------------------ OLMoE shapes
+@pytest.fixture(scope="module")
+def olmoe():
+    lay = make_layer(OLMOE, 2048, seed=3)
+    layer = Layer(dims_of(OLMOE), lay, 2048)
+    return lay, layer, LazyExperts(lay)
+
+
+def _sub(lay, tokens):
+    return LayerInputs(lay.shape, lay.w_gate, lay.w_up, lay.w_down, lay.w_router, lay.h[:tokens])
+
+
+def test_decode_token_full_size(olmoe):
+    lay, layer, experts = olmoe
+    for t in (0, 1, 2):
+        one = _sub(lay, 2048)
+        one.h = lay.h[t:t + 1]
+        y = layer.forward(one.h)
+        ref, _ = oracle_y(one, experts, 8)
+        assert_close(y, ref, f"decode token {t}")
+
+
+def _host_bank(layer):
+    host = torch.empty(layer.bank.numel(), dtype=torch.uint8, pin_memory=True)
+    host.copy_(layer.bank)
+    torch.cuda.synchronize()
+    return host
+
+
+@pytest.mark.parametrize("distinct", [40, 48, 64])
+def test_multi_wave_equals_single_wave(olmoe, distinct):
+    """16 tokens touching `distinct` experts through a 16-slot cache (3-4 waves)."""
+    lay, layer, experts = olmoe
+    dm = layer.dm
+    sub = _sub(lay, 16)
+    z = spread_logits(16, 64, 8, distinct, seed=2)
+    y1 = layer.forward(sub.h, logits=z)
+    po1 = layer.ws_array("pair_out", 128 * 2048, np.float32)
+
+    host = _host_bank(layer)
+    slots = torch.zeros(16 * api.expert_record_bytes(dm), dtype=torch.uint8, device="cuda:0")
+    cache = api.Cache(dm, 16, slot_bank=slots, host_bank=host)
+    ref_cache = O.SlotCache(64, 16, api.expert_record_bytes(dm))
+    for call in range(2):   # cold, then warm with the same active set
+        st = api.Stats()
+        y = layer.forward(sub.h, logits=z, cache=cache, stats=st)
+        assert np.array_equal(y, y1)
+        assert np.array_equal(layer.ws_array("pair_out", 128 * 2048, np.float32), po1)
+        ids = O.topk_experts(z, 8)
+        active = O.group_by_expert(ids, 64).active
+        waves = O.plan_waves(active, ref_cache.resident(), 16)
+        h0, m0 = ref_cache.hits, ref_cache.misses
+        for w in waves:
+            ref_cache.map_wave(w)
+        assert st.waves == len(waves) == -(-distinct // 16)
+        assert (st.hits, st.misses) == (ref_cache.hits - h0, ref_cache.misses - m0)
+        assert st.h2d_bytes == st.misses * api.expert_record_bytes(dm)
+        assert st.grouped_gemm_calls == 2 * len(waves)
+        so, eo, _ = cache.state()
+        assert so.tolist() == ref_cache.slot_of and eo.tolist() == ref_cache.expert_of
+    ys = layer.forward(sub.h, logits=z, cache=cache, sequential=True)
+    assert np.array_equal(ys, y1)
+    ref, _ = oracle_y(sub, experts, 8, logits=z)
+    assert_close(y1, ref, f"16 tokens, {distinct} experts")
+    cache.close()
+
+
+def test_global_to_slot_map_permutation(olmoe):
+    """Experts placed in permuted slots give the identical output (map preflight)."""
+    lay, layer, _ = olmoe
+    dm = layer.dm
+    sub = _sub(lay, 16)
+    y_res = layer.forward(sub.h)
+    host = _host_bank(layer)
+    slots = torch.zeros(64 * api.expert_record_bytes(dm), dtype=torch.uint8, device="cuda:0")
+    cache = api.Cache(dm, 64, slot_bank=slots, host_bank=host)
+    order = np.random.default_rng(0).permutation(64)
+    for chunk in np.array_split(order, 8):   # warm the slots in a scrambled order
+        sm, fills = cache.build_slot_map(sorted(chunk.tolist()))
+        cache.fill_slots(fills)
+    torch.cuda.synchronize()
+    so, _, _ = cache.state()
+    assert sorted(so.tolist()) == list(range(64)) and so.tolist() != list(range(64))
+    y = layer.forward(sub.h, cache=cache)
+    assert np.array_equal(y, y_res)
+    cache.close()
+
+
+def test_prefill_full_size_sampled(olmoe):
+    lay, layer, experts = olmoe
+    y = layer.forward(lay.h)                       # AUTO -> MFMA at 16,384 pairs
+    r = O.route(lay.f32("h"), lay.f32("w_router"), 8)
+    gr = O.group_by_expert(r.ids, 64)
+    assert np.array_equal(layer.ws_array("counts", 64, np.int32), gr.counts)
+    assert np.array_equal(layer.ws_array("sorted_pairs", 16384, np.int32), gr.sorted_pairs)
+    po = layer.ws_array("pair_out", 16384 * 2048, np.float32).reshape(16384, 2048)
+    for e in (int(gr.active[0]), int(gr.active[31]), int(gr.active[-1])):
+        seg = gr.sorted_pairs[gr.offsets[e]:gr.offsets[e + 1]]
+        pick = np.concatenate([seg[:3], seg[63:66], seg[-3:]])  # head, tile edge, ragged tail
+        assert_close(po[pick], O.pair_outputs(lay.f32("h"), experts, r, pick), f"prefill expert {e}")
+    toks = [0, 1000, 2047]
+    ref = O.moe_forward(lay.f32("h"), experts, r, tokens=toks)
+    assert_close(y[toks], ref, "prefill tokens")
+    experts.cache.clear()
+
+
+def test_prefill_paths_agree(olmoe):
+    lay, layer, experts = olmoe
+    sub = _sub(lay, 256)
+    y_g = layer.forward(sub.h, path=GEMV)
+    y_m = layer.forward(sub.h, path=MFMA)
+    ref, _ = oracle_y(sub, experts, 8, tokens=[0, 128, 255])
+    assert_close(y_g[[0, 128, 255]], ref, "256 tokens GEMV")
+    assert_close(y_m[[0, 128, 255]], ref, "256 tokens MFMA")
+    assert_close(y_m, y_g.astype(np.float64), "MFMA vs GEMV")
+    experts.cache.clear()
