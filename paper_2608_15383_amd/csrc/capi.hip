@@ -14,6 +14,13 @@
 
 using namespace emoe;
 
+namespace emoe {
+namespace {
+thread_local LaunchEvents t_launch_events;
+}
+LaunchEvents& launch_events() { return t_launch_events; }
+}  // namespace emoe
+
 // ------------------------------------------------------------------ errors
 namespace {
 
@@ -49,17 +56,22 @@ struct Profiler {
 };
 thread_local Profiler g_prof;
 
+// Run one launcher; while profiling, its kernel records the next event pair at
+// dispatch.  Launchers that launch nothing (empty inputs) record nothing.
 hipError_t timed_launch(int32_t kind, hipStream_t stream, hipError_t (*fn)(void*), void* ctx) {
+  (void)stream;
   Profiler& p = g_prof;
+  LaunchEvents& le = launch_events();
   const bool rec = p.on && p.used < p.max;
+  le = LaunchEvents();
   if (rec) {
-    hipError_t e = hipEventRecord(p.start[p.used], stream);
-    if (e != hipSuccess) return e;
+    le.start = p.start[p.used];
+    le.stop = p.stop[p.used];
   }
   hipError_t e = fn(ctx);
-  if (e != hipSuccess || !rec) return e;
-  e = hipEventRecord(p.stop[p.used], stream);
-  p.kind[p.used++] = kind;
+  const bool launched = le.used;
+  le = LaunchEvents();
+  if (e == hipSuccess && rec && launched) p.kind[p.used++] = kind;
   return e;
 }
 

@@ -4,6 +4,7 @@
 #pragma once
 
 #include <hip/hip_fp16.h>
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -109,6 +110,25 @@ __device__ __forceinline__ bool resolve_wave_expert(const WaveArg& wave, const G
     slot = wave.slot_of[expert];
   }
   return true;
+}
+
+// ---------------------------------------------------------------------------
+// Kernel launch.  While the C ABI's profiler is on, the next launch records a
+// start/stop event pair at dispatch (hipExtLaunchKernelGGL), which times the
+// kernel itself rather than the stream around it.
+// ---------------------------------------------------------------------------
+struct LaunchEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+  bool used = false;
+};
+LaunchEvents& launch_events();  // per host thread
+
+template <typename Kernel, typename... Args>
+inline void launch(Kernel kernel, dim3 grid, dim3 block, hipStream_t stream, Args... args) {
+  LaunchEvents& ev = launch_events();
+  hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, ev.start, ev.stop, 0, args...);
+  ev.used = true;
 }
 
 // ---------------------------------------------------------------------------

@@ -204,7 +204,7 @@ hipError_t launch_gateup_mfma(int d, int f, int top_k, int pairs, int n_experts,
   if (pairs == 0) return hipSuccess;
   // Column tile: 4 wavefronts x 2 (gate, up) pairs x 16 outputs = 128 act columns.
   dim3 grid(f / 128, max_row_tiles(pairs, n_experts));
-  hipLaunchKernelGGL(grouped_mfma_kernel<true>, grid, dim3(64 * kWaves), 0, stream, d, f, top_k,
+  launch(grouped_mfma_kernel<true>, grid, dim3(64 * kWaves), stream, d, f, top_k,
                      n_experts, h, gv, wave, slot_bank, record_bytes, act, (float*)nullptr);
   return hipGetLastError();
 }
@@ -216,7 +216,7 @@ hipError_t launch_down_mfma(int d, int f, int top_k, int pairs, int n_experts,
   if (pairs == 0) return hipSuccess;
   // Column tile: 4 wavefronts x 2 row blocks x 16 outputs = 128 output columns.
   dim3 grid(d / 128, max_row_tiles(pairs, n_experts));
-  hipLaunchKernelGGL(grouped_mfma_kernel<false>, grid, dim3(64 * kWaves), 0, stream, d, f, top_k,
+  launch(grouped_mfma_kernel<false>, grid, dim3(64 * kWaves), stream, d, f, top_k,
                      n_experts, act, gv, wave, slot_bank, record_bytes, (uint16_t*)nullptr,
                      pair_out);
   return hipGetLastError();

@@ -269,7 +269,7 @@ hipError_t launch_gateup_gemv(int d, int f, int top_k, int pairs, int n_experts,
   const int ge = grid_experts(wave, n_experts, pairs);
   if (ge == 0) return hipSuccess;
   dim3 grid(f / kTileRows, ge);
-  hipLaunchKernelGGL(gateup_gemv_kernel, grid, dim3(64 * kWaves), 0, stream, d, f, top_k, h, gv,
+  launch(gateup_gemv_kernel, grid, dim3(64 * kWaves), stream, d, f, top_k, h, gv,
                      wave, slot_bank, record_bytes, act);
   return hipGetLastError();
 }
@@ -281,7 +281,7 @@ hipError_t launch_down_gemv(int d, int f, int top_k, int pairs, int n_experts,
   const int ge = grid_experts(wave, n_experts, pairs);
   if (ge == 0) return hipSuccess;
   dim3 grid(d / (kTileRows * kWaves), ge);
-  hipLaunchKernelGGL(down_gemv_kernel, grid, dim3(64 * kWaves), 0, stream, d, f, top_k, act, gv,
+  launch(down_gemv_kernel, grid, dim3(64 * kWaves), stream, d, f, top_k, act, gv,
                      wave, slot_bank, record_bytes, pair_out);
   return hipGetLastError();
 }
@@ -290,8 +290,8 @@ hipError_t launch_combine(int tokens, int d, int top_k, const float* topk_w,
                           const float* pair_out, uint16_t* y, hipStream_t stream) {
   const int64_t n = (int64_t)tokens * (d / 4);
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(combine_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream,
-                     tokens, d, top_k, topk_w, pair_out, y);
+  launch(combine_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), stream, tokens, d, top_k,
+         topk_w, pair_out, y);
   return hipGetLastError();
 }
 

@@ -111,7 +111,7 @@ hipError_t launch_quantize(int d, int f, int n_experts, const uint16_t* w_gate,
   const int tiles = tiles_w13 + tiles_w2;
   const int64_t rec = record_layout(d, f).bytes;
   dim3 grid((tiles + kWavesPerBlock - 1) / kWavesPerBlock, n_experts);
-  hipLaunchKernelGGL(quantize_kernel, grid, dim3(64 * kWavesPerBlock), 0, stream, d, f, tiles_w13,
+  launch(quantize_kernel, grid, dim3(64 * kWavesPerBlock), stream, d, f, tiles_w13,
                      tiles, w_gate, w_up, w_down, records, rec, range_flag);
   return hipGetLastError();
 }

@@ -295,7 +295,7 @@ hipError_t launch_router_logits(int tokens, int n_experts, int d, const uint16_t
                                 const uint16_t* w_router, float* logits, hipStream_t stream) {
   if (tokens == 0) return hipSuccess;
   dim3 grid((tokens + kTokW - 1) / kTokW, (n_experts + 4 * kExpW - 1) / (4 * kExpW));
-  hipLaunchKernelGGL(router_logits_kernel, grid, dim3(256), 0, stream, tokens, n_experts, d, h,
+  launch(router_logits_kernel, grid, dim3(256), stream, tokens, n_experts, d, h,
                      w_router, logits);
   return hipGetLastError();
 }
@@ -303,7 +303,7 @@ hipError_t launch_router_logits(int tokens, int n_experts, int d, const uint16_t
 hipError_t launch_topk(int tokens, int n_experts, int top_k, int renormalize, const float* logits,
                        int32_t* topk_ids, float* topk_w, hipStream_t stream) {
   if (tokens == 0) return hipSuccess;
-  hipLaunchKernelGGL(topk_kernel, dim3((tokens + 3) / 4), dim3(256), 0, stream, tokens, n_experts,
+  launch(topk_kernel, dim3((tokens + 3) / 4), dim3(256), stream, tokens, n_experts,
                      top_k, renormalize, logits, topk_ids, topk_w);
   return hipGetLastError();
 }
@@ -311,7 +311,7 @@ hipError_t launch_topk(int tokens, int n_experts, int top_k, int renormalize, co
 hipError_t launch_group(int pairs, int n_experts, const int32_t* topk_ids, int32_t* counts,
                         int32_t* offsets, int32_t* sorted_pairs, int32_t* active,
                         int32_t* n_active, int32_t* tile_offsets, hipStream_t stream) {
-  hipLaunchKernelGGL(group_kernel, dim3(1), dim3(kGroupThreads), 0, stream, pairs, n_experts,
+  launch(group_kernel, dim3(1), dim3(kGroupThreads), stream, pairs, n_experts,
                      topk_ids, counts, offsets, sorted_pairs, active, n_active, tile_offsets);
   return hipGetLastError();
 }
