@@ -88,6 +88,7 @@ typedef struct emoe_ws_layout {
   size_t active;        /* i32   [E]      active experts, ascending */
   size_t n_active;      /* i32   [1]      number of active experts */
   size_t tile_offsets;  /* i32   [E+1]    MFMA row-tile prefix sum */
+  size_t pair_pos;      /* i32   [T*k]    grouped position of each pair id (fused decode) */
   size_t act;           /* bf16  [T*k][d_ff]    phi(g)*u per pair, grouped order */
   size_t pair_out;      /* f32   [T*k][d_model] expert output per pair id */
   size_t total;         /* bytes needed */
@@ -179,6 +180,11 @@ int32_t emoe_cache_preload_all(emoe_cache* cache, hipStream_t stream);
 int32_t emoe_cache_state(const emoe_cache* cache, int32_t* slot_of_expert,
                          int32_t* expert_of_slot, int64_t* stamp_of_slot);
 
+/* Number of bounded device-side waits of the fused decode launch that gave
+ * up (0 in correct operation; a nonzero value means results of some call
+ * are invalid).  Blocking: reads device memory after the device is idle. */
+int32_t emoe_cache_sync_timeouts(const emoe_cache* cache, int64_t* timeouts);
+
 /* Sec. 3.4: split the active set into waves of at most C experts.
  * counts: host [E].  Order: experts resident now (ascending id), then the
  * others (ascending id), cut into chunks of C.  Outputs (host):
@@ -218,7 +224,11 @@ int32_t emoe_fill_slots(emoe_cache* cache, const int32_t* fill_expert, const int
  * With a fully resident cache (C = E after preload) the call never blocks the
  * host.  Otherwise it copies counts[E] to the host once (one batched expert-id
  * transfer) and synchronizes `stream` to plan the waves.  If a fill fails the
- * cache map is restored to its state before that wave. */
+ * cache map is restored to its state before that wave.
+ * With full residency, the GEMV path and at most 4 tokens (and 32 pairs) the
+ * whole layer runs as one fused kernel launch with the same arithmetic (and
+ * bit-identical results).  Calls on one cache must not overlap in time (use
+ * one stream, or order the streams): the cache holds that launch's counters. */
 int32_t emoe_moe_forward(emoe_cache* cache, int32_t tokens, const uint16_t* h,
                          const uint16_t* w_router, const float* logits_override,
                          int32_t renormalize, int32_t path, uint16_t* y, void* workspace,
@@ -238,7 +248,8 @@ int32_t emoe_moe_forward_sequential(emoe_cache* cache, int32_t tokens, const uin
 /* Kernels launched by the layer calls, as reported by emoe_profile_end. */
 enum emoe_kernel {
   EMOE_K_ROUTER = 0, EMOE_K_TOPK = 1, EMOE_K_GROUP = 2, EMOE_K_GATEUP_GEMV = 3,
-  EMOE_K_DOWN_GEMV = 4, EMOE_K_GATEUP_MFMA = 5, EMOE_K_DOWN_MFMA = 6, EMOE_K_COMBINE = 7
+  EMOE_K_DOWN_GEMV = 4, EMOE_K_GATEUP_MFMA = 5, EMOE_K_DOWN_MFMA = 6, EMOE_K_COMBINE = 7,
+  EMOE_K_DECODE_FUSED = 8
 };
 /* Start recording a HIP event pair around each kernel that emoe_route,
  * emoe_moe_forward and emoe_moe_forward_sequential launch from this thread,

@@ -36,7 +36,7 @@ class Stats(C.Structure):
 class WsLayout(C.Structure):
     _fields_ = [(n, C.c_size_t) for n in ("logits", "topk_ids", "topk_w", "counts", "offsets",
                                           "sorted_pairs", "active", "n_active", "tile_offsets",
-                                          "act", "pair_out", "total")]
+                                          "pair_pos", "act", "pair_out", "total")]
 
 
 _vp = C.c_void_p
@@ -62,6 +62,7 @@ SIGNATURES = {
     "emoe_cache_destroy": (_i32, [_vp]),
     "emoe_cache_preload_all": (_i32, [_vp, _vp]),
     "emoe_cache_state": (_i32, [_vp, _vp, _vp, _vp]),
+    "emoe_cache_sync_timeouts": (_i32, [_vp, _i64p]),
     "emoe_plan_waves": (_i32, [_vp, _vp, _vp, _vp, _i32p]),
     "emoe_build_slot_map": (_i32, [_vp, _vp, _i32, _vp, _vp, _vp, _i32p, C.POINTER(Stats)]),
     "emoe_fill_slots": (_i32, [_vp, _vp, _vp, _i32, _vp]),
@@ -74,7 +75,7 @@ SIGNATURES = {
 }
 
 KERNEL_NAMES = ["router", "topk", "group", "gateup_gemv", "down_gemv", "gateup_mfma", "down_mfma",
-                "combine"]
+                "combine", "decode_fused"]
 
 _lib = None
 

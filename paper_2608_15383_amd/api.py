@@ -122,6 +122,12 @@ class Cache:
         check(lib().emoe_cache_state(self.handle, so.ctypes.data, eo.ctypes.data, st.ctypes.data))
         return so, eo, st
 
+    def sync_timeouts(self) -> int:
+        """emoe_cache_sync_timeouts: bounded device waits that gave up (0 when healthy)."""
+        n = C.c_int64()
+        check(lib().emoe_cache_sync_timeouts(self.handle, C.byref(n)))
+        return n.value
+
     def plan_waves(self, counts) -> list[list[int]]:
         e = self.dims.n_experts
         cnt = np.ascontiguousarray(counts, np.int32)

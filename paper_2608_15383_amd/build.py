@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libexactmoe.so")
-SOURCES = ["capi.hip", "quantize.hip", "route.hip", "gemv.hip", "gemm.hip"]
+SOURCES = ["capi.hip", "quantize.hip", "route.hip", "gemv.hip", "gemm.hip", "decode.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "common.h"
+#include "decode.h"
 
 using namespace emoe;
 
@@ -105,6 +106,8 @@ struct emoe_cache {
   std::vector<hipEvent_t> release;  // [C] completion of the last wave using the slot
   hipEvent_t ready = nullptr;       // completion of the last batch of fills
   int32_t* counts_host = nullptr;   // pinned [E]: the batched expert-id transfer
+  DecodeSync* sync = nullptr;       // device: counters of the fused decode launches
+  DecodeProgress prog;              // host: totals that set each fused launch's targets
 };
 
 namespace {
@@ -139,6 +142,7 @@ emoe_ws_layout make_layout(const emoe_dims& d, int32_t T) {
   L.active = take(E * 4);
   L.n_active = take(4);
   L.tile_offsets = take((E + 1) * 4);
+  L.pair_pos = take(P * 4);
   L.act = take(P * (size_t)d.d_ff * 2);
   L.pair_out = take(P * (size_t)d.d_model * 4);
   L.total = off;
@@ -396,6 +400,8 @@ int32_t emoe_cache_create(const emoe_dims* dims, int32_t capacity, void* slot_ba
     hipError_t e = hipGetDevice(&c->device);
     if (e == hipSuccess) e = hipHostMalloc(reinterpret_cast<void**>(&c->counts_host),
                                            sizeof(int32_t) * dims->n_experts, hipHostMallocDefault);
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&c->sync), sizeof(DecodeSync));
+    if (e == hipSuccess) e = hipMemset(c->sync, 0, sizeof(DecodeSync));
     if (e == hipSuccess && host_bank) {
       e = hipStreamCreateWithFlags(&c->copy_stream, hipStreamNonBlocking);
       if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ready, hipEventDisableTiming);
@@ -420,7 +426,19 @@ int32_t emoe_cache_destroy(emoe_cache* c) {
   if (c->ready) (void)hipEventDestroy(c->ready);
   if (c->copy_stream) (void)hipStreamDestroy(c->copy_stream);
   if (c->counts_host) (void)hipHostFree(c->counts_host);
+  if (c->sync) (void)hipFree(c->sync);
   delete c;
+  return EMOE_OK;
+}
+
+int32_t emoe_cache_sync_timeouts(const emoe_cache* c, int64_t* timeouts) {
+  if (!c || !timeouts) return fail(EMOE_EINVAL, "NULL argument");
+  *timeouts = 0;
+  if (!c->sync) return EMOE_OK;
+  EMOE_HIP(hipDeviceSynchronize());
+  DecodeSync s;
+  EMOE_HIP(hipMemcpy(&s, c->sync, sizeof s, hipMemcpyDeviceToHost));
+  *timeouts = s.timeouts;
   return EMOE_OK;
 }
 
@@ -597,6 +615,44 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
   int32_t* tiles = reinterpret_cast<int32_t*>(ws + L.tile_offsets);
   uint16_t* act = reinterpret_cast<uint16_t*>(ws + L.act);
   float* pair_out = reinterpret_cast<float*>(ws + L.pair_out);
+
+  int32_t* pair_pos = reinterpret_cast<int32_t*>(ws + L.pair_pos);
+  DecodeArgs a{};
+  if (c->resident_all && !sequential && path == EMOE_PATH_GEMV && c->sync) {
+    a.tokens = T;
+    a.d = d;
+    a.f = f;
+    a.n_experts = E;
+    a.top_k = k;
+    a.renormalize = renormalize ? 1 : 0;
+    a.h = h;
+    a.w_router = w_router;
+    a.logits_override = logits_override;
+    a.slot_bank = c->slot_bank;
+    a.record_bytes = c->record_bytes;
+    a.logits = logits;
+    a.topk_ids = ids;
+    a.topk_w = wts;
+    a.counts = counts;
+    a.offsets = offsets;
+    a.sorted_pairs = sorted;
+    a.active = active;
+    a.n_active = n_active;
+    a.pair_pos = pair_pos;
+    a.act = act;
+    a.pair_out = pair_out;
+    a.y = y;
+    a.sync = c->sync;
+  }
+  if (a.sync && decode_fused_plan(a)) {
+    // Few tokens, every expert resident: the whole layer in one launch.
+    EMOE_LAUNCH(EMOE_K_DECODE_FUSED, stream, launch_decode_fused(a, c->prog, stream));
+    ds.kernel_launches = 1;
+    ds.waves = 1;
+    ds.grouped_gemm_calls = 2;
+    add_stats(stats, ds);
+    return EMOE_OK;
+  }
 
   // Route (Eq. 1) and group by expert.
   const float* z = logits_override ? logits_override : logits;

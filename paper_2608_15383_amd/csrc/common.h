@@ -97,6 +97,62 @@ __device__ __forceinline__ float half_bits_to_f32(uint16_t b) {
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63); }
 
+// ---------------------------------------------------------------------------
+// Device-coherent access.  Inside the fused decode launch, workgroups on
+// different XCDs exchange data; the per-XCD L2 caches are not coherent with
+// each other, and cache-wide writeback / invalidate fences cost microseconds
+// per workgroup.  Data crossing workgroups is therefore written and read with
+// device-coherent accesses (sc1) instead, and ordered with an explicit wait
+// for outstanding memory operations.  kCo = false gives ordinary accesses.
+// ---------------------------------------------------------------------------
+template <bool kCo>
+__device__ __forceinline__ void st_u32(void* p, uint32_t v) {
+  if (kCo) __hip_atomic_store(static_cast<uint32_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  else *static_cast<uint32_t*>(p) = v;
+}
+
+template <bool kCo>
+__device__ __forceinline__ uint32_t ld_u32(const void* p) {
+  if (kCo) return __hip_atomic_load(static_cast<const uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return *static_cast<const uint32_t*>(p);
+}
+
+template <bool kCo>
+__device__ __forceinline__ int32_t ld_i32(const int32_t* p) { return (int32_t)ld_u32<kCo>(p); }
+
+template <bool kCo>
+__device__ __forceinline__ float ld_f32(const float* p) { return __uint_as_float(ld_u32<kCo>(p)); }
+
+// 16-byte loads from one buffer (base pointer uniform across the wavefront).
+// The coherent form is a raw buffer load with the sc1 cache policy.
+template <bool kCo>
+struct Buf128 {
+  const uint8_t* base;
+  __amdgpu_buffer_rsrc_t rsrc;
+  __device__ __forceinline__ Buf128(const void* b, uint32_t bytes)
+      : base(static_cast<const uint8_t*>(b)) {
+    if (kCo) rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(b), (short)0, (int)bytes,
+                                                      0x00020000);
+  }
+  __device__ __forceinline__ uint4 load(uint32_t byte_offset) const {
+    if (kCo) {
+      typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+      const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)byte_offset, 0, /*sc1*/ 16);
+      return make_uint4(v.x, v.y, v.z, v.w);
+    }
+    return *reinterpret_cast<const uint4*>(base + byte_offset);
+  }
+};
+
+// Wait until this wavefront's memory operations have completed (made
+// device-visible for coherent stores), without moving memory operations
+// across it.
+__device__ __forceinline__ void wait_memory() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 // Resolve the wave-local expert index w to (expert, slot); false if unused.
 __device__ __forceinline__ bool resolve_wave_expert(const WaveArg& wave, const GroupView& gv,
                                                     int w, int& expert, int& slot) {

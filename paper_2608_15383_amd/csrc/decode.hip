@@ -1,0 +1,292 @@
+// Fused single-launch decode layer for a few tokens with every expert
+// resident (C = E, Sec. 3.3): route, top-k, gate/up + SwiGLU, down and the
+// weighted combine in one kernel.
+//
+// On MI355X a kernel boundary costs about 2.4 us and a dependent round trip to
+// memory about 1.5 us under load, against roughly 5 us to stream the decode
+// layer's 26 MB of packed weights.  The six-kernel sequence is therefore
+// replaced by one grid whose workgroups play three roles by index:
+//   [0, nR)        router items: logits of 4 experts for every token;
+//   [nR, nR+nG)    gate/up items (one token-expert pair, row-block pairs);
+//   [nR+nG, ...)   down items (output row-block rb of every token).
+// Every gate/up and down workgroup waits for the router items, reads the
+// logits and runs the top-k itself (cheap, and it saves the round trips of
+// publishing the selection).  Down items then prefetch their down tiles while
+// the gate/up items stream theirs, wait for all gate/up items, and add the k
+// expert outputs of each token in rank order.  Down item 0 finally writes the
+// routing and grouping arrays to the workspace, as the unfused path does.
+//
+// A workgroup only waits for workgroups of lower index, which the hardware
+// dispatches first, and the grid is sized to be co-resident on an idle GPU.
+// Every wait is still bounded and counts a timeout instead of spinning
+// forever.  Data crossing workgroups is written and read device-coherently and
+// ordered by waiting for outstanding memory operations before a counter is
+// bumped, so no cache-wide fence is needed.  Counters only grow; the host
+// derives each launch's targets from its running totals.
+//
+// The arithmetic is that of the stand-alone kernels (device_route.h,
+// device_gemv.h), so the result is bit-identical to the unfused path.
+#include <mutex>
+
+#include "decode.h"
+#include "device_gemv.h"
+#include "device_route.h"
+
+namespace emoe {
+namespace {
+
+constexpr uint32_t kSpinLimit = 1u << 20;
+constexpr int kPollSleep = 8;  // s_sleep units (64 clocks) between polls
+
+__device__ __forceinline__ bool reached(uint32_t v, uint32_t target) {
+  return (int32_t)(v - target) >= 0;  // modulo-2^32 comparison
+}
+
+// Wait (bounded) until *p reaches target; whole workgroup.
+__device__ __forceinline__ void block_wait(const uint32_t* p, uint32_t target, uint32_t* timeouts) {
+  if (threadIdx.x == 0) {
+    uint32_t it = 0;
+    while (!reached(ld_u32<true>(p), target)) {
+      if (++it > kSpinLimit) {
+        atomicAdd(timeouts, 1u);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(kPollSleep);
+    }
+  }
+  __syncthreads();
+}
+
+// Wait (bounded) until gate_done[i] reaches target[i] for every spread counter.
+__device__ __forceinline__ void block_wait_gates(DecodeSync* sy, const uint32_t* target) {
+  if (threadIdx.x < 64) {
+    const int lane = lane_id();
+    const uint32_t tgt = lane < kSyncLanes ? target[lane] : 0u;
+    uint32_t it = 0;
+    while (true) {
+      const bool ok = lane >= kSyncLanes || reached(ld_u32<true>(&sy->gate_done[lane][0]), tgt);
+      if (__all(ok)) break;
+      if (++it > kSpinLimit) {
+        if (lane == 0) atomicAdd(&sy->timeouts, 1u);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(kPollSleep);
+    }
+  }
+  __syncthreads();
+}
+
+// Make this workgroup's coherent stores visible, then bump *p.
+__device__ __forceinline__ void block_signal(uint32_t* p) {
+  wait_memory();
+  __syncthreads();
+  if (threadIdx.x == 0) atomicAdd(p, 1u);
+}
+
+__global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
+  __shared__ GroupShared<256> gsh;
+  __shared__ GateUpShared gush;
+  __shared__ float o_lds[kFusedMaxPairs][16];
+  __shared__ int32_t s_ids[kFusedMaxPairs];
+  __shared__ float s_w[kFusedMaxPairs];
+  __shared__ uint4 s_act[kFusedActLdsBytes / 16];
+  __shared__ float s_xs[kFusedActLdsBytes / (2 * kGroup) * 4];  // [pair][group][quarter]
+
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wi = tid >> 6;
+  const int blk = blockIdx.x;
+  DecodeSync* sy = a.sync;
+  const int P = a.tokens * a.top_k;
+
+  if (blk < a.n_router) {
+    // ---------------------------------------------------------------- router
+    // Each logit goes to the workspace and to kSyncLanes replicas, so the
+    // hundreds of readers below spread over as many memory locations.
+    if (!a.logits_override) {
+      const int e0 = 4 * blk + wi;
+      if (e0 < a.n_experts) {
+        double s[kFusedMaxTokens][1];
+        wave_router_sums<kFusedMaxTokens, 1>(a.tokens, a.n_experts, a.d, 0, e0, a.h, a.w_router, s);
+#pragma unroll
+        for (int t = 0; t < kFusedMaxTokens; ++t) {
+          if (t >= a.tokens) break;
+          const uint32_t v = __float_as_uint((float)s[t][0]);
+          const int at = t * a.n_experts + e0;
+          if (lane < kSyncLanes) st_u32<true>(&sy->logits[lane][at], v);
+          if (lane == kSyncLanes) st_u32<false>(a.logits + at, v);
+        }
+      }
+    }
+    wait_memory();
+    __syncthreads();
+    if (tid < kSyncLanes) atomicAdd(&sy->route_done[tid][0], 1u);
+    return;
+  }
+
+  // Every other workgroup: wait for the logits and select the experts.
+  const int replica = blk % kSyncLanes;
+  block_wait(&sy->route_done[replica][0], a.route_target, &sy->timeouts);
+  const float* z = a.logits_override ? a.logits_override : sy->logits[replica];
+  TopkState st;  // wavefront wi selects the experts of token wi
+  if (wi < a.tokens) {
+    wave_topk_select<true>(z + (int64_t)wi * a.n_experts, a.n_experts, a.top_k, st);
+    wave_topk_store_ids<false>(st, a.top_k, s_ids + wi * a.top_k);
+  }
+  __syncthreads();
+
+  if (blk < a.n_router + a.n_gate) {
+    // ---------------------------------------------------------------- gate/up
+    // Item = (pair pi, row-block pairs b0 ..): one token row of one expert.
+    // The activation goes to act row pi (pair order).
+    const int item = blk - a.n_router;
+    const int pairs_of_f = a.f / kTileRows;
+    const int chunks = (pairs_of_f + a.pairs_per_item - 1) / a.pairs_per_item;
+    const int pi = item / chunks;
+    const int b0 = (item % chunks) * a.pairs_per_item;
+    const int b1 = min(b0 + a.pairs_per_item, pairs_of_f);
+    const int e = s_ids[pi];
+    const int top_k = a.top_k;
+    for (int b = b0; b < b1; ++b)
+      gateup_rows<true>(gush, a.d, a.f, a.h, [top_k](int s) { return s / top_k; }, pi, pi + 1,
+                        a.slot_bank + (int64_t)e * a.record_bytes, b, a.act);
+    block_signal(&sy->gate_done[item % kSyncLanes][0]);
+    return;
+  }
+
+  // ------------------------------------------------------------------ down + combine
+  const int rb = blk - a.n_router - a.n_gate;
+  const int G = a.f / kGroup;
+  // Wavefront wi owns pairs wi, wi+4, ...; the first two are prefetched.
+  DownBatch pre0, pre1;
+  if (wi < P)
+    down_load_batch(a.slot_bank + (int64_t)s_ids[wi] * a.record_bytes, a.d, a.f, rb, 0, pre0);
+  if (wi + kGemvWaves < P)
+    down_load_batch(a.slot_bank + (int64_t)s_ids[wi + kGemvWaves] * a.record_bytes, a.d, a.f, rb,
+                    0, pre1);
+  // The mixture weights are needed only by the combine: compute them while
+  // the tiles stream in.
+  if (wi < a.tokens)
+    wave_topk_weights<false>(st, a.n_experts, a.top_k, a.renormalize, s_w + wi * a.top_k);
+  block_wait_gates(sy, a.gate_target);
+
+  // Stage every pair's activation row in LDS with one coherent pass, then the
+  // per-(pair, group, quarter) activation sums used by every row block.
+  {
+    const uint32_t n16 = (uint32_t)P * (uint32_t)a.f / 8u;
+    const Buf128<true> xb(a.act, n16 * 16u);
+    for (uint32_t i = tid; i < n16; i += 256) s_act[i] = xb.load(16u * i);
+  }
+  __syncthreads();
+  const uint16_t* act_lds = reinterpret_cast<const uint16_t*>(s_act);
+  for (int i = tid; i < P * G * 4; i += 256) {
+    const int pi = i / (G * 4), g = (i >> 2) % G, q = i & 3;
+    uint4 x[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      x[k] = *reinterpret_cast<const uint4*>(act_lds + pi * a.f + g * kGroup + 8 * q + 32 * k);
+    s_xs[i] = lane_group_xsum(x);
+  }
+  __syncthreads();
+  // Expert output of pair pi for this row block; `first` is its first batch
+  // of tiles (prefetched when has_first).
+  auto pair_output = [&](int pi, DownBatch first, bool has_first) {
+    const uint8_t* rec = a.slot_bank + (int64_t)s_ids[pi] * a.record_bytes;
+    auto xload = [&](int, int k) {
+      return *reinterpret_cast<const uint4*>(act_lds + pi * a.f + k);
+    };
+    auto xsload = [&](int, int g) { return s_xs[(pi * G + g) * 4 + (lane >> 4)]; };
+    float acc[kTokChunk] = {0.f, 0.f, 0.f, 0.f};
+    if (!has_first) down_load_batch(rec, a.d, a.f, rb, 0, first);
+    down_apply_batch_xs(first, a.f, 0, xload, xsload, 1, acc);
+    for (int g0 = kDownBatch; g0 < G; g0 += kDownBatch) {
+      DownBatch bt;
+      down_load_batch(rec, a.d, a.f, rb, g0, bt);
+      down_apply_batch_xs(bt, a.f, g0, xload, xsload, 1, acc);
+    }
+    const float o = reduce_quarters(acc[0]);
+    if (lane < 16) {
+      o_lds[pi][lane] = o;
+      a.pair_out[(int64_t)pi * a.d + 16 * rb + lane] = o;
+    }
+  };
+  if (wi < P) pair_output(wi, pre0, true);
+  if (wi + kGemvWaves < P) pair_output(wi + kGemvWaves, pre1, true);
+  for (int pi = wi + 2 * kGemvWaves; pi < P; pi += kGemvWaves) pair_output(pi, pre0, false);
+  __syncthreads();
+  if (tid < 16 * a.tokens) {
+    const int t = tid >> 4, n = tid & 15;
+    float acc = 0.f;
+    for (int j = 0; j < a.top_k; ++j)
+      acc = fmaf(s_w[t * a.top_k + j], o_lds[t * a.top_k + j][n], acc);
+    a.y[(int64_t)t * a.d + 16 * rb + n] = (uint16_t)f32_to_bf16_rne(acc);
+  }
+
+  if (rb == 0) {
+    // The workspace's routing and grouping arrays, as the unfused path writes them.
+    for (int j = tid; j < P; j += 256) {
+      a.topk_ids[j] = s_ids[j];
+      a.topk_w[j] = s_w[j];
+    }
+    block_group<256, false>(gsh, P, a.n_experts, s_ids, a.counts, a.offsets, a.sorted_pairs,
+                            a.active, a.n_active, nullptr, a.pair_pos);
+  }
+}
+
+// Co-resident workgroups of the fused kernel on the current device.
+int fused_capacity() {
+  static std::mutex mu;
+  static int cap[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  std::lock_guard<std::mutex> lk(mu);
+  if (cap[dev] == 0) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_fused_kernel, 256, 0) !=
+            hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    cap[dev] = per_cu * cus;
+  }
+  return cap[dev];
+}
+
+}  // namespace
+
+bool decode_fused_plan(DecodeArgs& a) {
+  if (a.tokens < 1 || a.tokens > kFusedMaxTokens || a.tokens * a.top_k > kFusedMaxPairs)
+    return false;
+  if ((int64_t)a.tokens * a.top_k * a.f * 2 > kFusedActLdsBytes) return false;
+  const int P = a.tokens * a.top_k;
+  const int pairs_of_f = a.f / kTileRows;
+  a.n_router = a.logits_override ? 1 : (a.n_experts + 3) / 4;
+  a.n_down = a.d / kTileRows;
+  const int cap = fused_capacity();
+  for (int ppi = 1; ppi <= pairs_of_f; ppi *= 2) {
+    const int n_gate = P * ((pairs_of_f + ppi - 1) / ppi);
+    if (a.n_router + n_gate + a.n_down <= cap) {
+      a.pairs_per_item = ppi;
+      a.n_gate = n_gate;
+      return true;
+    }
+  }
+  return false;
+}
+
+hipError_t launch_decode_fused(DecodeArgs& a, DecodeProgress& prog, hipStream_t stream) {
+  a.route_target = prog.route_total + (uint32_t)a.n_router;
+  for (int i = 0; i < kSyncLanes; ++i)
+    a.gate_target[i] =
+        prog.gate_total[i] + (uint32_t)(a.n_gate / kSyncLanes + (i < a.n_gate % kSyncLanes));
+  launch(decode_fused_kernel, dim3(a.n_router + a.n_gate + a.n_down), dim3(256), stream, a);
+  const hipError_t e = hipGetLastError();
+  if (e == hipSuccess) {
+    prog.route_total = a.route_target;
+    for (int i = 0; i < kSyncLanes; ++i) prog.gate_total[i] = a.gate_target[i];
+  }
+  return e;
+}
+
+}  // namespace emoe

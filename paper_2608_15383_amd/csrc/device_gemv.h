@@ -1,0 +1,278 @@
+// Device routines of the weight-streaming (few tokens per expert) projections,
+// shared by the grouped GEMV kernels (gemv.hip) and the fused decode kernel
+// (decode.hip), so both produce bit-identical results.  kCo selects
+// device-coherent accesses for data exchanged between workgroups.
+//
+// In-register dequantization: for a code dword, ((dw >> 4p) & 0x000f000f) |
+// 0x43004300 is the bf16 pair (128 + u_2p, 128 + u_2p+1), exact because bf16
+// represents the integers 128..143.  With u = q + 8 the dot product over a
+// lane's 32 inputs is sum (u - 8) x = sum (128 + u) x - 136 sum x, so each
+// group needs one correction with the activations' sum before the FP16 group
+// scale is applied in fp32 (Sec. 3.2: W_hat = s q is never rounded).
+#pragma once
+
+#include "common.h"
+
+namespace emoe {
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+constexpr int kGemvWaves = 4;      // wavefronts per workgroup
+constexpr int kTokChunk = 4;       // token rows per pass over the weights
+constexpr int kGateBatch = 4;      // tiles per matrix one wavefront loads together (gate/up)
+constexpr int kDownBatch = 8;      // tiles one wavefront loads together (down)
+constexpr uint32_t kOnesBf16x2 = 0x3f803f80u;  // bf16 pair (1, 1)
+
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                        __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+__device__ __forceinline__ void dequant_dword(uint32_t dw, uint32_t* out) {
+#pragma unroll
+  for (int p = 0; p < 4; ++p) out[p] = ((dw >> (4 * p)) & 0x000f000fu) | 0x43004300u;
+}
+
+// Dot product of one lane's 32 codes of a group (its row, its inputs) with the
+// 32 matching activations x (4 x uint4): returns sum (128 + u) x and, when
+// want_xs, adds sum x to xs.
+__device__ __forceinline__ float lane_group_dot(const uint4 codes, const uint4* x, float& xs,
+                                                bool want_xs) {
+  const uint32_t c[4] = {codes.x, codes.y, codes.z, codes.w};
+  float acc = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t wp[4];
+    dequant_dword(c[i], wp);
+    const uint32_t xv[4] = {x[i].x, x[i].y, x[i].z, x[i].w};
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      acc = dot2(wp[p], xv[p], acc);
+      if (want_xs) xs = dot2(kOnesBf16x2, xv[p], xs);
+    }
+  }
+  return acc;
+}
+
+__device__ __forceinline__ void load_x32(const uint16_t* row, uint4* x) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) x[i] = *reinterpret_cast<const uint4*>(row + 32 * i);
+}
+
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  return g / (1.0f + expf(-g)) * u;
+}
+
+struct GateUpShared {
+  float red[kGemvWaves][kTokChunk][2][16];
+};
+
+// One workgroup of kGemvWaves wavefronts computes the SwiGLU activation
+// phi(W_g h) * (W_u h) of gate/up row-block pair b (outputs 16b .. 16b+15) for
+// the rows s in [begin, end) of one expert whose packed record is `rec`;
+// token_of(s) is the token of row s and the result goes to act row s (bf16,
+// pairs of outputs per 32-bit store).  The wavefronts split the input
+// groups round-robin and meet in LDS in wavefront order.  Each row's result
+// depends only on that row, not on which rows share the pass.
+template <bool kCo, typename TokenOf>
+__device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f,
+                                            const uint16_t* __restrict__ h, TokenOf token_of,
+                                            int begin, int end, const uint8_t* __restrict__ rec,
+                                            int b, uint16_t* __restrict__ act);
+
+// The grouped rows [begin, end) of one expert; the token of grouped row s is
+// sorted_pairs[s] / top_k.
+template <bool kCo>
+__device__ __forceinline__ void gateup_block(GateUpShared& sh, int d, int f, int top_k,
+                                             const uint16_t* __restrict__ h,
+                                             const int32_t* __restrict__ sorted_pairs, int begin,
+                                             int end, const uint8_t* __restrict__ rec, int b,
+                                             uint16_t* __restrict__ act) {
+  gateup_rows<kCo>(
+      sh, d, f, h, [&](int s) { return ld_i32<kCo>(sorted_pairs + s) / top_k; }, begin, end, rec,
+      b, act);
+}
+
+template <bool kCo, typename TokenOf>
+__device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f,
+                                            const uint16_t* __restrict__ h, TokenOf token_of,
+                                            int begin, int end, const uint8_t* __restrict__ rec,
+                                            int b, uint16_t* __restrict__ act) {
+  const int lane = lane_id();
+  const int wi = threadIdx.x >> 6;
+  const int G = d / kGroup;
+  const RecordLayout L = record_layout(d, f);
+  const uint8_t* gate_codes = rec + L.w13_codes + (int64_t)(2 * b) * G * kTileBytes + 16 * lane;
+  const uint8_t* up_codes = gate_codes + (int64_t)G * kTileBytes;
+  const int n_local = lane & 15;
+  const int quarter = lane >> 4;
+  const uint16_t* scales = reinterpret_cast<const uint16_t*>(rec + L.w13_scales);
+  const uint16_t* gate_sc = scales + (int64_t)(32 * b + n_local) * G;
+  const uint16_t* up_sc = scales + (int64_t)(32 * b + 16 + n_local) * G;
+
+  for (int m0 = begin; m0 < end; m0 += kTokChunk) {
+    const int mc = min(kTokChunk, end - m0);
+    const uint16_t* xrow[kTokChunk];
+#pragma unroll
+    for (int m = 0; m < kTokChunk; ++m) {
+      const int t = m < mc ? token_of(m0 + m) : 0;
+      xrow[m] = h + (int64_t)t * d + 8 * quarter;
+    }
+    float accg[kTokChunk], accu[kTokChunk];
+#pragma unroll
+    for (int m = 0; m < kTokChunk; ++m) accg[m] = accu[m] = 0.f;
+
+    for (int g0 = wi; g0 < G; g0 += kGemvWaves * kGateBatch) {
+      uint4 cg[kGateBatch], cu[kGateBatch];
+      float sg[kGateBatch], su[kGateBatch];
+#pragma unroll
+      for (int j = 0; j < kGateBatch; ++j) {
+        const int g = g0 + kGemvWaves * j;
+        if (g < G) {
+          cg[j] = *reinterpret_cast<const uint4*>(gate_codes + (int64_t)g * kTileBytes);
+          cu[j] = *reinterpret_cast<const uint4*>(up_codes + (int64_t)g * kTileBytes);
+          sg[j] = half_bits_to_f32(gate_sc[g]);
+          su[j] = half_bits_to_f32(up_sc[g]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kGateBatch; ++j) {
+        const int g = g0 + kGemvWaves * j;
+        if (g >= G) break;
+#pragma unroll
+        for (int m = 0; m < kTokChunk; ++m) {
+          if (m >= mc) break;
+          uint4 x[4];
+          load_x32(xrow[m] + g * kGroup, x);
+          float xs = 0.f;
+          const float pg = lane_group_dot(cg[j], x, xs, true);
+          const float pu = lane_group_dot(cu[j], x, xs, false);
+          accg[m] = fmaf(sg[j], fmaf(-136.f, xs, pg), accg[m]);
+          accu[m] = fmaf(su[j], fmaf(-136.f, xs, pu), accu[m]);
+        }
+      }
+    }
+#pragma unroll
+    for (int m = 0; m < kTokChunk; ++m) {
+      accg[m] += __shfl_xor(accg[m], 16);
+      accg[m] += __shfl_xor(accg[m], 32);
+      accu[m] += __shfl_xor(accu[m], 16);
+      accu[m] += __shfl_xor(accu[m], 32);
+      if (quarter == 0) {
+        sh.red[wi][m][0][n_local] = accg[m];
+        sh.red[wi][m][1][n_local] = accu[m];
+      }
+    }
+    __syncthreads();
+    if (wi == 0) {
+      const int m = lane >> 4;  // lane = 16 m + n
+      float g = 0.f, u = 0.f;
+#pragma unroll
+      for (int w = 0; w < kGemvWaves; ++w) {
+        g += sh.red[w][m][0][n_local];
+        u += sh.red[w][m][1][n_local];
+      }
+      const uint32_t a16 = f32_to_bf16_rne(silu_mul(g, u));
+      const uint32_t next = __shfl_down(a16, 1);
+      if (m < mc && (n_local & 1) == 0)
+        st_u32<kCo>(act + (int64_t)(m0 + m) * f + 16 * b + n_local, a16 | (next << 16));
+    }
+    __syncthreads();
+  }
+}
+
+// Down projection tiles of one wavefront: row-block rb, input groups
+// g0 .. g0+kDownBatch-1 (those < G).
+struct DownBatch {
+  uint4 c[kDownBatch];
+  float s[kDownBatch];
+};
+
+__device__ __forceinline__ void down_load_batch(const uint8_t* __restrict__ rec, int d, int f,
+                                                int rb, int g0, DownBatch& bt) {
+  const int lane = lane_id();
+  const int G = f / kGroup;
+  const RecordLayout L = record_layout(d, f);
+  const uint8_t* codes = rec + L.w2_codes + (int64_t)rb * G * kTileBytes + 16 * lane;
+  const uint16_t* sc = reinterpret_cast<const uint16_t*>(rec + L.w2_scales) +
+                       (int64_t)(16 * rb + (lane & 15)) * G;
+#pragma unroll
+  for (int j = 0; j < kDownBatch; ++j) {
+    if (g0 + j < G) {
+      bt.c[j] = *reinterpret_cast<const uint4*>(codes + (int64_t)(g0 + j) * kTileBytes);
+      bt.s[j] = half_bits_to_f32(sc[g0 + j]);
+    }
+  }
+}
+
+// acc[m] += contribution of the loaded batch to activation rows m < mc;
+// xload(m, k) returns the 8 bf16 activations k .. k+7 of row m.
+template <typename XLoad>
+__device__ __forceinline__ void down_apply_batch(const DownBatch& bt, int f, int g0, XLoad xload,
+                                                 int mc, float* acc) {
+  const int quarter = lane_id() >> 4;
+  const int G = f / kGroup;
+#pragma unroll
+  for (int j = 0; j < kDownBatch; ++j) {
+    const int g = g0 + j;
+    if (g >= G) break;
+#pragma unroll
+    for (int m = 0; m < kTokChunk; ++m) {
+      if (m >= mc) break;
+      uint4 x[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[i] = xload(m, g * kGroup + 8 * quarter + 32 * i);
+      float xs = 0.f;
+      const float p = lane_group_dot(bt.c[j], x, xs, true);
+      acc[m] = fmaf(bt.s[j], fmaf(-136.f, xs, p), acc[m]);
+    }
+  }
+}
+
+// Sum of the 32 activations x (4 x uint4) of one lane's inputs of a group, in
+// the order lane_group_dot accumulates it.
+__device__ __forceinline__ float lane_group_xsum(const uint4* x) {
+  float xs = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t xv[4] = {x[i].x, x[i].y, x[i].z, x[i].w};
+#pragma unroll
+    for (int p = 0; p < 4; ++p) xs = dot2(kOnesBf16x2, xv[p], xs);
+  }
+  return xs;
+}
+
+// down_apply_batch with the activation sums precomputed: xsload(m, g) is
+// lane_group_xsum of this lane's inputs of group g of row m.
+template <typename XLoad, typename XsLoad>
+__device__ __forceinline__ void down_apply_batch_xs(const DownBatch& bt, int f, int g0,
+                                                    XLoad xload, XsLoad xsload, int mc,
+                                                    float* acc) {
+  const int quarter = lane_id() >> 4;
+  const int G = f / kGroup;
+#pragma unroll
+  for (int j = 0; j < kDownBatch; ++j) {
+    const int g = g0 + j;
+    if (g >= G) break;
+#pragma unroll
+    for (int m = 0; m < kTokChunk; ++m) {
+      if (m >= mc) break;
+      uint4 x[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) x[i] = xload(m, g * kGroup + 8 * quarter + 32 * i);
+      float unused = 0.f;
+      const float p = lane_group_dot(bt.c[j], x, unused, false);
+      acc[m] = fmaf(bt.s[j], fmaf(-136.f, xsload(m, g), p), acc[m]);
+    }
+  }
+}
+
+// Sum a lane's partials over the four lanes of its row: afterwards lanes
+// 0..15 hold the outputs of rows 16*rb + lane.
+__device__ __forceinline__ float reduce_quarters(float v) {
+  v += __shfl_xor(v, 16);
+  v += __shfl_xor(v, 32);
+  return v;
+}
+
+}  // namespace emoe

@@ -1,0 +1,339 @@
+// Device routines of routing and grouping (Sec. 3.1 Eq. 1, Fig. 1, Sec. 3.4),
+// shared by the stand-alone kernels (route.hip) and the fused decode kernel
+// (decode.hip) so both compute bit-identical results.  kCo selects
+// device-coherent global accesses (fused launch) or ordinary ones.
+#pragma once
+
+#include "common.h"
+
+namespace emoe {
+
+constexpr int kPerLane = EMOE_MAX_EXPERTS / 64;  // experts held per lane in top-k / scans
+
+__device__ __forceinline__ void bf16x8_to_f64(const uint4 v, double* out) {
+  const uint32_t dw[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    out[2 * p] = (double)bf16_to_f32(dw[p] & 0xffffu);
+    out[2 * p + 1] = (double)bf16_to_f32(dw[p] >> 16);
+  }
+}
+
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// Logits of NT tokens (t0 .. t0+NT-1, those < tokens) for NE experts (e0 ..)
+// computed by one wavefront: lanes split d in 8-element chunks, products and
+// sums in fp64 (bf16 x bf16 products are exact), one rounding to fp32.
+// The fp64 sums are returned in every lane; wave_router_logits stores them.
+template <int NT, int NE>
+__device__ __forceinline__ void wave_router_sums(int tokens, int n_experts, int d, int t0, int e0,
+                                                 const uint16_t* __restrict__ h,
+                                                 const uint16_t* __restrict__ wr,
+                                                 double (&acc)[NT][NE]) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int a = 0; a < NT; ++a)
+#pragma unroll
+    for (int b = 0; b < NE; ++b) acc[a][b] = 0.0;
+  for (int k0 = 8 * lane; k0 < d; k0 += 512) {
+    double wv[NE][8];
+#pragma unroll
+    for (int b = 0; b < NE; ++b) {
+      if (e0 + b < n_experts) {
+        bf16x8_to_f64(*reinterpret_cast<const uint4*>(wr + (int64_t)(e0 + b) * d + k0), wv[b]);
+      } else {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) wv[b][r] = 0.0;
+      }
+    }
+#pragma unroll
+    for (int a = 0; a < NT; ++a) {
+      if (t0 + a >= tokens) break;
+      double hv[8];
+      bf16x8_to_f64(*reinterpret_cast<const uint4*>(h + (int64_t)(t0 + a) * d + k0), hv);
+#pragma unroll
+      for (int b = 0; b < NE; ++b)
+#pragma unroll
+        for (int r = 0; r < 8; ++r) acc[a][b] = fma(hv[r], wv[b][r], acc[a][b]);
+    }
+  }
+#pragma unroll
+  for (int a = 0; a < NT; ++a)
+#pragma unroll
+    for (int b = 0; b < NE; ++b) acc[a][b] = wave_sum_f64(acc[a][b]);
+}
+
+template <int NT, int NE, bool kCo>
+__device__ __forceinline__ void wave_router_logits(int tokens, int n_experts, int d, int t0, int e0,
+                                                   const uint16_t* __restrict__ h,
+                                                   const uint16_t* __restrict__ wr,
+                                                   float* __restrict__ logits) {
+  double s[NT][NE];
+  wave_router_sums<NT, NE>(tokens, n_experts, d, t0, e0, h, wr, s);
+#pragma unroll
+  for (int a = 0; a < NT; ++a) {
+#pragma unroll
+    for (int b = 0; b < NE; ++b) {
+      const int t = t0 + a, e = e0 + b;
+      if (lane_id() == 0 && t < tokens && e < n_experts)
+        st_u32<kCo>(&logits[(int64_t)t * n_experts + e], __float_as_uint((float)s[a][b]));
+    }
+  }
+}
+
+// Wavefront-wide max / min of a 32-bit unsigned value with DPP lane moves
+// (xor 1, xor 2, half-row mirror, row mirror, then the row broadcasts), the
+// result read from lane 63 so every lane gets it.
+template <bool kMax>
+__device__ __forceinline__ uint32_t dpp_combine(uint32_t a, uint32_t b) {
+  return kMax ? (a > b ? a : b) : (a < b ? a : b);
+}
+
+template <bool kMax>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v) {
+  const int x = (int)v;
+  v = dpp_combine<kMax>(v, (uint32_t)__builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false));
+  int y = (int)v;
+  v = dpp_combine<kMax>(v, (uint32_t)__builtin_amdgcn_update_dpp(y, y, 0x4E, 0xF, 0xF, false));
+  y = (int)v;
+  v = dpp_combine<kMax>(v, (uint32_t)__builtin_amdgcn_update_dpp(y, y, 0x141, 0xF, 0xF, false));
+  y = (int)v;
+  v = dpp_combine<kMax>(v, (uint32_t)__builtin_amdgcn_update_dpp(y, y, 0x140, 0xF, 0xF, false));
+  y = (int)v;
+  v = dpp_combine<kMax>(v, (uint32_t)__builtin_amdgcn_update_dpp(y, y, 0x142, 0xA, 0xF, false));
+  y = (int)v;
+  v = dpp_combine<kMax>(v, (uint32_t)__builtin_amdgcn_update_dpp(y, y, 0x143, 0xC, 0xF, false));
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// Top-k of one token's logits z[E] by one wavefront, and its mixture weights
+// (softmax over the selected logits when renormalize, else over all E), fp64.
+// Round j picks the largest remaining logit (order key: a monotone integer
+// image of the fp32 value, -0 folded onto +0) and, among equal logits, the
+// lowest expert id.  kCo: device-coherent loads of z; kCoStore:
+// device-coherent result stores.
+// wave_topk_select leaves the selection in registers (TopkState);
+// wave_topk_store_ids and wave_topk_weights write it out.
+struct TopkState {
+  float v[kPerLane];       // this lane's logits
+  int sel_id[kPerLane];    // rank j lives in lane j % 64, register j / 64
+  float sel_z[kPerLane];
+  float zmax;
+};
+
+template <bool kCo>
+__device__ __forceinline__ void wave_topk_select(const float* __restrict__ z, int n_experts,
+                                                 int top_k, TopkState& st) {
+  const int lane = lane_id();
+  const int nc = (n_experts + 63) / 64;  // logits per lane in use
+  float* v = st.v;
+  int* sel_id = st.sel_id;
+  float* sel_z = st.sel_z;
+  uint32_t key[kPerLane];  // 0 = not a candidate (keys of non-NaN floats are > 0)
+#pragma unroll
+  for (int c = 0; c < kPerLane; ++c) {
+    const int e = lane + 64 * c;
+    v[c] = e < n_experts ? ld_f32<kCo>(z + e) : 0.f;
+    const uint32_t u = __float_as_uint(v[c] + 0.0f);  // -0 -> +0
+    key[c] = e < n_experts ? ((u & 0x80000000u) ? ~u : (u | 0x80000000u)) : 0u;
+  }
+  float zmax = 0.f;
+  for (int j = 0; j < top_k; ++j) {
+    uint32_t best = 0;
+#pragma unroll
+    for (int c = 0; c < kPerLane; ++c)
+      if (c < nc) best = key[c] > best ? key[c] : best;
+    const uint32_t m = wave_reduce_u32<true>(best);
+    int e;
+    if (nc == 1) {
+      // One logit per lane: the lowest lane holding the maximum is the
+      // lowest expert id among equal logits.
+      e = (int)__builtin_ctzll(__ballot(key[0] == m));
+    } else {
+      uint32_t idx = 0xffffffffu;
+#pragma unroll
+      for (int c = kPerLane - 1; c >= 0; --c)
+        if (c < nc && key[c] == m) idx = (uint32_t)(lane + 64 * c);
+      e = (int)wave_reduce_u32<false>(idx);
+    }
+    const int ce = e >> 6;
+    float vw = v[0];
+#pragma unroll
+    for (int c = 1; c < kPerLane; ++c)
+      if (ce == c) vw = v[c];
+    const float zw = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(vw), e & 63));
+#pragma unroll
+    for (int c = 0; c < kPerLane; ++c)
+      if (lane + 64 * c == e) key[c] = 0u;
+    if (j == 0) zmax = zw;
+#pragma unroll
+    for (int c = 0; c < kPerLane; ++c) {
+      if (j == lane + 64 * c) {
+        sel_id[c] = e;
+        sel_z[c] = zw;
+      }
+    }
+  }
+  st.zmax = zmax;
+}
+
+template <bool kCoStore>
+__device__ __forceinline__ void wave_topk_store_ids(const TopkState& st, int top_k,
+                                                    int32_t* __restrict__ ids_out) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int c = 0; c < kPerLane; ++c)
+    if (lane + 64 * c < top_k) st_u32<kCoStore>(ids_out + lane + 64 * c, (uint32_t)st.sel_id[c]);
+}
+
+template <bool kCoStore>
+__device__ __forceinline__ void wave_topk_weights(const TopkState& st, int n_experts, int top_k,
+                                                  int renormalize, float* __restrict__ w_out) {
+  const int lane = lane_id();
+  const float* v = st.v;
+  const float* sel_z = st.sel_z;
+  const float zmax = st.zmax;
+  double part = 0.0;
+  if (renormalize) {
+#pragma unroll
+    for (int c = 0; c < kPerLane; ++c)
+      if (lane + 64 * c < top_k) part += exp((double)sel_z[c] - (double)zmax);
+  } else {
+#pragma unroll
+    for (int c = 0; c < kPerLane; ++c)
+      if (lane + 64 * c < n_experts) part += exp((double)v[c] - (double)zmax);
+  }
+  const double denom = wave_sum_f64(part);
+#pragma unroll
+  for (int c = 0; c < kPerLane; ++c) {
+    const int j = lane + 64 * c;
+    if (j < top_k)
+      st_u32<kCoStore>(w_out + j,
+                       __float_as_uint((float)(exp((double)sel_z[c] - (double)zmax) / denom)));
+  }
+}
+
+template <bool kCo, bool kCoStore = kCo>
+__device__ __forceinline__ void wave_topk(const float* __restrict__ z, int n_experts, int top_k,
+                                          int renormalize, int32_t* __restrict__ ids_out,
+                                          float* __restrict__ w_out) {
+  TopkState st;
+  wave_topk_select<kCo>(z, n_experts, top_k, st);
+  wave_topk_store_ids<kCoStore>(st, top_k, ids_out);
+  wave_topk_weights<kCoStore>(st, n_experts, top_k, renormalize, w_out);
+}
+
+__device__ __forceinline__ int wave_exclusive_scan(int v, int& total) {
+  const int lane = lane_id();
+  int x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  total = __shfl(x, 63);
+  return x - v;
+}
+
+// LDS of the block-wide grouping.
+template <int kThreads>
+struct GroupShared {
+  int cnt[EMOE_MAX_EXPERTS];
+  int off[EMOE_MAX_EXPERTS];
+  int placed[EMOE_MAX_EXPERTS];
+  int wcnt[kThreads / 64][EMOE_MAX_EXPERTS];
+};
+
+// Grouping of the P pairs by expert, by one workgroup of kThreads threads:
+// counts, exclusive offsets, a stable counting sort of the pair ids (pairs of
+// one expert keep ascending id), the ascending active list, n_active and,
+// when the pointers are non-null, the MFMA row-tile prefix sum and the
+// inverse permutation pair_pos[pi] = grouped position.
+template <int kThreads, bool kCo>
+__device__ void block_group(GroupShared<kThreads>& sh, int pairs, int n_experts,
+                            const int32_t* __restrict__ ids, int32_t* __restrict__ counts,
+                            int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_pairs,
+                            int32_t* __restrict__ active, int32_t* __restrict__ n_active,
+                            int32_t* __restrict__ tile_offsets, int32_t* __restrict__ pair_pos) {
+  constexpr int kWaves = kThreads / 64;
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid >> 6;
+  for (int e = tid; e < EMOE_MAX_EXPERTS; e += kThreads) {
+    sh.cnt[e] = 0;
+    sh.placed[e] = 0;
+  }
+  __syncthreads();
+  for (int i = tid; i < pairs; i += kThreads) atomicAdd(&sh.cnt[ld_i32<kCo>(ids + i)], 1);
+  __syncthreads();
+  if (wave == 0) {
+    int c[kPerLane], local = 0, nz = 0, tl = 0;
+#pragma unroll
+    for (int q = 0; q < kPerLane; ++q) {
+      const int e = kPerLane * lane + q;
+      c[q] = e < n_experts ? sh.cnt[e] : 0;
+      local += c[q];
+      nz += c[q] > 0;
+      tl += (c[q] + kMfmaRows - 1) / kMfmaRows;
+    }
+    int total, nz_total, tl_total;
+    int base = wave_exclusive_scan(local, total);
+    int nz_base = wave_exclusive_scan(nz, nz_total);
+    int tl_base = wave_exclusive_scan(tl, tl_total);
+#pragma unroll
+    for (int q = 0; q < kPerLane; ++q) {
+      const int e = kPerLane * lane + q;
+      if (e < n_experts) {
+        sh.off[e] = base;
+        st_u32<kCo>(counts + e, (uint32_t)c[q]);
+        st_u32<kCo>(offsets + e, (uint32_t)base);
+        if (tile_offsets) st_u32<kCo>(tile_offsets + e, (uint32_t)tl_base);
+        if (c[q] > 0) st_u32<kCo>(active + nz_base++, (uint32_t)e);
+      }
+      base += c[q];
+      tl_base += (c[q] + kMfmaRows - 1) / kMfmaRows;
+    }
+    if (lane == 0) {
+      st_u32<kCo>(offsets + n_experts, (uint32_t)total);
+      if (tile_offsets) st_u32<kCo>(tile_offsets + n_experts, (uint32_t)tl_total);
+      st_u32<kCo>(n_active, (uint32_t)nz_total);
+    }
+  }
+  __syncthreads();
+  int bits = 0;
+  while ((1 << bits) < n_experts) ++bits;
+  for (int base = 0; base < pairs; base += kThreads) {
+    for (int e = lane; e < EMOE_MAX_EXPERTS; e += 64) sh.wcnt[wave][e] = 0;
+    __syncthreads();
+    const int i = base + tid;
+    const bool valid = i < pairs;
+    const int e = valid ? ld_i32<kCo>(ids + i) : 0;
+    uint64_t match = __ballot(valid);
+    for (int b = 0; b < bits; ++b) {
+      const uint64_t m = __ballot(valid && ((e >> b) & 1));
+      match &= ((e >> b) & 1) ? m : ~m;
+    }
+    const int rank = __popcll(match & ((1ull << lane) - 1ull));
+    if (valid && rank == 0) sh.wcnt[wave][e] = __popcll(match);
+    __syncthreads();
+    if (valid) {
+      int pos = sh.placed[e] + rank;
+      for (int w = 0; w < wave; ++w) pos += sh.wcnt[w][e];
+      st_u32<kCo>(sorted_pairs + sh.off[e] + pos, (uint32_t)i);
+      if (pair_pos) st_u32<kCo>(pair_pos + i, (uint32_t)(sh.off[e] + pos));
+    }
+    __syncthreads();
+    for (int x = tid; x < n_experts; x += kThreads) {
+      int s = 0;
+      for (int w = 0; w < kWaves; ++w) s += sh.wcnt[w][x];
+      sh.placed[x] += s;
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace emoe

@@ -314,3 +314,42 @@ def test_prefill_paths_agree(olmoe):
     assert_close(y_m[[0, 128, 255]], ref, "256 tokens MFMA")
     assert_close(y_m, y_g.astype(np.float64), "MFMA vs GEMV")
     experts.cache.clear()
+
+
+# ------------------------------------------------------------------ fused decode launch
+@pytest.mark.parametrize("shape,tokens", [(TINY, 1), (TINY, 4), (LayerShape(384, 256, 6, 3), 3),
+                                          (LayerShape(256, 384, 1, 1), 1),
+                                          (LayerShape(128, 128, 200, 8), 4), (OLMOE, 2),
+                                          (OLMOE, 4)])
+def test_fused_decode_matches_unfused_bitwise(shape, tokens):
+    """The single-launch decode layer equals the per-kernel path bit for bit."""
+    lay = make_layer(shape, tokens, seed=17)
+    layer = Layer(dims_of(shape), lay, tokens)
+    st = api.Stats()
+    y_f = layer.forward(lay.h, stats=st)
+    fits = tokens * shape.top_k * shape.d_ff * 2 <= 32768   # activation rows staged in LDS
+    assert (st.kernel_launches == 1) == fits            # fused when it fits
+    po_f = layer.ws_array("pair_out", tokens * shape.top_k * shape.d_model, np.float32)
+    y_s = layer.forward(lay.h, sequential=True)          # per-expert launches, unfused kernels
+    po_s = layer.ws_array("pair_out", tokens * shape.top_k * shape.d_model, np.float32)
+    assert np.array_equal(y_f, y_s) and np.array_equal(po_f, po_s)
+    ref, _ = oracle_y(lay, LazyExperts(lay), shape.top_k)
+    assert_close(y_f, ref, f"fused {shape} T={tokens}")
+    assert layer.cache.sync_timeouts() == 0
+
+
+def test_fused_decode_repeated_calls_and_override():
+    """Back-to-back fused launches reuse the cache's counters; override logits work."""
+    lay = make_layer(OLMOE, 4, seed=19)
+    layer = Layer(dims_of(OLMOE), lay, 4)
+    experts = LazyExperts(lay)
+    z = spread_logits(4, 64, 8, 32, seed=5)
+    for rep in range(3):
+        for t in (1, 2, 4):
+            sub = _sub(lay, t)
+            y = layer.forward(sub.h, logits=z[:t])
+            ys = layer.forward(sub.h, logits=z[:t], sequential=True)
+            assert np.array_equal(y, ys), (rep, t)
+    ref, _ = oracle_y(_sub(lay, 4), experts, 8, logits=z)
+    assert_close(y, ref, "fused with override")
+    assert layer.cache.sync_timeouts() == 0
