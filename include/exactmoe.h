@@ -52,7 +52,9 @@ enum emoe_status {
  * when the call averages at least EMOE_MFMA_MIN_PAIRS_PER_EXPERT token-expert
  * pairs per expert, else the VALU weight-streaming GEMV.  The choice is made
  * once per call from (tokens, top_k, n_experts), so every wave of a call uses
- * the same arithmetic. */
+ * the same arithmetic.  The MFMA path needs tokens*d_model*2 and
+ * tokens*top_k*d_ff*2 below 2^31 bytes (AUTO takes the GEMV otherwise; an
+ * explicit MFMA request fails with EMOE_ESHAPE). */
 enum emoe_path { EMOE_PATH_AUTO = 0, EMOE_PATH_GEMV = 1, EMOE_PATH_MFMA = 2 };
 #define EMOE_MFMA_MIN_PAIRS_PER_EXPERT 32
 
@@ -91,6 +93,9 @@ typedef struct emoe_ws_layout {
   size_t pair_pos;      /* i32   [T*k]    grouped position of each pair id (fused decode) */
   size_t act;           /* bf16  [T*k][d_ff]    phi(g)*u per pair, grouped order */
   size_t pair_out;      /* f32   [T*k][d_model] expert output per pair id */
+  size_t x_bias;        /* f32   [T][d_model/128]   -136 * group sums of h (MFMA path) */
+  size_t act_bias;      /* f32   [T*k][d_ff/128]    -136 * group sums of act, grouped order
+                                                      (MFMA path) */
   size_t total;         /* bytes needed */
 } emoe_ws_layout;
 
@@ -249,7 +254,7 @@ int32_t emoe_moe_forward_sequential(emoe_cache* cache, int32_t tokens, const uin
 enum emoe_kernel {
   EMOE_K_ROUTER = 0, EMOE_K_TOPK = 1, EMOE_K_GROUP = 2, EMOE_K_GATEUP_GEMV = 3,
   EMOE_K_DOWN_GEMV = 4, EMOE_K_GATEUP_MFMA = 5, EMOE_K_DOWN_MFMA = 6, EMOE_K_COMBINE = 7,
-  EMOE_K_DECODE_FUSED = 8
+  EMOE_K_DECODE_FUSED = 8, EMOE_K_ROW_BIAS = 9
 };
 /* Start recording a HIP event pair around each kernel that emoe_route,
  * emoe_moe_forward and emoe_moe_forward_sequential launch from this thread,

@@ -145,6 +145,8 @@ emoe_ws_layout make_layout(const emoe_dims& d, int32_t T) {
   L.pair_pos = take(P * 4);
   L.act = take(P * (size_t)d.d_ff * 2);
   L.pair_out = take(P * (size_t)d.d_model * 4);
+  L.x_bias = take((size_t)T * (d.d_model / EMOE_GROUP) * 4);
+  L.act_bias = take(P * (size_t)(d.d_ff / EMOE_GROUP) * 4);
   L.total = off;
   return L;
 }
@@ -600,8 +602,13 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
     return fail(EMOE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, L.total);
   const int E = D.n_experts, k = D.top_k, d = D.d_model, f = D.d_ff;
   const int P = T * k;
+  // The MFMA kernels address activations with 32-bit buffer offsets.
+  const bool mfma_fits = (int64_t)P * f * 2 <= INT32_MAX && (int64_t)T * d * 2 <= INT32_MAX &&
+                         c->record_bytes <= INT32_MAX;
   if (path == EMOE_PATH_AUTO)
-    path = (P >= EMOE_MFMA_MIN_PAIRS_PER_EXPERT * E) ? EMOE_PATH_MFMA : EMOE_PATH_GEMV;
+    path = (P >= EMOE_MFMA_MIN_PAIRS_PER_EXPERT * E && mfma_fits) ? EMOE_PATH_MFMA : EMOE_PATH_GEMV;
+  if (path == EMOE_PATH_MFMA && !mfma_fits)
+    return fail(EMOE_ESHAPE, "MFMA path: %d tokens exceed its 2 GiB activation addressing", T);
 
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   float* logits = reinterpret_cast<float*>(ws + L.logits);
@@ -615,6 +622,8 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
   int32_t* tiles = reinterpret_cast<int32_t*>(ws + L.tile_offsets);
   uint16_t* act = reinterpret_cast<uint16_t*>(ws + L.act);
   float* pair_out = reinterpret_cast<float*>(ws + L.pair_out);
+  float* x_bias = reinterpret_cast<float*>(ws + L.x_bias);
+  float* act_bias = reinterpret_cast<float*>(ws + L.act_bias);
 
   int32_t* pair_pos = reinterpret_cast<int32_t*>(ws + L.pair_pos);
   DecodeArgs a{};
@@ -665,13 +674,20 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
               launch_group(P, E, ids, counts, offsets, sorted, active, n_active, tiles, stream));
   ds.kernel_launches += 2;
   const GroupView gv{sorted, offsets, active, n_active, tiles};
+  if (path == EMOE_PATH_MFMA) {
+    // Accumulator start of the gate/up MFMA chains, once per call.
+    EMOE_LAUNCH(EMOE_K_ROW_BIAS, stream, launch_row_bias(T, d, h, x_bias, stream));
+    ds.kernel_launches += 1;
+  }
 
   auto run_wave = [&](const WaveArg& wa) -> int32_t {
     if (path == EMOE_PATH_MFMA) {
       EMOE_LAUNCH(EMOE_K_GATEUP_MFMA, stream,
-                  launch_gateup_mfma(d, f, k, P, E, h, gv, wa, c->slot_bank, c->record_bytes, act, stream));
+                  launch_gateup_mfma(T, d, f, k, E, h, x_bias, gv, wa, c->slot_bank, c->record_bytes,
+                                     act, act_bias, stream));
       EMOE_LAUNCH(EMOE_K_DOWN_MFMA, stream,
-                  launch_down_mfma(d, f, k, P, E, act, gv, wa, c->slot_bank, c->record_bytes, pair_out, stream));
+                  launch_down_mfma(T, d, f, k, E, act, act_bias, gv, wa, c->slot_bank, c->record_bytes,
+                                   pair_out, stream));
     } else {
       EMOE_LAUNCH(EMOE_K_GATEUP_GEMV, stream,
                   launch_gateup_gemv(d, f, k, P, E, h, gv, wa, c->slot_bank, c->record_bytes, act, stream));

@@ -220,13 +220,18 @@ hipError_t launch_down_gemv(int d, int f, int top_k, int pairs, int n_experts,
                             const uint8_t* slot_bank, int64_t record_bytes, float* pair_out,
                             hipStream_t stream);
 
-hipError_t launch_gateup_mfma(int d, int f, int top_k, int pairs, int n_experts,
-                              const uint16_t* h, const GroupView& gv, const WaveArg& wave,
-                              const uint8_t* slot_bank, int64_t record_bytes, uint16_t* act,
-                              hipStream_t stream);
+// Grouped MFMA projections.  h_bias / act_bias: -136 * per-row sums of each
+// 128-input group of h (launch_row_bias) and of act (written by the gate/up
+// launch for the down launch).
+hipError_t launch_row_bias(int rows, int K, const uint16_t* x, float* bias, hipStream_t stream);
 
-hipError_t launch_down_mfma(int d, int f, int top_k, int pairs, int n_experts,
-                            const uint16_t* act, const GroupView& gv, const WaveArg& wave,
+hipError_t launch_gateup_mfma(int tokens, int d, int f, int top_k, int n_experts, const uint16_t* h,
+                              const float* h_bias, const GroupView& gv, const WaveArg& wave,
+                              const uint8_t* slot_bank, int64_t record_bytes, uint16_t* act,
+                              float* act_bias, hipStream_t stream);
+
+hipError_t launch_down_mfma(int tokens, int d, int f, int top_k, int n_experts, const uint16_t* act,
+                            const float* act_bias, const GroupView& gv, const WaveArg& wave,
                             const uint8_t* slot_bank, int64_t record_bytes, float* pair_out,
                             hipStream_t stream);
 

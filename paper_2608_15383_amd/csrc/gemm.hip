@@ -2,16 +2,28 @@
 // (prefill / large batches), where each expert's projection is a dense
 // contraction over its token rows.
 //
-// A workgroup owns one row-tile (up to 64 token rows of one expert, grouped
-// order) and one column tile of the expert's weights.  Token rows are staged
-// group by group (128 inputs) in LDS, double buffered, together with their
-// per-group sums.  Each wavefront loads its weight tiles straight from the
-// packed record: one coalesced 16-byte load per lane per tile, whose four
-// dwords expand in registers to the four B operands of
-// v_mfma_f32_16x16x32_bf16 (layout in common.h).  The codes enter the MFMA as
-// bf16 (128 + u); per group and output the fp32 result is corrected by
-// -136 * (row sum) and scaled by the FP16 group scale in fp32, so the
-// dequantized weight s * q is never rounded (Sec. 3.2).
+// A workgroup (8 wavefronts, one per SIMD pair) owns one row tile (up to 64
+// token rows of one expert, grouped order) and one column tile of 512 weight
+// rows; each wavefront owns 4 weight row-blocks (64 outputs) for all 64 rows.
+//  - Per 128-input group, the token rows (16 KB) and each wavefront's four
+//    packed weight tiles (4 KB) are copied from memory straight into LDS by
+//    buffer loads with the LDS destination (no register staging), in a ring of
+//    three stages, so every load is issued two groups ahead of its use.  The
+//    16-byte chunks of a token row are XOR-swizzled by the row index, which
+//    makes the MFMA A-fragment reads free of bank conflicts.
+//  - Each dword of codes expands in registers to one B operand of
+//    v_mfma_f32_16x16x32_bf16 (record layout in common.h): the codes enter as
+//    bf16 (128 + u), and the chain of four MFMAs of a group starts from the
+//    accumulator value -136 * (row sum of the group), precomputed per row, so
+//    the fp32 chain result is sum_k x_k * q_k with q = u - 8.  It is scaled by
+//    the FP16 group scale in fp32; the dequantized weight s * q is never
+//    rounded (Sec. 3.2).
+//  - The stages are handed over with one barrier per group; waits count only
+//    this wavefront's outstanding loads, so the two younger stages stay in
+//    flight across it.
+// Consecutive workgroups cover the column tiles of one row tile.
+#include <type_traits>
+
 #include "common.h"
 
 namespace emoe {
@@ -20,38 +32,94 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 4;
-constexpr int kRows = kMfmaRows;         // 64 token rows per tile
-constexpr int kLdsStride = kGroup + 8;   // staged row length in bf16 (16-byte pad)
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kNPW = 4;                                   // 16-row weight blocks per wavefront
+constexpr int kRows = kMfmaRows;                          // 64 token rows per tile
+constexpr int kCols = kWaves * kNPW * kTileRows;          // 512 weight rows per workgroup
+constexpr int kStages = 3;
+constexpr int kChunks = kGroup / 8;                       // 16-byte chunks per row and group
+constexpr int kBatchLoads = 2 + kNPW + kNPW + 1;          // loads one thread issues per group
+constexpr float kCodeBias = 136.f;                        // 128 (magic number) + 8 (offset binary)
 
-__device__ __forceinline__ bf16x8_t dequant_b(uint32_t dw) {
-  uint32_t p[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) p[j] = ((dw >> (4 * j)) & 0x000f000fu) | 0x43004300u;
-  return __builtin_bit_cast(bf16x8_t, make_uint4(p[0], p[1], p[2], p[3]));
+// One stage of the LDS ring.  The three stages are separate LDS variables, so
+// the compiler can tell the loads landing in one stage from the reads of
+// another and waits only for the stage being read.
+struct Stage {
+  uint16_t a[kRows * kGroup];            // token rows of the group (swizzled chunks)
+  uint8_t w[kWaves][kNPW][kTileBytes];   // each wavefront's four weight tiles
+  float bias[kWaves][kRows];             // -136 * row sums of the group (a copy per wavefront)
+};
+static_assert(kStages * sizeof(Stage) <= 160 * 1024, "LDS");
+static_assert(kWaves * kRows * 16 * sizeof(float) <= sizeof(Stage::a) + sizeof(Stage::w), "epilogue");
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-__device__ __forceinline__ float bf16x8_sum(const uint4 v) {
-  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-  float s = 0.f;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) s += bf16_to_f32(w[j] & 0xffffu) + bf16_to_f32(w[j] >> 16);
-  return s;
+// Buffer loads of 16 (4) bytes per lane into LDS at lds + 16 (4) * lane.
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rsrc, void* lds, uint32_t voffset,
+                                           uint32_t soffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)lds, 16,
+                                           (int)voffset, (int)soffset, 0, 0);
+}
+__device__ __forceinline__ void load_lds4(__amdgpu_buffer_rsrc_t rsrc, void* lds, uint32_t voffset,
+                                          uint32_t soffset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)lds, 4,
+                                           (int)voffset, (int)soffset, 0, 0);
 }
 
+// Wait until at most n of this wavefront's vector memory loads are in flight.
+template <int n>
+__device__ __forceinline__ void wait_loads() {
+  static_assert(n >= 0 && n < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier that orders LDS accesses but does not wait for loads.
+__device__ __forceinline__ void barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Four bf16 pairs (128 + u) from one dword of codes: ((dw >> 4p) & mask) |
+// magic.  The caller passes mask and magic as opaque register values, so the
+// compiler emits one v_and_or_b32 per pair (gfx9 VOP3 takes no literal) and
+// still sees every instruction for its MFMA operand hazard checks.
+__device__ __forceinline__ bf16x8_t dequant_b(uint32_t dw, uint32_t mask, uint32_t magic) {
+  const uint32_t p0 = (dw & mask) | magic;
+  const uint32_t p1 = ((dw >> 4) & mask) | magic;
+  const uint32_t p2 = ((dw >> 8) & mask) | magic;
+  const uint32_t p3 = ((dw >> 12) & mask) | magic;
+  return __builtin_bit_cast(bf16x8_t, make_uint4(p0, p1, p2, p3));
+}
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// kGateUp: x = h [tokens][d] gathered through the grouped pair ids, weights
+// W13, output act (bf16, grouped order) plus the bias table of act for the
+// down projection.  Otherwise: x = act [pairs][f] in grouped order, weights
+// W2, output pair_out (fp32, pair-id order).
 template <bool kGateUp>
-__global__ __launch_bounds__(256) void grouped_mfma_kernel(
-    int d, int f, int top_k, int n_experts, const uint16_t* __restrict__ x, GroupView gv,
-    WaveArg wave, const uint8_t* __restrict__ slot_bank, int64_t record_bytes,
-    uint16_t* __restrict__ act_out, float* __restrict__ pair_out) {
-  // 16-row weight blocks per wavefront: gate/up takes two (gate, up) pairs.
-  constexpr int NPW = kGateUp ? 4 : 2;
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][kRows][kLdsStride];
-  __shared__ __attribute__((aligned(16))) float hs[2][kRows];
+__global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
+    int d, int f, int top_k, int n_experts, const uint16_t* __restrict__ x, uint32_t x_bytes,
+    const float* __restrict__ x_bias, uint32_t bias_bytes, GroupView gv, WaveArg wave,
+    const uint8_t* __restrict__ slot_bank, int64_t record_bytes, uint16_t* __restrict__ act_out,
+    float* __restrict__ act_bias_out, float* __restrict__ pair_out) {
+  __shared__ __attribute__((aligned(16))) Stage st0;
+  __shared__ __attribute__((aligned(16))) Stage st1;
+  __shared__ __attribute__((aligned(16))) Stage st2;
+  auto stage_of = [&](auto stage) -> Stage& __attribute__((always_inline)) {
+    constexpr int S = decltype(stage)::value;
+    if constexpr (S == 0) return st0;
+    else if constexpr (S == 1) return st1;
+    else return st2;
+  };
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
-  const int wi = tid >> 6;
+  const int wi = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   // Row tile -> expert (largest e with tile_offsets[e] <= tile).
   const int tile = blockIdx.y;
@@ -69,124 +137,251 @@ __global__ __launch_bounds__(256) void grouped_mfma_kernel(
 
   const int K = kGateUp ? d : f;
   const int G = K / kGroup;
+  const int n_blocks = (kGateUp ? 2 * f : d) / kTileRows;
   const RecordLayout L = record_layout(d, f);
   const uint8_t* rec = slot_bank + (int64_t)slot * record_bytes;
-  const uint8_t* codes = rec + (kGateUp ? L.w13_codes : L.w2_codes);
-  const uint16_t* scales = reinterpret_cast<const uint16_t*>(rec + (kGateUp ? L.w13_scales : L.w2_scales));
-  const int rb0 = NPW * (blockIdx.x * kWaves + wi);
+  // A wavefront's 4 row blocks are all valid or all past the end (the number
+  // of row blocks is a multiple of 8); a wavefront past the end loads row
+  // block 0 so every wavefront issues the same loads, and computes nothing.
+  const int rb_raw = kNPW * (blockIdx.x * kWaves + wi);
+  const bool wvalid = rb_raw < n_blocks;
+  const int rb0 = wvalid ? rb_raw : 0;
   const int n_local = lane & 15;
   const int quarter = lane >> 4;
 
-  // Staging assignment: thread -> (row m, 32-input quarter c) of the group.
-  const int sm = tid >> 2;
-  const int sc = tid & 3;
-  const uint16_t* src = nullptr;
-  if (sm < rows) {
-    if (kGateUp) {
-      const int t = gv.sorted_pairs[row0 + sm] / top_k;
-      src = x + (int64_t)t * d;
-    } else {
-      src = x + (int64_t)(row0 + sm) * f;
-    }
-    src += 32 * sc;
-  }
-  uint4 stage[4];
-  auto fetch = [&](int g) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      stage[i] = src ? *reinterpret_cast<const uint4*>(src + g * kGroup + 8 * i)
-                     : make_uint4(0u, 0u, 0u, 0u);
+  const __amdgpu_buffer_rsrc_t x_rsrc = make_rsrc(x, x_bytes);
+  const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(x_bias, bias_bytes);
+  const __amdgpu_buffer_rsrc_t w_rsrc = make_rsrc(rec, (uint32_t)record_bytes);
+
+  // Source row of a tile row (rows past the tile's end repeat its last row;
+  // their results are discarded).
+  auto src_row = [&](int m) -> int __attribute__((always_inline)) {
+    const int mc = min(m, rows - 1);
+    return kGateUp ? gv.sorted_pairs[row0 + mc] / top_k : row0 + mc;
   };
-  auto commit = [&](int buf) {
-    float s = 0.f;
+  // Token-row chunks this thread copies: stage chunk (2*wi + j)*64 + lane is
+  // row m = 4*(2*wi + j) + lane/16, slot p = lane%16, holding chunk p ^ (m%16).
+  uint32_t a_off[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      *reinterpret_cast<uint4*>(&As[buf][sm][32 * sc + 8 * i]) = stage[i];
-      s += bf16x8_sum(stage[i]);
-    }
-    s += __shfl_xor(s, 1);
-    s += __shfl_xor(s, 2);
-    if (sc == 0) hs[buf][sm] = s;
+  for (int j = 0; j < 2; ++j) {
+    const int m = 4 * (2 * wi + j) + (lane >> 4);
+    const int c = (lane & 15) ^ (m & 15);
+    a_off[j] = (uint32_t)src_row(m) * (uint32_t)(K * 2) + 16u * c;
+  }
+  // Bias: every wavefront copies all 64 rows (lane = row) for itself.
+  const uint32_t b_off = (uint32_t)src_row(lane) * (uint32_t)(G * 4);
+  const uint32_t w_off = (uint32_t)((kGateUp ? L.w13_codes : L.w2_codes) +
+                                    (int64_t)rb0 * G * kTileBytes) + 16u * lane;
+  const uint32_t s_off = (uint32_t)((kGateUp ? L.w13_scales : L.w2_scales) +
+                                    ((int64_t)16 * rb0 + n_local) * G * 2);
+
+  uint16_t sc[kStages][kNPW];  // raw fp16 scales of the groups in flight
+
+  // Issue every load of group g into stage S (same count in every thread).
+  auto issue = [&](int g, auto stage) __attribute__((always_inline)) {
+    Stage& sm = stage_of(stage);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      load_lds16(x_rsrc, &sm.a[(2 * wi + j) * 64 * 8], a_off[j], (uint32_t)g * kGroup * 2);
+#pragma unroll
+    for (int r = 0; r < kNPW; ++r)
+      load_lds16(w_rsrc, &sm.w[wi][r][0], w_off + (uint32_t)(r * G * kTileBytes),
+                   (uint32_t)g * kTileBytes);
+#pragma unroll
+    for (int r = 0; r < kNPW; ++r)
+      sc[decltype(stage)::value][r] = __builtin_amdgcn_raw_buffer_load_b16(w_rsrc, (int)(s_off + (uint32_t)(r * 16 * G * 2)),
+                                                      g * 2, 0);
+    load_lds4(b_rsrc, &sm.bias[wi][0], b_off, (uint32_t)g * 4);
   };
 
-  f32x4_t acc[NPW][4];
+  // Dequantization constants, hidden from constant folding (the empty asm
+  // statements emit nothing): mask in an SGPR, magic in a VGPR.
+  uint32_t kMask = 0x000f000fu, kMagic = 0x43004300u;
+  asm("" : "+s"(kMask));
+  asm("" : "+v"(kMagic));
+
+  f32x4_t acc[kNPW][4];
 #pragma unroll
-  for (int r = 0; r < NPW; ++r)
+  for (int r = 0; r < kNPW; ++r)
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi) acc[r][mi] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  fetch(0);
-  commit(0);
-  __syncthreads();
-
-  for (int g = 0; g < G; ++g) {
-    const int buf = g & 1;
-    if (g + 1 < G) fetch(g + 1);
-    uint4 wc[NPW];
-    float ws[NPW];
+  auto compute = [&](auto stage) __attribute__((always_inline)) {
+    constexpr int S = decltype(stage)::value;
+    const Stage& sm = stage_of(stage);
+    f32x4_t c0[4];
 #pragma unroll
-    for (int r = 0; r < NPW; ++r) {
-      wc[r] = *reinterpret_cast<const uint4*>(codes + ((int64_t)(rb0 + r) * G + g) * kTileBytes +
-                                              16 * lane);
-      ws[r] = half_bits_to_f32(scales[(int64_t)(16 * (rb0 + r) + n_local) * G + g]);
-    }
-    f32x4_t tmp[NPW][4];
+    for (int mi = 0; mi < 4; ++mi)
+      c0[mi] = *reinterpret_cast<const f32x4_t*>(&sm.bias[wi][16 * mi + 4 * quarter]);
+    uint4 wc[kNPW];
 #pragma unroll
-    for (int r = 0; r < NPW; ++r)
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi) tmp[r][mi] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int r = 0; r < kNPW; ++r) wc[r] = *reinterpret_cast<const uint4*>(&sm.w[wi][r][16 * lane]);
+    f32x4_t tmp[kNPW][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       bf16x8_t a[4];
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
-        a[mi] = *reinterpret_cast<const bf16x8_t*>(&As[buf][16 * mi + n_local][32 * i + 8 * quarter]);
+      for (int mi = 0; mi < 4; ++mi) {
+        const int m = 16 * mi + n_local;
+        a[mi] = *reinterpret_cast<const bf16x8_t*>(&sm.a[m * kGroup + 8 * ((4 * i + quarter) ^ n_local)]);
+      }
 #pragma unroll
-      for (int r = 0; r < NPW; ++r) {
+      for (int r = 0; r < kNPW; ++r) {
         const uint32_t dw = i == 0 ? wc[r].x : i == 1 ? wc[r].y : i == 2 ? wc[r].z : wc[r].w;
-        const bf16x8_t b = dequant_b(dw);
+        const bf16x8_t b = dequant_b(dw, kMask, kMagic);
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi)
-          tmp[r][mi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], b, tmp[r][mi], 0, 0, 0);
+          tmp[r][mi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], b, i == 0 ? c0[mi] : tmp[r][mi], 0, 0, 0);
       }
     }
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi) {
-      const float4 hv = *reinterpret_cast<const float4*>(&hs[buf][16 * mi + 4 * quarter]);
-      const float hj[4] = {hv.x, hv.y, hv.z, hv.w};
+    for (int r = 0; r < kNPW; ++r) {
+      const float s = half_bits_to_f32(sc[S][r]);
 #pragma unroll
-      for (int r = 0; r < NPW; ++r)
+      for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[r][mi][j] = fmaf(ws[r], fmaf(-136.f, hj[j], tmp[r][mi][j]), acc[r][mi][j]);
+        for (int j = 0; j < 4; ++j) acc[r][mi][j] = fmaf(s, tmp[r][mi][j], acc[r][mi][j]);
     }
-    if (g + 1 < G) commit(buf ^ 1);
-    __syncthreads();
+  };
+
+  // One group: refill the stage freed by the previous group (kMore), compute,
+  // then wait for the next group's loads, leaving the newest batch in flight.
+  // Issuing is decided at compile time so the wait counts stay exact.
+  auto step = [&](int g, auto stage, auto more) __attribute__((always_inline)) {
+    constexpr int S = decltype(stage)::value;
+    constexpr bool kMore = decltype(more)::value;
+    if constexpr (kMore) issue(g + 2, std::integral_constant<int, (S + 2) % kStages>());
+    if (wvalid) compute(stage);
+    if constexpr (kMore) wait_loads<kBatchLoads>(); else wait_loads<0>();
+    barrier();
+  };
+  using Yes = std::true_type;
+  using No = std::false_type;
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  // Steps g .. g+lc-1 still issue; the last two do not.  Stages continue from 0.
+  auto tail = [&](int g, auto lc) __attribute__((always_inline)) {
+    constexpr int Lc = decltype(lc)::value;
+    if constexpr (Lc >= 1) step(g, S0(), Yes());
+    if constexpr (Lc >= 2) step(g + 1, S1(), Yes());
+    step(g + Lc, std::integral_constant<int, Lc % kStages>(), No());
+    step(g + Lc + 1, std::integral_constant<int, (Lc + 1) % kStages>(), No());
+  };
+
+  issue(0, S0());
+  if (G > 1) {
+    issue(1, S1());
+    wait_loads<kBatchLoads>();
+  } else {
+    wait_loads<0>();
+  }
+  barrier();
+  if (G == 1) {
+    step(0, S0(), No());
+  } else {
+    // Groups 0 .. G-3 issue a later group; whole triples run in the loop.
+    const int n_issue = G - 2;
+    int g = 0;
+    for (; g + kStages <= n_issue; g += kStages) {
+      step(g, S0(), Yes());
+      step(g + 1, S1(), Yes());
+      step(g + 2, S2(), Yes());
+    }
+    const int left = n_issue - g;
+    if (left == 0) tail(g, std::integral_constant<int, 0>());
+    else if (left == 1) tail(g, std::integral_constant<int, 1>());
+    else tail(g, std::integral_constant<int, 2>());
   }
 
-  // Epilogue.  Lane holds rows m = 16*mi + 4*quarter + j of output column n_local.
+  // Epilogue.  Lane holds rows m = 16*mi + 4*quarter + j of output column
+  // n_local of its row blocks.
+  if (kGateUp) {
+    // act = silu(gate) * up (row block 2p is gate, 2p+1 up), rounded to bf16,
+    // and per row the sum of the rounded values over each 128-column group
+    // (wavefronts 4h..4h+3 cover group 2*blockIdx.x + h), for the down bias.
+    float* part = reinterpret_cast<float*>(&st0);  // [kWaves][kRows][16]
 #pragma unroll
-  for (int mi = 0; mi < 4; ++mi) {
+    for (int mi = 0; mi < 4; ++mi) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int m = 16 * mi + 4 * quarter + j;
-      if (m >= rows) continue;
-      if (kGateUp) {
+      for (int j = 0; j < 4; ++j) {
+        const int m = 16 * mi + 4 * quarter + j;
+        float rs = 0.f;
 #pragma unroll
-        for (int p = 0; p < NPW / 2; ++p) {
+        for (int p = 0; p < kNPW / 2; ++p) {
           const float gv_ = acc[2 * p][mi][j];
           const float uv = acc[2 * p + 1][mi][j];
-          const float a = gv_ / (1.0f + expf(-gv_)) * uv;
+          const uint32_t ab = f32_to_bf16_rne(gv_ / (1.0f + expf(-gv_)) * uv);
+          rs += bf16_bits_to_f32(ab);
           const int col = 16 * ((rb0 >> 1) + p) + n_local;
-          act_out[(int64_t)(row0 + m) * f + col] = (uint16_t)f32_to_bf16_rne(a);
+          if (wvalid && m < rows) act_out[(int64_t)(row0 + m) * f + col] = (uint16_t)ab;
         }
-      } else {
+        part[(wi * kRows + m) * 16 + n_local] = rs;
+      }
+    }
+    barrier();
+    const int Gf = f / kGroup;
+    if (tid < 2 * kRows) {
+      const int h = tid / kRows, m = tid % kRows;
+      const int g = 2 * blockIdx.x + h;
+      if (m < rows && g < Gf) {
+        float s = 0.f;
+        for (int w = 4 * h; w < 4 * h + 4; ++w)
+#pragma unroll
+          for (int n = 0; n < 16; n += 4) {
+            const float4 v = *reinterpret_cast<const float4*>(&part[(w * kRows + m) * 16 + n]);
+            s += v.x;
+            s += v.y;
+            s += v.z;
+            s += v.w;
+          }
+        act_bias_out[(int64_t)(row0 + m) * Gf + g] = -kCodeBias * s;
+      }
+    }
+  } else {
+    if (!wvalid) return;
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int m = 16 * mi + 4 * quarter + j;
+        if (m >= rows) continue;
         const int pi = gv.sorted_pairs[row0 + m];
 #pragma unroll
-        for (int r = 0; r < NPW; ++r)
+        for (int r = 0; r < kNPW; ++r)
           pair_out[(int64_t)pi * d + 16 * (rb0 + r) + n_local] = acc[r][mi][j];
       }
     }
+  }
+}
+
+// bias[row][g] = -136 * sum of x[row][128g .. 128g+127] (fp32, fixed order):
+// the accumulator start of the MFMA chains for the gate/up projection.
+__global__ __launch_bounds__(256) void row_bias_kernel(int rows, int K, const uint16_t* __restrict__ x,
+                                                       float* __restrict__ bias) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int lane = lane_id();
+  const int G = K / kGroup;
+  const uint16_t* xr = x + (int64_t)row * K;
+  for (int c0 = 0; c0 < K / 8; c0 += 64) {
+    const int c = c0 + lane;
+    float s = 0.f;
+    if (c < K / 8) {
+      const uint4 v = *reinterpret_cast<const uint4*>(xr + 8 * c);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        s += bf16_bits_to_f32(w[q] & 0xffffu);
+        s += bf16_bits_to_f32(w[q] >> 16);
+      }
+    }
+    // Sum over the 16 lanes holding one group.
+    s += __shfl_xor(s, 1);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 4);
+    s += __shfl_xor(s, 8);
+    if ((lane & 15) == 0 && c < K / 8) bias[(int64_t)row * G + c / kChunks] = -kCodeBias * s;
   }
 }
 
@@ -197,28 +392,35 @@ inline int max_row_tiles(int pairs, int n_experts) {
 
 }  // namespace
 
-hipError_t launch_gateup_mfma(int d, int f, int top_k, int pairs, int n_experts,
-                              const uint16_t* h, const GroupView& gv, const WaveArg& wave,
-                              const uint8_t* slot_bank, int64_t record_bytes, uint16_t* act,
-                              hipStream_t stream) {
-  if (pairs == 0) return hipSuccess;
-  // Column tile: 4 wavefronts x 2 (gate, up) pairs x 16 outputs = 128 act columns.
-  dim3 grid(f / 128, max_row_tiles(pairs, n_experts));
-  launch(grouped_mfma_kernel<true>, grid, dim3(64 * kWaves), stream, d, f, top_k,
-                     n_experts, h, gv, wave, slot_bank, record_bytes, act, (float*)nullptr);
+hipError_t launch_row_bias(int rows, int K, const uint16_t* x, float* bias, hipStream_t stream) {
+  if (rows == 0) return hipSuccess;
+  launch(row_bias_kernel, dim3((rows + 3) / 4), dim3(256), stream, rows, K, x, bias);
   return hipGetLastError();
 }
 
-hipError_t launch_down_mfma(int d, int f, int top_k, int pairs, int n_experts,
-                            const uint16_t* act, const GroupView& gv, const WaveArg& wave,
+hipError_t launch_gateup_mfma(int tokens, int d, int f, int top_k, int n_experts, const uint16_t* h,
+                              const float* h_bias, const GroupView& gv, const WaveArg& wave,
+                              const uint8_t* slot_bank, int64_t record_bytes, uint16_t* act,
+                              float* act_bias, hipStream_t stream) {
+  const int pairs = tokens * top_k;
+  if (pairs == 0) return hipSuccess;
+  dim3 grid((2 * f + kCols - 1) / kCols, max_row_tiles(pairs, n_experts));
+  launch(grouped_mfma_kernel<true>, grid, dim3(kThreads), stream, d, f, top_k, n_experts, h,
+         (uint32_t)((int64_t)tokens * d * 2), h_bias, (uint32_t)((int64_t)tokens * (d / kGroup) * 4),
+         gv, wave, slot_bank, record_bytes, act, act_bias, (float*)nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_down_mfma(int tokens, int d, int f, int top_k, int n_experts, const uint16_t* act,
+                            const float* act_bias, const GroupView& gv, const WaveArg& wave,
                             const uint8_t* slot_bank, int64_t record_bytes, float* pair_out,
                             hipStream_t stream) {
+  const int pairs = tokens * top_k;
   if (pairs == 0) return hipSuccess;
-  // Column tile: 4 wavefronts x 2 row blocks x 16 outputs = 128 output columns.
-  dim3 grid(d / 128, max_row_tiles(pairs, n_experts));
-  launch(grouped_mfma_kernel<false>, grid, dim3(64 * kWaves), stream, d, f, top_k,
-                     n_experts, act, gv, wave, slot_bank, record_bytes, (uint16_t*)nullptr,
-                     pair_out);
+  dim3 grid((d + kCols - 1) / kCols, max_row_tiles(pairs, n_experts));
+  launch(grouped_mfma_kernel<false>, grid, dim3(kThreads), stream, d, f, top_k, n_experts, act,
+         (uint32_t)((int64_t)pairs * f * 2), act_bias, (uint32_t)((int64_t)pairs * (f / kGroup) * 4),
+         gv, wave, slot_bank, record_bytes, (uint16_t*)nullptr, (float*)nullptr, pair_out);
   return hipGetLastError();
 }
 
