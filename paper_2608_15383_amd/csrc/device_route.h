@@ -239,20 +239,33 @@ __device__ __forceinline__ int wave_exclusive_scan(int v, int& total) {
   return x - v;
 }
 
-// LDS of the block-wide grouping.
+// LDS of the block-wide grouping: per wavefront and expert, first the
+// wavefront's count, then its first grouped position.
 template <int kThreads>
 struct GroupShared {
-  int cnt[EMOE_MAX_EXPERTS];
-  int off[EMOE_MAX_EXPERTS];
-  int placed[EMOE_MAX_EXPERTS];
-  int wcnt[kThreads / 64][EMOE_MAX_EXPERTS];
+  int wbase[kThreads / 64][EMOE_MAX_EXPERTS];
 };
+
+// Lanes of the wavefront whose expert equals this lane's (valid lanes only),
+// found with one ballot per bit of the expert id.
+__device__ __forceinline__ uint64_t match_expert(bool valid, int e, int bits) {
+  uint64_t m = __ballot(valid);
+  for (int b = 0; b < bits; ++b) {
+    const bool set = (e >> b) & 1;
+    const uint64_t x = __ballot(valid && set);
+    m &= set ? x : ~x;
+  }
+  return m;
+}
 
 // Grouping of the P pairs by expert, by one workgroup of kThreads threads:
 // counts, exclusive offsets, a stable counting sort of the pair ids (pairs of
 // one expert keep ascending id), the ascending active list, n_active and,
 // when the pointers are non-null, the MFMA row-tile prefix sum and the
 // inverse permutation pair_pos[pi] = grouped position.
+// Each wavefront owns a contiguous range of 64-pair chunks: pass 1 counts its
+// pairs per expert, a scan turns the counts into each wavefront's first
+// position per expert, and pass 2 places its pairs in order.
 template <int kThreads, bool kCo>
 __device__ void block_group(GroupShared<kThreads>& sh, int pairs, int n_experts,
                             const int32_t* __restrict__ ids, int32_t* __restrict__ counts,
@@ -263,19 +276,37 @@ __device__ void block_group(GroupShared<kThreads>& sh, int pairs, int n_experts,
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid >> 6;
-  for (int e = tid; e < EMOE_MAX_EXPERTS; e += kThreads) {
-    sh.cnt[e] = 0;
-    sh.placed[e] = 0;
+  int bits = 0;
+  while ((1 << bits) < n_experts) ++bits;
+  const int n_chunks = (pairs + 63) / 64;
+  const int per_wave = (n_chunks + kWaves - 1) / kWaves;
+  const int c0 = min(n_chunks, wave * per_wave);
+  const int c1 = min(n_chunks, c0 + per_wave);
+  int* wb = sh.wbase[wave];
+  for (int e = lane; e < n_experts; e += 64) wb[e] = 0;
+
+  // Pass 1: this wavefront's count per expert.
+  int e_next = (c0 < c1 && lane < pairs - 64 * c0) ? ld_i32<kCo>(ids + 64 * c0 + lane) : 0;
+  for (int c = c0; c < c1; ++c) {
+    const int i = 64 * c + lane;
+    const bool valid = i < pairs;
+    const int e = e_next;
+    if (c + 1 < c1 && i + 64 < pairs) e_next = ld_i32<kCo>(ids + i + 64);
+    const uint64_t m = match_expert(valid, e, bits);
+    const int rank = __popcll(m & ((1ull << lane) - 1ull));
+    if (valid && rank == 0) wb[e] += __popcll(m);
   }
   __syncthreads();
-  for (int i = tid; i < pairs; i += kThreads) atomicAdd(&sh.cnt[ld_i32<kCo>(ids + i)], 1);
-  __syncthreads();
+
+  // Totals, offsets, active list, row tiles; then each wavefront's base.
   if (wave == 0) {
     int c[kPerLane], local = 0, nz = 0, tl = 0;
 #pragma unroll
     for (int q = 0; q < kPerLane; ++q) {
       const int e = kPerLane * lane + q;
-      c[q] = e < n_experts ? sh.cnt[e] : 0;
+      c[q] = 0;
+      if (e < n_experts)
+        for (int w = 0; w < kWaves; ++w) c[q] += sh.wbase[w][e];
       local += c[q];
       nz += c[q] > 0;
       tl += (c[q] + kMfmaRows - 1) / kMfmaRows;
@@ -288,11 +319,16 @@ __device__ void block_group(GroupShared<kThreads>& sh, int pairs, int n_experts,
     for (int q = 0; q < kPerLane; ++q) {
       const int e = kPerLane * lane + q;
       if (e < n_experts) {
-        sh.off[e] = base;
         st_u32<kCo>(counts + e, (uint32_t)c[q]);
         st_u32<kCo>(offsets + e, (uint32_t)base);
         if (tile_offsets) st_u32<kCo>(tile_offsets + e, (uint32_t)tl_base);
         if (c[q] > 0) st_u32<kCo>(active + nz_base++, (uint32_t)e);
+        int run = base;
+        for (int w = 0; w < kWaves; ++w) {
+          const int n = sh.wbase[w][e];
+          sh.wbase[w][e] = run;
+          run += n;
+        }
       }
       base += c[q];
       tl_base += (c[q] + kMfmaRows - 1) / kMfmaRows;
@@ -304,35 +340,23 @@ __device__ void block_group(GroupShared<kThreads>& sh, int pairs, int n_experts,
     }
   }
   __syncthreads();
-  int bits = 0;
-  while ((1 << bits) < n_experts) ++bits;
-  for (int base = 0; base < pairs; base += kThreads) {
-    for (int e = lane; e < EMOE_MAX_EXPERTS; e += 64) sh.wcnt[wave][e] = 0;
-    __syncthreads();
-    const int i = base + tid;
+
+  // Pass 2: stable placement.  Every lane reads its expert's base before the
+  // group leader advances it (one wavefront's LDS accesses run in order).
+  e_next = (c0 < c1 && lane < pairs - 64 * c0) ? ld_i32<kCo>(ids + 64 * c0 + lane) : 0;
+  for (int c = c0; c < c1; ++c) {
+    const int i = 64 * c + lane;
     const bool valid = i < pairs;
-    const int e = valid ? ld_i32<kCo>(ids + i) : 0;
-    uint64_t match = __ballot(valid);
-    for (int b = 0; b < bits; ++b) {
-      const uint64_t m = __ballot(valid && ((e >> b) & 1));
-      match &= ((e >> b) & 1) ? m : ~m;
-    }
-    const int rank = __popcll(match & ((1ull << lane) - 1ull));
-    if (valid && rank == 0) sh.wcnt[wave][e] = __popcll(match);
-    __syncthreads();
+    const int e = e_next;
+    if (c + 1 < c1 && i + 64 < pairs) e_next = ld_i32<kCo>(ids + i + 64);
+    const uint64_t m = match_expert(valid, e, bits);
+    const int rank = __popcll(m & ((1ull << lane) - 1ull));
     if (valid) {
-      int pos = sh.placed[e] + rank;
-      for (int w = 0; w < wave; ++w) pos += sh.wcnt[w][e];
-      st_u32<kCo>(sorted_pairs + sh.off[e] + pos, (uint32_t)i);
-      if (pair_pos) st_u32<kCo>(pair_pos + i, (uint32_t)(sh.off[e] + pos));
+      const int pos = wb[e] + rank;
+      st_u32<kCo>(sorted_pairs + pos, (uint32_t)i);
+      if (pair_pos) st_u32<kCo>(pair_pos + i, (uint32_t)pos);
     }
-    __syncthreads();
-    for (int x = tid; x < n_experts; x += kThreads) {
-      int s = 0;
-      for (int w = 0; w < kWaves; ++w) s += sh.wcnt[w][x];
-      sh.placed[x] += s;
-    }
-    __syncthreads();
+    if (valid && rank == 0) wb[e] += __popcll(m);
   }
 }
 

@@ -110,7 +110,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
   __shared__ __attribute__((aligned(16))) Stage st0;
   __shared__ __attribute__((aligned(16))) Stage st1;
   __shared__ __attribute__((aligned(16))) Stage st2;
-  auto stage_of = [&](auto stage) -> Stage& __attribute__((always_inline)) {
+  auto stage_of = [&](auto stage) __attribute__((always_inline)) -> Stage& {
     constexpr int S = decltype(stage)::value;
     if constexpr (S == 0) return st0;
     else if constexpr (S == 1) return st1;
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
 
   // Source row of a tile row (rows past the tile's end repeat its last row;
   // their results are discarded).
-  auto src_row = [&](int m) -> int __attribute__((always_inline)) {
+  auto src_row = [&](int m) __attribute__((always_inline)) -> int {
     const int mc = min(m, rows - 1);
     return kGateUp ? gv.sorted_pairs[row0 + mc] / top_k : row0 + mc;
   };

@@ -1,7 +1,8 @@
 // Routing and grouping kernels (Sec. 3.1 Eq. 1, Fig. 1 "tokens are grouped by
 // selected expert", Sec. 3.4).  The arithmetic lives in device_route.h.
 //
-//   router_logits_kernel: z[t][e] = fp32(sum_i h[t][i] * W_r[e][i]), fp64 sum.
+//   router_logits_kernel: z[t][e] = fp32(sum_i h[t][i] * W_r[e][i]), fp64 sum
+//                         on fp64 MFMA.
 //   topk_kernel:          k largest logits per token (ties -> lower expert id)
 //                         and their softmax mixture weights in fp64.
 //   group_kernel:         per-expert counts, exclusive offsets, a stable
@@ -12,19 +13,71 @@
 namespace emoe {
 namespace {
 
-// A wavefront computes a kTokW x kExpW block of logits.
-constexpr int kTokW = 4;
-constexpr int kExpW = 4;
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
+// Router logits on fp64 MFMA (v_mfma_f64_16x16x4f64): a workgroup computes a
+// 16-token x 16-expert tile and its four wavefronts split d into quarters.
+// Per 32 inputs, lane l loads 8 consecutive bf16 of token row l%16 and of
+// expert row l%16 (inputs 8*(l/16) .. +7) and feeds them to 8 MFMAs; A and B
+// take the same input for the same lane, so every product h_k * w_k is
+// formed once and exactly, and summed in fp64.  The four partial sums are
+// added in wavefront order and rounded once to fp32.
 __global__ __launch_bounds__(256) void router_logits_kernel(int tokens, int n_experts, int d,
                                                             const uint16_t* __restrict__ h,
                                                             const uint16_t* __restrict__ wr,
                                                             float* __restrict__ logits) {
+  __shared__ double part[4][4][64];
+  const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
-  const int t0 = blockIdx.x * kTokW;
-  const int e0 = (blockIdx.y * 4 + wave) * kExpW;
-  if (e0 >= n_experts) return;
-  wave_router_logits<kTokW, kExpW, false>(tokens, n_experts, d, t0, e0, h, wr, logits);
+  const int t0 = blockIdx.x * 16, e0 = blockIdx.y * 16;
+  const int row = lane & 15, q = lane >> 4;
+  // Rows past the end repeat the last row; their results are not stored.
+  const int t = min(t0 + row, tokens - 1);
+  const int e = min(e0 + row, n_experts - 1);
+  const int kq = d / 4;
+  const uint16_t* hp = h + (int64_t)t * d + wave * kq + 8 * q;
+  const uint16_t* wp = wr + (int64_t)e * d + wave * kq + 8 * q;
+  f64x4_t acc = {0.0, 0.0, 0.0, 0.0};
+  // Loads run kAhead steps of 32 inputs ahead of the MFMAs.
+  constexpr int kAhead = 4;
+  const int n = kq / 32;
+  uint4 hb[kAhead], wb[kAhead];
+#pragma unroll
+  for (int j = 0; j < kAhead; ++j) {
+    if (j < n) {
+      hb[j] = *reinterpret_cast<const uint4*>(hp + 32 * j);
+      wb[j] = *reinterpret_cast<const uint4*>(wp + 32 * j);
+    }
+  }
+  for (int i = 0; i < n; i += kAhead) {
+#pragma unroll
+    for (int j = 0; j < kAhead; ++j) {
+      if (i + j < n) {
+        double hv[8], wv[8];
+        bf16x8_to_f64(hb[j], hv);
+        bf16x8_to_f64(wb[j], wv);
+        if (i + j + kAhead < n) {
+          hb[j] = *reinterpret_cast<const uint4*>(hp + 32 * (i + j + kAhead));
+          wb[j] = *reinterpret_cast<const uint4*>(wp + 32 * (i + j + kAhead));
+        }
+#pragma unroll
+        for (int s = 0; s < 8; ++s) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(hv[s], wv[s], acc, 0, 0, 0);
+      }
+    }
+  }
+  // Lane l holds rows (tokens) l/16 + 4*r of column (expert) l%16 (the fp64
+  // MFMA interleaves its output rows by register).
+#pragma unroll
+  for (int r = 0; r < 4; ++r) part[wave][r][lane] = acc[r];
+  __syncthreads();
+  if (wave == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const double z = ((part[0][r][lane] + part[1][r][lane]) + part[2][r][lane]) + part[3][r][lane];
+      const int tt = t0 + q + 4 * r, ee = e0 + row;
+      if (tt < tokens && ee < n_experts) logits[(int64_t)tt * n_experts + ee] = (float)z;
+    }
+  }
 }
 
 __global__ __launch_bounds__(256) void topk_kernel(int tokens, int n_experts, int top_k,
@@ -53,7 +106,7 @@ __global__ __launch_bounds__(kGroupThreads) void group_kernel(
 hipError_t launch_router_logits(int tokens, int n_experts, int d, const uint16_t* h,
                                 const uint16_t* w_router, float* logits, hipStream_t stream) {
   if (tokens == 0) return hipSuccess;
-  dim3 grid((tokens + kTokW - 1) / kTokW, (n_experts + 4 * kExpW - 1) / (4 * kExpW));
+  dim3 grid((tokens + 15) / 16, (n_experts + 15) / 16);
   launch(router_logits_kernel, grid, dim3(256), stream, tokens, n_experts, d, h, w_router, logits);
   return hipGetLastError();
 }
