@@ -92,10 +92,13 @@ typedef struct emoe_ws_layout {
   size_t tile_offsets;  /* i32   [E+1]    MFMA row-tile prefix sum */
   size_t pair_pos;      /* i32   [T*k]    grouped position of each pair id (fused decode) */
   size_t act;           /* bf16  [T*k][d_ff]    phi(g)*u per pair, grouped order */
-  size_t pair_out;      /* f32   [T*k][d_model] expert output per pair id */
+  size_t pair_out;      /* expert output per pair id, [T*k][d_model]: f32 on the GEMV
+                           path, bf16 (in the first half of the field) on the MFMA path */
   size_t x_bias;        /* f32   [T][d_model/128]   -136 * group sums of h (MFMA path) */
   size_t act_bias;      /* f32   [T*k][d_ff/128]    -136 * group sums of act, grouped order
                                                       (MFMA path) */
+  size_t chunk_counts;  /* i32   [ceil(T*k/64)][E]  pairs per expert in each 64-pair chunk
+                                                      (grouping of large calls) */
   size_t total;         /* bytes needed */
 } emoe_ws_layout;
 
@@ -254,7 +257,7 @@ int32_t emoe_moe_forward_sequential(emoe_cache* cache, int32_t tokens, const uin
 enum emoe_kernel {
   EMOE_K_ROUTER = 0, EMOE_K_TOPK = 1, EMOE_K_GROUP = 2, EMOE_K_GATEUP_GEMV = 3,
   EMOE_K_DOWN_GEMV = 4, EMOE_K_GATEUP_MFMA = 5, EMOE_K_DOWN_MFMA = 6, EMOE_K_COMBINE = 7,
-  EMOE_K_DECODE_FUSED = 8, EMOE_K_ROW_BIAS = 9
+  EMOE_K_DECODE_FUSED = 8, EMOE_K_ROW_BIAS = 9, EMOE_K_GROUP_COUNT = 10
 };
 /* Start recording a HIP event pair around each kernel that emoe_route,
  * emoe_moe_forward and emoe_moe_forward_sequential launch from this thread,

@@ -37,7 +37,7 @@ class WsLayout(C.Structure):
     _fields_ = [(n, C.c_size_t) for n in ("logits", "topk_ids", "topk_w", "counts", "offsets",
                                           "sorted_pairs", "active", "n_active", "tile_offsets",
                                           "pair_pos", "act", "pair_out", "x_bias", "act_bias",
-                                          "total")]
+                                          "chunk_counts", "total")]
 
 
 _vp = C.c_void_p
@@ -76,7 +76,7 @@ SIGNATURES = {
 }
 
 KERNEL_NAMES = ["router", "topk", "group", "gateup_gemv", "down_gemv", "gateup_mfma", "down_mfma",
-                "combine", "decode_fused", "row_bias"]
+                "combine", "decode_fused", "row_bias", "group_count"]
 
 _lib = None
 

@@ -147,6 +147,7 @@ emoe_ws_layout make_layout(const emoe_dims& d, int32_t T) {
   L.pair_out = take(P * (size_t)d.d_model * 4);
   L.x_bias = take((size_t)T * (d.d_model / EMOE_GROUP) * 4);
   L.act_bias = take(P * (size_t)(d.d_ff / EMOE_GROUP) * 4);
+  L.chunk_counts = take((P + 63) / 64 * E * 4);
   L.total = off;
   return L;
 }
@@ -670,9 +671,18 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
     ds.kernel_launches += 1;
   }
   EMOE_LAUNCH(EMOE_K_TOPK, stream, launch_topk(T, E, k, renormalize, z, ids, wts, stream));
-  EMOE_LAUNCH(EMOE_K_GROUP, stream,
-              launch_group(P, E, ids, counts, offsets, sorted, active, n_active, tiles, stream));
-  ds.kernel_launches += 2;
+  if (P > kGroupWideMinPairs) {
+    int32_t* chunk_counts = reinterpret_cast<int32_t*>(ws + L.chunk_counts);
+    EMOE_LAUNCH(EMOE_K_GROUP_COUNT, stream, launch_group_count(P, E, ids, chunk_counts, stream));
+    EMOE_LAUNCH(EMOE_K_GROUP, stream,
+                launch_group_place(P, E, ids, chunk_counts, counts, offsets, sorted, active,
+                                   n_active, tiles, stream));
+    ds.kernel_launches += 3;
+  } else {
+    EMOE_LAUNCH(EMOE_K_GROUP, stream,
+                launch_group(P, E, ids, counts, offsets, sorted, active, n_active, tiles, stream));
+    ds.kernel_launches += 2;
+  }
   const GroupView gv{sorted, offsets, active, n_active, tiles};
   if (path == EMOE_PATH_MFMA) {
     // Accumulator start of the gate/up MFMA chains, once per call.
@@ -687,7 +697,7 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
                                      act, act_bias, stream));
       EMOE_LAUNCH(EMOE_K_DOWN_MFMA, stream,
                   launch_down_mfma(T, d, f, k, E, act, act_bias, gv, wa, c->slot_bank, c->record_bytes,
-                                   pair_out, stream));
+                                   reinterpret_cast<uint16_t*>(pair_out), stream));
     } else {
       EMOE_LAUNCH(EMOE_K_GATEUP_GEMV, stream,
                   launch_gateup_gemv(d, f, k, P, E, h, gv, wa, c->slot_bank, c->record_bytes, act, stream));
@@ -757,7 +767,8 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
         for (int i = 0; i < n; ++i) EMOE_HIP(hipEventRecord(c->release[smap[we[i]]], stream));
     }
   }
-  EMOE_LAUNCH(EMOE_K_COMBINE, stream, launch_combine(T, d, k, wts, pair_out, y, stream));
+  EMOE_LAUNCH(EMOE_K_COMBINE, stream,
+              launch_combine(T, d, k, wts, pair_out, path == EMOE_PATH_MFMA, y, stream));
   ds.kernel_launches += 1;
   add_stats(stats, ds);
   return EMOE_OK;

@@ -204,6 +204,17 @@ hipError_t launch_group(int pairs, int n_experts, const int32_t* topk_ids, int32
                         int32_t* offsets, int32_t* sorted_pairs, int32_t* active,
                         int32_t* n_active, int32_t* tile_offsets, hipStream_t stream);
 
+// The same grouping over many workgroups, for large calls (pairs > 0): per
+// 64-pair chunk expert counts into chunk_counts [ceil(pairs/64)][E], then the
+// offsets and a stable placement (identical results to launch_group).
+hipError_t launch_group_count(int pairs, int n_experts, const int32_t* topk_ids,
+                              int32_t* chunk_counts, hipStream_t stream);
+hipError_t launch_group_place(int pairs, int n_experts, const int32_t* topk_ids,
+                              const int32_t* chunk_counts, int32_t* counts, int32_t* offsets,
+                              int32_t* sorted_pairs, int32_t* active, int32_t* n_active,
+                              int32_t* tile_offsets, hipStream_t stream);
+constexpr int kGroupWideMinPairs = 1024;  // smaller calls group in one workgroup
+
 // Number of wave-local expert indices a grouped launch must cover.
 inline int grid_experts(const WaveArg& wave, int n_experts, int pairs) {
   if (wave.n >= 0) return wave.n;
@@ -230,12 +241,14 @@ hipError_t launch_gateup_mfma(int tokens, int d, int f, int top_k, int n_experts
                               const uint8_t* slot_bank, int64_t record_bytes, uint16_t* act,
                               float* act_bias, hipStream_t stream);
 
+// The MFMA down projection writes its pair outputs in bf16.
 hipError_t launch_down_mfma(int tokens, int d, int f, int top_k, int n_experts, const uint16_t* act,
                             const float* act_bias, const GroupView& gv, const WaveArg& wave,
-                            const uint8_t* slot_bank, int64_t record_bytes, float* pair_out,
+                            const uint8_t* slot_bank, int64_t record_bytes, uint16_t* pair_out,
                             hipStream_t stream);
 
-hipError_t launch_combine(int tokens, int d, int top_k, const float* topk_w,
-                          const float* pair_out, uint16_t* y, hipStream_t stream);
+// pair_out: fp32 (GEMV paths) or bf16 (pair_out_bf16, MFMA path).
+hipError_t launch_combine(int tokens, int d, int top_k, const float* topk_w, const void* pair_out,
+                          bool pair_out_bf16, uint16_t* y, hipStream_t stream);
 
 }  // namespace emoe

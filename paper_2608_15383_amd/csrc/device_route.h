@@ -285,16 +285,31 @@ __device__ void block_group(GroupShared<kThreads>& sh, int pairs, int n_experts,
   int* wb = sh.wbase[wave];
   for (int e = lane; e < n_experts; e += 64) wb[e] = 0;
 
+  // The expert ids of kBatch chunks are loaded together, so one memory
+  // latency covers kBatch chunks.
+  constexpr int kBatch = 8;
+  auto load_batch = [&](int cb, int (&eb)[kBatch]) {
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int i = 64 * (cb + j) + lane;
+      eb[j] = (cb + j < c1 && i < pairs) ? ld_i32<kCo>(ids + i) : 0;
+    }
+  };
+
   // Pass 1: this wavefront's count per expert.
-  int e_next = (c0 < c1 && lane < pairs - 64 * c0) ? ld_i32<kCo>(ids + 64 * c0 + lane) : 0;
-  for (int c = c0; c < c1; ++c) {
-    const int i = 64 * c + lane;
-    const bool valid = i < pairs;
-    const int e = e_next;
-    if (c + 1 < c1 && i + 64 < pairs) e_next = ld_i32<kCo>(ids + i + 64);
-    const uint64_t m = match_expert(valid, e, bits);
-    const int rank = __popcll(m & ((1ull << lane) - 1ull));
-    if (valid && rank == 0) wb[e] += __popcll(m);
+  for (int cb = c0; cb < c1; cb += kBatch) {
+    int eb[kBatch];
+    load_batch(cb, eb);
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (cb + j >= c1) break;
+      const int i = 64 * (cb + j) + lane;
+      const bool valid = i < pairs;
+      const int e = eb[j];
+      const uint64_t m = match_expert(valid, e, bits);
+      const int rank = __popcll(m & ((1ull << lane) - 1ull));
+      if (valid && rank == 0) wb[e] += __popcll(m);
+    }
   }
   __syncthreads();
 
@@ -343,20 +358,24 @@ __device__ void block_group(GroupShared<kThreads>& sh, int pairs, int n_experts,
 
   // Pass 2: stable placement.  Every lane reads its expert's base before the
   // group leader advances it (one wavefront's LDS accesses run in order).
-  e_next = (c0 < c1 && lane < pairs - 64 * c0) ? ld_i32<kCo>(ids + 64 * c0 + lane) : 0;
-  for (int c = c0; c < c1; ++c) {
-    const int i = 64 * c + lane;
-    const bool valid = i < pairs;
-    const int e = e_next;
-    if (c + 1 < c1 && i + 64 < pairs) e_next = ld_i32<kCo>(ids + i + 64);
-    const uint64_t m = match_expert(valid, e, bits);
-    const int rank = __popcll(m & ((1ull << lane) - 1ull));
-    if (valid) {
-      const int pos = wb[e] + rank;
-      st_u32<kCo>(sorted_pairs + pos, (uint32_t)i);
-      if (pair_pos) st_u32<kCo>(pair_pos + i, (uint32_t)pos);
+  for (int cb = c0; cb < c1; cb += kBatch) {
+    int eb[kBatch];
+    load_batch(cb, eb);
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (cb + j >= c1) break;
+      const int i = 64 * (cb + j) + lane;
+      const bool valid = i < pairs;
+      const int e = eb[j];
+      const uint64_t m = match_expert(valid, e, bits);
+      const int rank = __popcll(m & ((1ull << lane) - 1ull));
+      if (valid) {
+        const int pos = wb[e] + rank;
+        st_u32<kCo>(sorted_pairs + pos, (uint32_t)i);
+        if (pair_pos) st_u32<kCo>(pair_pos + i, (uint32_t)pos);
+      }
+      if (valid && rank == 0) wb[e] += __popcll(m);
     }
-    if (valid && rank == 0) wb[e] += __popcll(m);
   }
 }
 

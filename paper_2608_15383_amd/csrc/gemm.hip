@@ -100,13 +100,13 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as
 // kGateUp: x = h [tokens][d] gathered through the grouped pair ids, weights
 // W13, output act (bf16, grouped order) plus the bias table of act for the
 // down projection.  Otherwise: x = act [pairs][f] in grouped order, weights
-// W2, output pair_out (fp32, pair-id order).
+// W2, output pair_out (bf16, pair-id order).
 template <bool kGateUp>
 __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
     int d, int f, int top_k, int n_experts, const uint16_t* __restrict__ x, uint32_t x_bytes,
     const float* __restrict__ x_bias, uint32_t bias_bytes, GroupView gv, WaveArg wave,
     const uint8_t* __restrict__ slot_bank, int64_t record_bytes, uint16_t* __restrict__ act_out,
-    float* __restrict__ act_bias_out, float* __restrict__ pair_out) {
+    float* __restrict__ act_bias_out, uint16_t* __restrict__ pair_out) {
   __shared__ __attribute__((aligned(16))) Stage st0;
   __shared__ __attribute__((aligned(16))) Stage st1;
   __shared__ __attribute__((aligned(16))) Stage st2;
@@ -349,7 +349,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
         const int pi = gv.sorted_pairs[row0 + m];
 #pragma unroll
         for (int r = 0; r < kNPW; ++r)
-          pair_out[(int64_t)pi * d + 16 * (rb0 + r) + n_local] = acc[r][mi][j];
+          pair_out[(int64_t)pi * d + 16 * (rb0 + r) + n_local] = (uint16_t)f32_to_bf16_rne(acc[r][mi][j]);
       }
     }
   }
@@ -407,13 +407,13 @@ hipError_t launch_gateup_mfma(int tokens, int d, int f, int top_k, int n_experts
   dim3 grid((2 * f + kCols - 1) / kCols, max_row_tiles(pairs, n_experts));
   launch(grouped_mfma_kernel<true>, grid, dim3(kThreads), stream, d, f, top_k, n_experts, h,
          (uint32_t)((int64_t)tokens * d * 2), h_bias, (uint32_t)((int64_t)tokens * (d / kGroup) * 4),
-         gv, wave, slot_bank, record_bytes, act, act_bias, (float*)nullptr);
+         gv, wave, slot_bank, record_bytes, act, act_bias, (uint16_t*)nullptr);
   return hipGetLastError();
 }
 
 hipError_t launch_down_mfma(int tokens, int d, int f, int top_k, int n_experts, const uint16_t* act,
                             const float* act_bias, const GroupView& gv, const WaveArg& wave,
-                            const uint8_t* slot_bank, int64_t record_bytes, float* pair_out,
+                            const uint8_t* slot_bank, int64_t record_bytes, uint16_t* pair_out,
                             hipStream_t stream) {
   const int pairs = tokens * top_k;
   if (pairs == 0) return hipSuccess;

@@ -71,9 +71,11 @@ __global__ __launch_bounds__(256) void down_gemv_kernel(int d, int f, int top_k,
 }
 
 // y[t] = sum_j p[t][j] * o[t*k + j], j in rank order, fp32, rounded to bf16.
+// The pair outputs o are fp32 (kBf16 = false) or bf16.
+template <bool kBf16>
 __global__ __launch_bounds__(256) void combine_kernel(int tokens, int d, int top_k,
                                                       const float* __restrict__ topk_w,
-                                                      const float* __restrict__ pair_out,
+                                                      const void* __restrict__ pair_out,
                                                       uint16_t* __restrict__ y) {
   const int quads = d / 4;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -84,7 +86,14 @@ __global__ __launch_bounds__(256) void combine_kernel(int tokens, int d, int top
   for (int j = 0; j < top_k; ++j) {
     const int64_t pi = (int64_t)t * top_k + j;
     const float w = topk_w[pi];
-    const float4 o = *reinterpret_cast<const float4*>(pair_out + pi * d + 4 * c);
+    float4 o;
+    if (kBf16) {
+      const uint2 v = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(pair_out) + pi * d + 4 * c);
+      o = make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                      __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+    } else {
+      o = *reinterpret_cast<const float4*>(static_cast<const float*>(pair_out) + pi * d + 4 * c);
+    }
     acc.x = fmaf(w, o.x, acc.x);
     acc.y = fmaf(w, o.y, acc.y);
     acc.z = fmaf(w, o.z, acc.z);
@@ -119,12 +128,15 @@ hipError_t launch_down_gemv(int d, int f, int top_k, int pairs, int n_experts,
   return hipGetLastError();
 }
 
-hipError_t launch_combine(int tokens, int d, int top_k, const float* topk_w,
-                          const float* pair_out, uint16_t* y, hipStream_t stream) {
+hipError_t launch_combine(int tokens, int d, int top_k, const float* topk_w, const void* pair_out,
+                          bool pair_out_bf16, uint16_t* y, hipStream_t stream) {
   const int64_t n = (int64_t)tokens * (d / 4);
   if (n == 0) return hipSuccess;
-  launch(combine_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), stream, tokens, d, top_k,
-         topk_w, pair_out, y);
+  const dim3 grid((unsigned)((n + 255) / 256));
+  if (pair_out_bf16)
+    launch(combine_kernel<true>, grid, dim3(256), stream, tokens, d, top_k, topk_w, pair_out, y);
+  else
+    launch(combine_kernel<false>, grid, dim3(256), stream, tokens, d, top_k, topk_w, pair_out, y);
   return hipGetLastError();
 }
 

@@ -101,7 +101,157 @@ __global__ __launch_bounds__(kGroupThreads) void group_kernel(
                                     active, n_active, tile_offsets, nullptr);
 }
 
+// Grouping spread over many workgroups (large calls): 64-pair chunks, one per
+// wavefront, kChunkWaves chunks per workgroup.
+constexpr int kChunkWaves = 16;
+
+// chunk_counts[c][e]: pairs of chunk c (pairs 64c .. 64c+63) routed to e.
+__global__ __launch_bounds__(64 * kChunkWaves) void chunk_count_kernel(
+    int pairs, int n_experts, const int32_t* __restrict__ ids, int32_t* __restrict__ chunk_counts) {
+  __shared__ int row[kChunkWaves][EMOE_MAX_EXPERTS];
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int c = blockIdx.x * kChunkWaves + wave;
+  if (c >= (pairs + 63) / 64) return;  // whole wavefront; no barrier below
+  int bits = 0;
+  while ((1 << bits) < n_experts) ++bits;
+  int* r = row[wave];
+  for (int e = lane; e < n_experts; e += 64) r[e] = 0;
+  const int i = 64 * c + lane;
+  const bool valid = i < pairs;
+  const int e = valid ? ids[i] : 0;
+  const uint64_t m = match_expert(valid, e, bits);
+  const int rank = __popcll(m & ((1ull << lane) - 1ull));
+  if (valid && rank == 0) r[e] = __popcll(m);  // one wavefront: LDS accesses stay in order
+  for (int x = lane; x < n_experts; x += 64) chunk_counts[(int64_t)c * n_experts + x] = r[x];
+}
+
+// Each workgroup sums the chunk table (all chunks, and those before its own),
+// derives the exclusive offsets and its chunks' first positions per expert,
+// and places its chunks' pairs in order (stable).  Workgroup 0 also writes
+// counts, offsets, the active list, n_active and the row-tile prefix sum.
+__global__ __launch_bounds__(64 * kChunkWaves) void chunk_place_kernel(
+    int pairs, int n_experts, const int32_t* __restrict__ ids,
+    const int32_t* __restrict__ chunk_counts, int32_t* __restrict__ counts,
+    int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_pairs,
+    int32_t* __restrict__ active, int32_t* __restrict__ n_active,
+    int32_t* __restrict__ tile_offsets) {
+  __shared__ int part_all[kChunkWaves][EMOE_MAX_EXPERTS];
+  __shared__ int part_pre[kChunkWaves][EMOE_MAX_EXPERTS];
+  __shared__ int base[kChunkWaves][EMOE_MAX_EXPERTS];
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int n_chunks = (pairs + 63) / 64;
+  const int c0 = blockIdx.x * kChunkWaves;
+  // Wavefront w sums chunks w, w + 16, ...: all of them, and those before c0.
+#pragma unroll
+  for (int q = 0; q < kPerLane; ++q) {
+    const int e = 64 * q + lane;
+    if (e >= n_experts) break;
+    int all = 0, pre = 0;
+    // Loads in batches of 8, so one memory latency covers 8 chunks.
+    for (int cb = wave; cb < n_chunks; cb += 8 * kChunkWaves) {
+      int v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int c = cb + j * kChunkWaves;
+        v[j] = c < n_chunks ? chunk_counts[(int64_t)c * n_experts + e] : 0;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        all += v[j];
+        if (cb + j * kChunkWaves < c0) pre += v[j];
+      }
+    }
+    part_all[wave][e] = all;
+    part_pre[wave][e] = pre;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    int cnt[kPerLane], pre[kPerLane], local = 0, nz = 0, tl = 0;
+#pragma unroll
+    for (int q = 0; q < kPerLane; ++q) {
+      const int e = kPerLane * lane + q;
+      cnt[q] = 0;
+      pre[q] = 0;
+      if (e < n_experts)
+        for (int w = 0; w < kChunkWaves; ++w) {
+          cnt[q] += part_all[w][e];
+          pre[q] += part_pre[w][e];
+        }
+      local += cnt[q];
+      nz += cnt[q] > 0;
+      tl += (cnt[q] + kMfmaRows - 1) / kMfmaRows;
+    }
+    int total, nz_total, tl_total;
+    int off = wave_exclusive_scan(local, total);
+    int nz_base = wave_exclusive_scan(nz, nz_total);
+    int tl_base = wave_exclusive_scan(tl, tl_total);
+    const bool writer = blockIdx.x == 0;
+#pragma unroll
+    for (int q = 0; q < kPerLane; ++q) {
+      const int e = kPerLane * lane + q;
+      if (e < n_experts) {
+        if (writer) {
+          counts[e] = cnt[q];
+          offsets[e] = off;
+          tile_offsets[e] = tl_base;
+          if (cnt[q] > 0) active[nz_base++] = e;
+        }
+        int own[kChunkWaves];
+#pragma unroll
+        for (int w = 0; w < kChunkWaves; ++w)
+          own[w] = c0 + w < n_chunks ? chunk_counts[(int64_t)(c0 + w) * n_experts + e] : 0;
+        int run = off + pre[q];
+#pragma unroll
+        for (int w = 0; w < kChunkWaves; ++w) {
+          base[w][e] = run;
+          run += own[w];
+        }
+      }
+      off += cnt[q];
+      tl_base += (cnt[q] + kMfmaRows - 1) / kMfmaRows;
+    }
+    if (writer && lane == 0) {
+      offsets[n_experts] = total;
+      tile_offsets[n_experts] = tl_total;
+      *n_active = nz_total;
+    }
+  }
+  __syncthreads();
+  const int c = c0 + wave;
+  if (c >= n_chunks) return;
+  int bits = 0;
+  while ((1 << bits) < n_experts) ++bits;
+  const int i = 64 * c + lane;
+  const bool valid = i < pairs;
+  const int e = valid ? ids[i] : 0;
+  const uint64_t m = match_expert(valid, e, bits);
+  const int rank = __popcll(m & ((1ull << lane) - 1ull));
+  if (valid) sorted_pairs[base[wave][e] + rank] = i;
+}
+
 }  // namespace
+
+hipError_t launch_group_count(int pairs, int n_experts, const int32_t* topk_ids,
+                              int32_t* chunk_counts, hipStream_t stream) {
+  const int n_wg = ((pairs + 63) / 64 + kChunkWaves - 1) / kChunkWaves;
+  if (n_wg == 0) return hipSuccess;
+  launch(chunk_count_kernel, dim3(n_wg), dim3(64 * kChunkWaves), stream, pairs, n_experts, topk_ids,
+         chunk_counts);
+  return hipGetLastError();
+}
+
+hipError_t launch_group_place(int pairs, int n_experts, const int32_t* topk_ids,
+                              const int32_t* chunk_counts, int32_t* counts, int32_t* offsets,
+                              int32_t* sorted_pairs, int32_t* active, int32_t* n_active,
+                              int32_t* tile_offsets, hipStream_t stream) {
+  const int n_wg = ((pairs + 63) / 64 + kChunkWaves - 1) / kChunkWaves;
+  if (n_wg == 0) return hipSuccess;
+  launch(chunk_place_kernel, dim3(n_wg), dim3(64 * kChunkWaves), stream, pairs, n_experts, topk_ids,
+         chunk_counts, counts, offsets, sorted_pairs, active, n_active, tile_offsets);
+  return hipGetLastError();
+}
 
 hipError_t launch_router_logits(int tokens, int n_experts, int d, const uint16_t* h,
                                 const uint16_t* w_router, float* logits, hipStream_t stream) {

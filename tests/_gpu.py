@@ -80,6 +80,14 @@ class Layer:
         torch.cuda.synchronize()
         return bf16_bits_to_f32(host_bits(y))
 
+    def pair_out(self, pairs: int, mfma: bool) -> np.ndarray:
+        """Pair outputs of the last call as float32 [pairs][d_model] (the MFMA
+        path stores them in bf16, the GEMV path in fp32)."""
+        d = self.dm.d_model
+        if mfma:
+            return bf16_bits_to_f32(self.ws_array("pair_out", pairs * d, np.uint16)).reshape(pairs, d)
+        return self.ws_array("pair_out", pairs * d, np.float32).reshape(pairs, d)
+
     def ws_array(self, name: str, count: int, dtype) -> np.ndarray:
         """Copy of a workspace array written by the last forward call."""
         off = getattr(api.workspace_layout(self.dm, self.tokens), name)

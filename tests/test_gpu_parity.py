@@ -155,7 +155,7 @@ def test_forward_tiny_config(path):
     y = layer.forward(lay.h, path=path)
     ref, r = oracle_y(lay, LazyExperts(lay), TINY.top_k)
     assert_close(y, ref, f"tiny path={path}")
-    po = layer.ws_array("pair_out", 16 * 2 * 256, np.float32).reshape(32, 256)
+    po = layer.pair_out(32, mfma=path == MFMA)
     assert_close(po, O.pair_outputs(lay.f32("h"), LazyExperts(lay), r, range(32)), "tiny pairs")
 
 
@@ -170,6 +170,27 @@ def test_forward_ragged_and_degenerate_shapes(shape, tokens, path):
     y = layer.forward(lay.h, path=path)
     ref, _ = oracle_y(lay, LazyExperts(lay), shape.top_k)
     assert_close(y, ref, f"{shape} T={tokens} path={path}")
+
+
+@pytest.mark.parametrize("shape,tokens", [(LayerShape(128, 128, 200, 5), 300),
+                                          (LayerShape(128, 128, 64, 8), 2048)])
+def test_forward_grouping_of_large_calls_bit_exact(shape, tokens):
+    """Calls above 1024 pairs group over many workgroups (per-chunk counts, then
+    a stable placement); the arrays must equal the oracle's grouping."""
+    lay = make_layer(shape, tokens, seed=5)
+    layer = Layer(dims_of(shape), lay, tokens)
+    layer.forward(lay.h, path=GEMV)
+    E, P = shape.n_experts, tokens * shape.top_k
+    r = O.route(lay.f32("h"), lay.f32("w_router"), shape.top_k)
+    gr = O.group_by_expert(r.ids, E)
+    assert np.array_equal(layer.ws_array("topk_ids", P, np.int32).reshape(tokens, -1), r.ids)
+    assert np.array_equal(layer.ws_array("counts", E, np.int32), gr.counts)
+    assert np.array_equal(layer.ws_array("offsets", E + 1, np.int32), gr.offsets)
+    assert np.array_equal(layer.ws_array("sorted_pairs", P, np.int32), gr.sorted_pairs)
+    assert layer.ws_array("n_active", 1, np.int32)[0] == len(gr.active)
+    assert np.array_equal(layer.ws_array("active", len(gr.active), np.int32), gr.active)
+    tiles = np.concatenate([[0], np.cumsum(-(-gr.counts // 64))])
+    assert np.array_equal(layer.ws_array("tile_offsets", E + 1, np.int32), tiles)
 
 
 @pytest.mark.parametrize("path", [GEMV, MFMA])
@@ -293,7 +314,7 @@ def test_prefill_full_size_sampled(olmoe):
     gr = O.group_by_expert(r.ids, 64)
     assert np.array_equal(layer.ws_array("counts", 64, np.int32), gr.counts)
     assert np.array_equal(layer.ws_array("sorted_pairs", 16384, np.int32), gr.sorted_pairs)
-    po = layer.ws_array("pair_out", 16384 * 2048, np.float32).reshape(16384, 2048)
+    po = layer.pair_out(16384, mfma=True)
     for e in (int(gr.active[0]), int(gr.active[31]), int(gr.active[-1])):
         seg = gr.sorted_pairs[gr.offsets[e]:gr.offsets[e + 1]]
         pick = np.concatenate([seg[:3], seg[63:66], seg[-3:]])  # head, tile edge, ragged tail
