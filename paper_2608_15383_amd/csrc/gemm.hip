@@ -51,7 +51,8 @@ struct Stage {
   float bias[kWaves][kRows];             // -136 * row sums of the group (a copy per wavefront)
 };
 static_assert(kStages * sizeof(Stage) <= 160 * 1024, "LDS");
-static_assert(kWaves * kRows * 16 * sizeof(float) <= sizeof(Stage::a) + sizeof(Stage::w), "epilogue");
+static_assert(kRows * (kCols / 2 + 8) * 2 <= sizeof(Stage), "gate/up epilogue tile");
+static_assert(kRows / 2 * (kCols + 8) * 2 <= sizeof(Stage), "down epilogue half tile");
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
@@ -96,6 +97,14 @@ __device__ __forceinline__ bf16x8_t dequant_b(uint32_t dw, uint32_t mask, uint32
 }
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// silu(x) = x / (1 + e^-x) with the hardware exp2 and reciprocal (about 1 ulp
+// each in fp32; the result is rounded to bf16 next).  Large negative x gives
+// e^-x = inf and a zero reciprocal, so silu -> -0 as in exact arithmetic.
+__device__ __forceinline__ float silu_fast(float x) {
+  const float e = __builtin_amdgcn_exp2f(-x * 1.44269504088896340736f);
+  return x * __builtin_amdgcn_rcpf(1.0f + e);
+}
 
 // kGateUp: x = h [tokens][d] gathered through the grouped pair ids, weights
 // W13, output act (bf16, grouped order) plus the bias table of act for the
@@ -295,61 +304,78 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
   }
 
   // Epilogue.  Lane holds rows m = 16*mi + 4*quarter + j of output column
-  // n_local of its row blocks.
+  // n_local of its row blocks.  Outputs are rounded to bf16, staged in LDS
+  // (the stages are free now) and written as 16-byte chunks.
   if (kGateUp) {
-    // act = silu(gate) * up (row block 2p is gate, 2p+1 up), rounded to bf16,
-    // and per row the sum of the rounded values over each 128-column group
-    // (wavefronts 4h..4h+3 cover group 2*blockIdx.x + h), for the down bias.
-    float* part = reinterpret_cast<float*>(&st0);  // [kWaves][kRows][16]
+    // act = silu(gate) * up (row block 2p is gate, 2p+1 up); the workgroup's
+    // 256 act columns start at 256 * blockIdx.x.
+    constexpr int kStride = 256 + 8;  // row pitch in bf16 (padded against bank conflicts)
+    uint16_t* tile_act = reinterpret_cast<uint16_t*>(&st0);
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi) {
+    for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int m = 16 * mi + 4 * quarter + j;
-        float rs = 0.f;
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int p = 0; p < kNPW / 2; ++p) {
           const float gv_ = acc[2 * p][mi][j];
           const float uv = acc[2 * p + 1][mi][j];
-          const uint32_t ab = f32_to_bf16_rne(gv_ / (1.0f + expf(-gv_)) * uv);
-          rs += bf16_bits_to_f32(ab);
-          const int col = 16 * ((rb0 >> 1) + p) + n_local;
-          if (wvalid && m < rows) act_out[(int64_t)(row0 + m) * f + col] = (uint16_t)ab;
+          tile_act[(16 * mi + 4 * quarter + j) * kStride + 16 * (2 * wi + p) + n_local] =
+              (uint16_t)f32_to_bf16_rne(silu_fast(gv_) * uv);
         }
-        part[(wi * kRows + m) * 16 + n_local] = rs;
-      }
-    }
     barrier();
+    // Thread t copies chunks (row t/32 + 16q, column chunk t%32) and sums
+    // each chunk; the 16 threads of one 128-column group then add their sums
+    // (butterfly), giving the bias of that row and group for the down kernel.
+    const int cc = tid & 31;
+    const int col = 256 * blockIdx.x + 8 * cc;
     const int Gf = f / kGroup;
-    if (tid < 2 * kRows) {
-      const int h = tid / kRows, m = tid % kRows;
-      const int g = 2 * blockIdx.x + h;
-      if (m < rows && g < Gf) {
-        float s = 0.f;
-        for (int w = 4 * h; w < 4 * h + 4; ++w)
+    const int g = col / kGroup;
 #pragma unroll
-          for (int n = 0; n < 16; n += 4) {
-            const float4 v = *reinterpret_cast<const float4*>(&part[(w * kRows + m) * 16 + n]);
-            s += v.x;
-            s += v.y;
-            s += v.z;
-            s += v.w;
-          }
-        act_bias_out[(int64_t)(row0 + m) * Gf + g] = -kCodeBias * s;
+    for (int q = 0; q < 4; ++q) {
+      const int m = (tid >> 5) + 16 * q;
+      const uint4 v = *reinterpret_cast<const uint4*>(&tile_act[m * kStride + 8 * cc]);
+      const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+      float sum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        sum += bf16_bits_to_f32(w4[e] & 0xffffu);
+        sum += bf16_bits_to_f32(w4[e] >> 16);
+      }
+      sum += __shfl_xor(sum, 1);
+      sum += __shfl_xor(sum, 2);
+      sum += __shfl_xor(sum, 4);
+      sum += __shfl_xor(sum, 8);
+      if (m < rows && col < f) {
+        *reinterpret_cast<uint4*>(act_out + (int64_t)(row0 + m) * f + col) = v;
+        if ((tid & 15) == 0) act_bias_out[(int64_t)(row0 + m) * Gf + g] = -kCodeBias * sum;
       }
     }
   } else {
-    if (!wvalid) return;
+    // Rows 0..31 are staged in stage 0, rows 32..63 in stage 1.
+    constexpr int kStride = kCols + 8;
+    uint16_t* half0 = reinterpret_cast<uint16_t*>(&st0);
+    uint16_t* half1 = reinterpret_cast<uint16_t*>(&st1);
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi) {
+      uint16_t* t = mi < 2 ? half0 : half1;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int m = 16 * mi + 4 * quarter + j;
-        if (m >= rows) continue;
-        const int pi = gv.sorted_pairs[row0 + m];
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int r = 0; r < kNPW; ++r)
-          pair_out[(int64_t)pi * d + 16 * (rb0 + r) + n_local] = (uint16_t)f32_to_bf16_rne(acc[r][mi][j]);
+          t[(16 * (mi & 1) + 4 * quarter + j) * kStride + 16 * (kNPW * wi + r) + n_local] =
+              (uint16_t)f32_to_bf16_rne(acc[r][mi][j]);
+    }
+    barrier();
+    const int cc = tid & 63;
+    const int col = kCols * blockIdx.x + 8 * cc;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int m = (tid >> 6) + 8 * q;
+      const uint16_t* t = m < 32 ? half0 : half1;
+      if (m < rows && col < d) {
+        const uint4 v = *reinterpret_cast<const uint4*>(&t[(m & 31) * kStride + 8 * cc]);
+        const int pi = gv.sorted_pairs[row0 + m];
+        *reinterpret_cast<uint4*>(pair_out + (int64_t)pi * d + col) = v;
       }
     }
   }
