@@ -1,6 +1,7 @@
 """Benchmark of the MI355X fused W4A16 routed-expert layer on one GPU.
 
-    python bench.py [--steps K] [--warmup W] [--workload decode|prefill] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload decode|prefill|multiwave|stack]
+                    [--no-cpu-baseline]
 
 A step is one full layer call (route, group, grouped gate/up+SwiGLU, grouped
 down, combine) on OLMoE-shaped synthetic inputs (d_model 2048, d_ff 1024,
@@ -12,6 +13,16 @@ decode  : 1 token, all 64 experts resident; 16 distinct expert banks are
           256 MB last-level cache across steps.  value = algorithmic HBM GB/s.
 prefill : 2048 tokens (16,384 token-expert pairs), all experts resident.
           value = expert TFLOP/s.
+multiwave: 16 tokens through a 16-slot cache backed by a pinned host bank of
+          the 64 packed experts; routing logits select 40/48/56/64 distinct
+          experts (3-4 waves).  Fused and per-expert sequential paths, cold
+          (empty slots) and warm (experts 0-15 resident), end to end (fills
+          included) and kernels only.  value = fused warm tokens/s at 56
+          experts.
+stack   : 16 layers x 64 experts (1024 packed records in one pinned host
+          bank), a 16-slot cache per layer, 64 tokens per step, Zipf(1.1)
+          expert popularity per layer (Gumbel top-8).  value = tokens/s over
+          32 steps of 16 layer calls; H2D bytes and hit rates reported.
 """
 from __future__ import annotations
 
@@ -37,7 +48,8 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=None)
     p.add_argument("--warmup", type=int, default=None)
-    p.add_argument("--workload", default="decode", choices=["decode", "prefill"])
+    p.add_argument("--workload", default="decode",
+                   choices=["decode", "prefill", "multiwave", "stack"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
 
@@ -107,12 +119,7 @@ def oracle_baseline(weights, wr, h, k, alg_bytes, flops, unit, budget_s=12.0):
                    seconds_per_call=per_call)
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              f"(the layer runs on a single device).", file=sys.stderr)
-        sys.exit(2)
+def bench_layer(args):
     import torch
     from paper_2608_15383_amd import api
 
@@ -230,6 +237,250 @@ def main():
             cpu["sample"] += "; 8 tokens of the 2048-token batch"
         out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
+
+
+def quantized_host_bank(api, dm, torch, seeds):
+    """Packed records of len(seeds) 64-expert layers in one pinned host bank."""
+    rec = api.expert_record_bytes(dm)
+    host = torch.empty(len(seeds) * N_EXPERTS * rec, dtype=torch.uint8, pin_memory=True)
+    raw = []
+    for li, seed in enumerate(seeds):
+        bank, cache, weights = make_bank(api, dm, torch, seed)
+        host[li * N_EXPERTS * rec:(li + 1) * N_EXPERTS * rec].copy_(bank)
+        if li == 0:
+            raw = weights
+        cache.close()
+        del bank, cache, weights
+    torch.cuda.synchronize()
+    return host, raw
+
+
+def pinned_h2d_gbs(torch, host):
+    """Measured pinned host -> device copy bandwidth (hipMemcpyAsync)."""
+    n = min(host.numel(), 256 << 20)
+    dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst.copy_(host[:n], non_blocking=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(4):
+        dst.copy_(host[:n], non_blocking=True)
+    torch.cuda.synchronize()
+    return 4 * n / (time.perf_counter() - t0) / 1e9
+
+
+def bench_multiwave(args):
+    """16 tokens, 16 slots, 40-64 distinct experts: fused vs sequential waves."""
+    import torch
+    from paper_2608_15383_amd import api
+    from paper_2608_15383_amd.inputs import spread_logits
+
+    torch.cuda.init()
+    dm = api.dims(D_MODEL, D_FF, N_EXPERTS, TOP_K)
+    T, C = 16, 16
+    reps = args.steps or 5
+    rec = api.expert_record_bytes(dm)
+    host, weights = quantized_host_bank(api, dm, torch, [1000])
+    keep_weights = None
+    if not args.no_cpu_baseline:
+        keep_weights = tuple(w.view(torch.int16).cpu().numpy().view(np.uint16) for w in weights)
+    del weights
+    torch.cuda.empty_cache()
+    h2d_gbs = pinned_h2d_gbs(torch, host)
+    slots = torch.zeros(C * rec, dtype=torch.uint8, device="cuda")
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    h = torch.randn((T, D_MODEL), dtype=torch.bfloat16, device="cuda", generator=gen)
+    y = torch.empty_like(h)
+    ws = torch.empty(api.workspace_bytes(dm, T), dtype=torch.uint8, device="cuda")
+    log(f"multiwave: host bank ready, pinned H2D {h2d_gbs:.1f} GB/s")
+
+    def one_call(z, state, sequential):
+        cache = api.Cache(dm, C, slot_bank=slots, host_bank=host)
+        if state == "warm":
+            _, fills = cache.build_slot_map(list(range(C)))
+            cache.fill_slots(fills)
+        torch.cuda.synchronize()
+        st = api.Stats()
+        api.profile_begin(4096)
+        t0 = time.perf_counter()
+        api.moe_forward(cache, h, None, y, ws, logits_override=z, stats=st, sequential=sequential)
+        torch.cuda.synchronize()
+        e2e = time.perf_counter() - t0
+        prof = api.profile_end(4096)
+        cache.close()
+        return e2e, sum(t for _, t in prof) * 1e-3, st, y.clone()
+
+    cases, outs = [], {}
+    for D in (40, 48, 56, 64):
+        z = torch.from_numpy(spread_logits(T, N_EXPERTS, TOP_K, D, seed=2)).to("cuda")
+        for state in ("cold", "warm"):
+            row = dict(distinct_experts=D, state=state)
+            for name, seq in (("fused", False), ("sequential", True)):
+                one_call(z, state, seq)                      # warm-up of this case
+                e2e, kern, k_sum = [], [], None
+                for _ in range(reps):
+                    a, b, st, yy = one_call(z, state, seq)
+                    e2e.append(a)
+                    kern.append(b)
+                    k_sum = st
+                outs[(D, state, name)] = yy
+                row[name] = dict(e2e_ms=1e3 * float(np.median(e2e)), kernel_ms=1e3 * float(np.median(kern)),
+                                 waves=int(k_sum.waves), hits=int(k_sum.hits), misses=int(k_sum.misses),
+                                 h2d_bytes=int(k_sum.h2d_bytes), kernel_launches=int(k_sum.kernel_launches))
+            row["speedup_e2e"] = row["sequential"]["e2e_ms"] / row["fused"]["e2e_ms"]
+            row["speedup_kernels"] = row["sequential"]["kernel_ms"] / row["fused"]["kernel_ms"]
+            row["fused_equals_sequential"] = bool(torch.equal(outs[(D, state, "fused")],
+                                                              outs[(D, state, "sequential")]))
+            cases.append(row)
+            log(f"D={D} {state}: fused {row['fused']['e2e_ms']:.2f} ms e2e / "
+                f"{row['fused']['kernel_ms']:.3f} ms kernels, sequential "
+                f"{row['sequential']['e2e_ms']:.2f} / {row['sequential']['kernel_ms']:.3f} ms")
+    head = next(c for c in cases if c["distinct_experts"] == 56 and c["state"] == "warm")
+    sec = head["fused"]["e2e_ms"] * 1e-3
+    kern_s = head["fused"]["kernel_ms"] * 1e-3
+    alg = 56 * rec + 2 * T * D_MODEL * 2
+    ach = alg / kern_s / 1e9
+    out = dict(metric=METRIC, value=T / sec, unit="tokens/s", n_gpus=1, steps=reps, warmup=1,
+               ms_per_step=1e3 * sec, higher_is_better=True, scaling="weak", vs_baseline=None,
+               dtype="bf16", data="synthetic",
+               config=dict(workload="olmoe_16tok_16slots_waves", tokens=T, d_model=D_MODEL, d_ff=D_FF,
+                           n_experts=N_EXPERTS, top_k=TOP_K, slots=C, group=128,
+                           weights="int4 group-128, fp16 scales", headline="56 experts, warm, fused"),
+               roofline=dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
+                             frac=ach / HBM_PEAK_GBS, traffic=None,
+                             kernel="all kernels of the fused call (fills excluded)",
+                             alg_bytes_per_launch=alg),
+               host_link=dict(pinned_h2d_gbs=h2d_gbs), cases=cases)
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        out["cpu_baseline"] = oracle_multiwave(keep_weights, T, head)
+    print(json.dumps(out), flush=True)
+
+
+def oracle_multiwave(weights, T, head, budget_s=12.0):
+    """The CPU oracle on the 56-expert 16-token batch (single and multi-wave)."""
+    import oracle as O
+    from paper_2608_15383_amd.inputs import bf16_bits_to_f32, spread_logits
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = 1
+    wg, wu, wd = weights
+    rng = np.random.default_rng(7)
+    h = rng.standard_normal((T, D_MODEL)).astype(np.float32)
+    z = spread_logits(T, N_EXPERTS, TOP_K, 56, seed=2)
+    r = O.route(h, None, TOP_K, logits_override=z)
+    needed = sorted(set(r.ids.reshape(-1).tolist()))
+    experts = {e: O.quantize_expert(bf16_bits_to_f32(wg[e]), bf16_bits_to_f32(wu[e]),
+                                    bf16_bits_to_f32(wd[e])) for e in needed}
+    calls, t0 = 0, time.perf_counter()
+    while True:
+        for ex in experts.values():
+            ex._hat.clear()
+        O.moe_forward(h, experts, O.route(h, None, TOP_K, logits_override=z))
+        calls += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or calls >= 1000:
+            break
+    return dict(value=T * calls / el, unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=f"{calls} calls of the 16-token, 56-expert batch, {el:.1f} s, numpy fp64 "
+                       f"with dequantization each call")
+
+
+def bench_stack(args):
+    """16 layers, 16 slots each, Zipf(1.1) routing, 64 tokens per step."""
+    import torch
+    from paper_2608_15383_amd import api
+    from paper_2608_15383_amd.inputs import zipf_gumbel_logits
+
+    torch.cuda.init()
+    dm = api.dims(D_MODEL, D_FF, N_EXPERTS, TOP_K)
+    L, T, C = 16, 64, 16
+    steps = args.steps or 32
+    warmup = args.warmup if args.warmup is not None else 4
+    rec = api.expert_record_bytes(dm)
+    log("stack: quantizing 16 x 64 experts into the pinned host bank")
+    host, weights = quantized_host_bank(api, dm, torch, [2000 + l for l in range(L)])
+    del weights
+    torch.cuda.empty_cache()
+    h2d_gbs = pinned_h2d_gbs(torch, host)
+    banks = [torch.zeros(C * rec, dtype=torch.uint8, device="cuda") for _ in range(L)]
+    caches = [api.Cache(dm, C, slot_bank=banks[l],
+                        host_bank=host[l * N_EXPERTS * rec:(l + 1) * N_EXPERTS * rec]) for l in range(L)]
+    rng = np.random.default_rng(4)
+    perms = [rng.permutation(N_EXPERTS) for _ in range(L)]
+    n_steps = warmup + steps
+    z_all = np.stack([np.stack([zipf_gumbel_logits(T, N_EXPERTS, 1.1, perms[l], rng) for l in range(L)])
+                      for _ in range(n_steps)])
+    z_dev = torch.from_numpy(z_all).to("cuda")            # [steps][L][T][E]
+    gen = torch.Generator(device="cuda").manual_seed(9)
+    hs = [torch.randn((T, D_MODEL), dtype=torch.bfloat16, device="cuda", generator=gen) for _ in range(8)]
+    y = torch.empty_like(hs[0])
+    ws = torch.empty(api.workspace_bytes(dm, T), dtype=torch.uint8, device="cuda")
+    log(f"stack ready: pinned H2D {h2d_gbs:.1f} GB/s")
+
+    def step(s, st):
+        for l in range(L):
+            api.moe_forward(caches[l], hs[(s * L + l) % len(hs)], None, y, ws,
+                            logits_override=z_dev[s, l], stats=st)
+
+    first = api.Stats()
+    step(0, first)
+    torch.cuda.synchronize()
+    for s in range(1, warmup):
+        step(s, api.Stats())
+    torch.cuda.synchronize()
+    st = api.Stats()
+    t0 = time.perf_counter()
+    for s in range(warmup, n_steps):
+        step(s, st)
+    torch.cuda.synchronize()
+    sec = time.perf_counter() - t0
+    api.profile_begin(1 << 16)
+    step(warmup, api.Stats())
+    prof = api.profile_end(1 << 16)
+    kern = {}
+    for name, t in prof:
+        kern.setdefault(name, []).append(t)
+    kern = {n: dict(avg_us=1e3 * float(np.mean(v)), launches=len(v)) for n, v in kern.items()}
+    kernel_ms = sum(v["avg_us"] * v["launches"] for v in kern.values()) * 1e-3
+
+    def hit_rate(x):
+        tot = x.hits + x.misses
+        return x.hits / tot if tot else 0.0
+
+    calls = steps * L
+    h2d_per_call = st.h2d_bytes / calls
+    dom = max(kern, key=lambda n: kern[n]["avg_us"] * kern[n]["launches"])
+    out = dict(metric=METRIC, value=T * steps / sec, unit="tokens/s", n_gpus=1, steps=steps,
+               warmup=warmup, ms_per_step=1e3 * sec / steps, higher_is_better=True, scaling="weak",
+               vs_baseline=None, dtype="bf16", data="synthetic",
+               config=dict(workload="olmoe_stack16_zipf1.1_16slots", layers=L, tokens=T,
+                           d_model=D_MODEL, d_ff=D_FF, n_experts=N_EXPERTS, top_k=TOP_K, slots=C,
+                           group=128, weights="int4 group-128, fp16 scales",
+                           activations="8 pre-drawn N(0,1) token blocks cycled over layers and steps"),
+               hit_rate_steady=hit_rate(st), hit_rate_cold_first_step=hit_rate(first),
+               h2d_bytes_per_layer_call=h2d_per_call, waves_per_layer_call=st.waves / calls,
+               misses_per_layer_call=st.misses / calls,
+               h2d_gbs_achieved=st.h2d_bytes / sec / 1e9,
+               host_link=dict(bound="host link", achieved=st.h2d_bytes / sec / 1e9,
+                              pinned_copy_gbs=h2d_gbs, frac=st.h2d_bytes / sec / 1e9 / h2d_gbs),
+               kernels_ms_per_step=kernel_ms, kernels=kern, dominant_kernel=dom)
+    print(json.dumps(out), flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              f"(the layer runs on a single device).", file=sys.stderr)
+        sys.exit(2)
+    if args.workload == "multiwave":
+        bench_multiwave(args)
+    elif args.workload == "stack":
+        bench_stack(args)
+    else:
+        bench_layer(args)
 
 
 if __name__ == "__main__":
