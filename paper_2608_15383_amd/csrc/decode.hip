@@ -42,38 +42,36 @@ __device__ __forceinline__ bool reached(uint32_t v, uint32_t target) {
   return (int32_t)(v - target) >= 0;  // modulo-2^32 comparison
 }
 
-// Wait (bounded) until *p reaches target; whole workgroup.
-__device__ __forceinline__ void block_wait(const uint32_t* p, uint32_t target, uint32_t* timeouts) {
-  if (threadIdx.x == 0) {
-    uint32_t it = 0;
-    while (!reached(ld_u32<true>(p), target)) {
-      if (++it > kSpinLimit) {
-        atomicAdd(timeouts, 1u);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(kPollSleep);
+// Wait (bounded) until the gate/up counters of pair pi reach their targets;
+// one wavefront (lanes 0 .. cpp-1 each poll one counter).
+__device__ __forceinline__ void wave_wait_pair(DecodeSync* sy, const DecodeArgs& a, int pi) {
+  const int lane = lane_id();
+  const int cpp = a.counters_per_pair;
+  const int c = pi * cpp + lane;
+  const uint32_t tgt = lane < cpp ? a.gate_target[c] : 0u;
+  uint32_t it = 0;
+  while (true) {
+    const bool ok = lane >= cpp || reached(ld_u32<true>(&sy->gate_done[c][0]), tgt);
+    if (__all(ok)) break;
+    if (++it > kSpinLimit) {
+      if (lane == 0) atomicAdd(&sy->timeouts, 1u);
+      break;
     }
+    __builtin_amdgcn_s_sleep(kPollSleep);
   }
-  __syncthreads();
 }
 
-// Wait (bounded) until gate_done[i] reaches target[i] for every spread counter.
-__device__ __forceinline__ void block_wait_gates(DecodeSync* sy, const uint32_t* target) {
-  if (threadIdx.x < 64) {
-    const int lane = lane_id();
-    const uint32_t tgt = lane < kSyncLanes ? target[lane] : 0u;
-    uint32_t it = 0;
-    while (true) {
-      const bool ok = lane >= kSyncLanes || reached(ld_u32<true>(&sy->gate_done[lane][0]), tgt);
-      if (__all(ok)) break;
-      if (++it > kSpinLimit) {
-        if (lane == 0) atomicAdd(&sy->timeouts, 1u);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(kPollSleep);
-    }
-  }
-  __syncthreads();
+// Copy `bytes` (a multiple of 256) from coherent global memory to LDS with
+// buffer loads that target LDS (one wavefront, 4 bytes per lane per load,
+// device-coherent: sc1).  Completion is this wavefront's vmcnt.
+__device__ __forceinline__ void wave_copy_to_lds(const void* src, uint32_t bytes, void* lds) {
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(src), (short)0, (int)bytes, 0x00020000);
+  const uint32_t voff = 4u * (uint32_t)lane_id();
+  for (uint32_t off = 0; off < bytes; off += 256)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rsrc, (__attribute__((address_space(3))) void*)(static_cast<uint8_t*>(lds) + off), 4,
+        (int)voff, (int)off, 0, /*sc1*/ 16);
 }
 
 // Make this workgroup's coherent stores visible, then bump *p.
@@ -101,8 +99,9 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
 
   if (blk < a.n_router) {
     // ---------------------------------------------------------------- router
-    // Each logit goes to the workspace and to kSyncLanes replicas, so the
-    // hundreds of readers below spread over as many memory locations.
+    // Each logit goes to the workspace and, tagged with the epoch, to
+    // kSyncLanes replicas, so the hundreds of readers below spread over as
+    // many memory locations.
     if (!a.logits_override) {
       const int e0 = 4 * blk + wi;
       if (e0 < a.n_experts) {
@@ -113,24 +112,48 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
           if (t >= a.tokens) break;
           const uint32_t v = __float_as_uint((float)s[t][0]);
           const int at = t * a.n_experts + e0;
-          if (lane < kSyncLanes) st_u32<true>(&sy->logits[lane][at], v);
+          if (lane < kSyncLanes)
+            __hip_atomic_store(&sy->logits[lane][at], ((uint64_t)a.epoch << 32) | v,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           if (lane == kSyncLanes) st_u32<false>(a.logits + at, v);
         }
       }
     }
-    wait_memory();
-    __syncthreads();
-    if (tid < kSyncLanes) atomicAdd(&sy->route_done[tid][0], 1u);
     return;
   }
 
-  // Every other workgroup: wait for the logits and select the experts.
+  // Every other workgroup: wavefront wi < T waits for token wi's logits (this
+  // launch's epoch in every tag) and selects its experts.
   const int replica = blk % kSyncLanes;
-  block_wait(&sy->route_done[replica][0], a.route_target, &sy->timeouts);
-  const float* z = a.logits_override ? a.logits_override : sy->logits[replica];
-  TopkState st;  // wavefront wi selects the experts of token wi
+  TopkState st;
   if (wi < a.tokens) {
-    wave_topk_select<true>(z + (int64_t)wi * a.n_experts, a.n_experts, a.top_k, st);
+    if (a.logits_override) {
+      wave_topk_select<false>(a.logits_override + (int64_t)wi * a.n_experts, a.n_experts, a.top_k, st);
+    } else {
+      const uint64_t* zt = sy->logits[replica] + wi * a.n_experts;
+      uint32_t it = 0;
+      while (true) {
+        bool ok = true;
+#pragma unroll
+        for (int c = 0; c < kPerLane; ++c) {
+          const int e = lane + 64 * c;
+          if (e < a.n_experts) {
+            const uint64_t x = __hip_atomic_load(zt + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            ok = ok && (uint32_t)(x >> 32) == a.epoch;
+            st.v[c] = __uint_as_float((uint32_t)x);
+          } else {
+            st.v[c] = 0.f;
+          }
+        }
+        if (__all(ok)) break;
+        if (++it > kSpinLimit) {
+          if (lane == 0) atomicAdd(&sy->timeouts, 1u);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(kPollSleep);
+      }
+      wave_topk_select_loaded(a.n_experts, a.top_k, st);
+    }
     wave_topk_store_ids<false>(st, a.top_k, s_ids + wi * a.top_k);
   }
   __syncthreads();
@@ -150,7 +173,8 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     for (int b = b0; b < b1; ++b)
       gateup_rows<true>(gush, a.d, a.f, a.h, [top_k](int s) { return s / top_k; }, pi, pi + 1,
                         a.slot_bank + (int64_t)e * a.record_bytes, b, a.act);
-    block_signal(&sy->gate_done[item % kSyncLanes][0]);
+    const int cpp = a.counters_per_pair;
+    block_signal(&sy->gate_done[pi * cpp + (item % chunks) % cpp][0]);
     return;
   }
 
@@ -168,26 +192,26 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   // the tiles stream in.
   if (wi < a.tokens)
     wave_topk_weights<false>(st, a.n_experts, a.top_k, a.renormalize, s_w + wi * a.top_k);
-  block_wait_gates(sy, a.gate_target);
 
-  // Stage every pair's activation row in LDS with one coherent pass, then the
-  // per-(pair, group, quarter) activation sums used by every row block.
-  {
-    const uint32_t n16 = (uint32_t)P * (uint32_t)a.f / 8u;
-    const Buf128<true> xb(a.act, n16 * 16u);
-    for (uint32_t i = tid; i < n16; i += 256) s_act[i] = xb.load(16u * i);
-  }
-  __syncthreads();
+  // Pair by pair, as soon as its gate/up workgroups are done: copy its
+  // activation row to LDS, its per-(group, quarter) activation sums, then its
+  // expert output for this row block.  Wavefront wi owns pairs wi, wi+4, ...
   const uint16_t* act_lds = reinterpret_cast<const uint16_t*>(s_act);
-  for (int i = tid; i < P * G * 4; i += 256) {
-    const int pi = i / (G * 4), g = (i >> 2) % G, q = i & 3;
-    uint4 x[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      x[k] = *reinterpret_cast<const uint4*>(act_lds + pi * a.f + g * kGroup + 8 * q + 32 * k);
-    s_xs[i] = lane_group_xsum(x);
+  for (int pi = wi; pi < P; pi += kGemvWaves) {
+    wave_wait_pair(sy, a, pi);
+    wave_copy_to_lds(a.act + (int64_t)pi * a.f, (uint32_t)a.f * 2u, s_act + pi * (a.f / 8));
   }
-  __syncthreads();
+  wait_memory();
+  for (int pi = wi; pi < P; pi += kGemvWaves) {
+    for (int i = lane; i < G * 4; i += 64) {
+      const int g = i >> 2, q = i & 3;
+      uint4 x[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        x[k] = *reinterpret_cast<const uint4*>(act_lds + pi * a.f + g * kGroup + 8 * q + 32 * k);
+      s_xs[pi * G * 4 + i] = lane_group_xsum(x);
+    }
+  }
   // Expert output of pair pi for this row block; `first` is its first batch
   // of tiles (prefetched when has_first).
   auto pair_output = [&](int pi, DownBatch first, bool has_first) {
@@ -265,10 +289,15 @@ bool decode_fused_plan(DecodeArgs& a) {
   a.n_down = a.d / kTileRows;
   const int cap = fused_capacity();
   for (int ppi = 1; ppi <= pairs_of_f; ppi *= 2) {
-    const int n_gate = P * ((pairs_of_f + ppi - 1) / ppi);
+    const int chunks = (pairs_of_f + ppi - 1) / ppi;
+    const int n_gate = P * chunks;
     if (a.n_router + n_gate + a.n_down <= cap) {
       a.pairs_per_item = ppi;
+      a.items_per_pair = chunks;
       a.n_gate = n_gate;
+      int cpp = kGateCounters / P;  // >= 1: P <= kFusedMaxPairs = kGateCounters
+      if (cpp > chunks) cpp = chunks;
+      a.counters_per_pair = cpp;
       return true;
     }
   }
@@ -276,15 +305,20 @@ bool decode_fused_plan(DecodeArgs& a) {
 }
 
 hipError_t launch_decode_fused(DecodeArgs& a, DecodeProgress& prog, hipStream_t stream) {
-  a.route_target = prog.route_total + (uint32_t)a.n_router;
-  for (int i = 0; i < kSyncLanes; ++i)
-    a.gate_target[i] =
-        prog.gate_total[i] + (uint32_t)(a.n_gate / kSyncLanes + (i < a.n_gate % kSyncLanes));
+  a.epoch = prog.epoch + 1u;
+  if (a.epoch == 0u) a.epoch = 1u;  // 0 is the zeroed memory's tag
+  // Pair pi's items i = 0 .. chunks-1 signal counter pi*cpp + i % cpp.
+  const int P = a.tokens * a.top_k, cpp = a.counters_per_pair, chunks = a.items_per_pair;
+  for (int c = 0; c < kGateCounters; ++c) {
+    const int j = c % cpp;
+    const uint32_t n = c < P * cpp ? (uint32_t)((chunks - j + cpp - 1) / cpp) : 0u;
+    a.gate_target[c] = prog.gate_total[c] + n;
+  }
   launch(decode_fused_kernel, dim3(a.n_router + a.n_gate + a.n_down), dim3(256), stream, a);
   const hipError_t e = hipGetLastError();
   if (e == hipSuccess) {
-    prog.route_total = a.route_target;
-    for (int i = 0; i < kSyncLanes; ++i) prog.gate_total[i] = a.gate_target[i];
+    prog.epoch = a.epoch;
+    for (int c = 0; c < kGateCounters; ++c) prog.gate_total[c] = a.gate_target[c];
   }
   return e;
 }

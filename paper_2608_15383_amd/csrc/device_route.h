@@ -112,10 +112,11 @@ __device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v) {
 
 // Top-k of one token's logits z[E] by one wavefront, and its mixture weights
 // (softmax over the selected logits when renormalize, else over all E), fp64.
-// Round j picks the largest remaining logit (order key: a monotone integer
-// image of the fp32 value, -0 folded onto +0) and, among equal logits, the
-// lowest expert id.  kCo: device-coherent loads of z; kCoStore:
-// device-coherent result stores.
+// Order: larger logit first (order key: a monotone integer image of the fp32
+// value, -0 folded onto +0) and, among equal logits, the lower expert id.  Up
+// to 64 experts use a ballot radix select; more experts take k rounds of a
+// wavefront max.  kCo: device-coherent loads of z; kCoStore: device-coherent
+// result stores.
 // wave_topk_select leaves the selection in registers (TopkState);
 // wave_topk_store_ids and wave_topk_weights write it out.
 struct TopkState {
@@ -125,9 +126,9 @@ struct TopkState {
   float zmax;
 };
 
-template <bool kCo>
-__device__ __forceinline__ void wave_topk_select(const float* __restrict__ z, int n_experts,
-                                                 int top_k, TopkState& st) {
+// Selection from the logits already in st.v (lane l holds expert l + 64c in
+// register c).
+__device__ __forceinline__ void wave_topk_select_loaded(int n_experts, int top_k, TopkState& st) {
   const int lane = lane_id();
   const int nc = (n_experts + 63) / 64;  // logits per lane in use
   float* v = st.v;
@@ -137,29 +138,66 @@ __device__ __forceinline__ void wave_topk_select(const float* __restrict__ z, in
 #pragma unroll
   for (int c = 0; c < kPerLane; ++c) {
     const int e = lane + 64 * c;
-    v[c] = e < n_experts ? ld_f32<kCo>(z + e) : 0.f;
     const uint32_t u = __float_as_uint(v[c] + 0.0f);  // -0 -> +0
     key[c] = e < n_experts ? ((u & 0x80000000u) ? ~u : (u | 0x80000000u)) : 0u;
   }
   float zmax = 0.f;
+  if (nc == 1) {
+    // At most 64 experts, one per lane.  Radix select of the k-th largest key
+    // from the top bit down with ballots (lanes still tied on the bits seen
+    // so far in `cand`, lanes certainly selected in `sel`), the lowest lanes
+    // (expert ids) first among equal keys; then each selected lane's rank is
+    // the number of selected lanes ahead of it.
+    uint64_t cand = __ballot(lane < n_experts);
+    uint64_t sel = 0;
+    int need = top_k;
+    // The 32 bit-plane ballots do not depend on each other; unrolled, they
+    // issue back to back and only the scalar mask updates form a chain.
+    uint64_t plane[32];
+#pragma unroll
+    for (int b = 0; b < 32; ++b) plane[b] = __ballot((key[0] >> b) & 1u);
+#pragma unroll
+    for (int b = 31; b >= 0; --b) {
+      const uint64_t ones = plane[b] & cand;
+      const int n1 = __popcll(ones);
+      if (n1 >= need) {
+        cand = ones;
+      } else {
+        sel |= ones;
+        need -= n1;
+        cand &= ~ones;
+      }
+    }
+    for (; need > 0; --need) {
+      sel |= cand & (~cand + 1ull);  // lowest remaining tied lane
+      cand &= cand - 1ull;
+    }
+    for (uint64_t m = sel; m != 0; m &= m - 1ull) {
+      const int s = (int)__builtin_ctzll(m);
+      const uint32_t ks = (uint32_t)__builtin_amdgcn_readlane((int)key[0], s);
+      const float zs = __uint_as_float((uint32_t)__builtin_amdgcn_readlane((int)__float_as_uint(v[0]), s));
+      const uint64_t ahead = (__ballot(key[0] > ks) & sel) | (__ballot(key[0] == ks) & sel & ((1ull << s) - 1ull));
+      const int r = __popcll(ahead);
+      if (lane == r) {
+        sel_id[0] = s;
+        sel_z[0] = zs;
+      }
+      if (r == 0) zmax = zs;
+    }
+    st.zmax = zmax;
+    return;
+  }
   for (int j = 0; j < top_k; ++j) {
     uint32_t best = 0;
 #pragma unroll
     for (int c = 0; c < kPerLane; ++c)
       if (c < nc) best = key[c] > best ? key[c] : best;
     const uint32_t m = wave_reduce_u32<true>(best);
-    int e;
-    if (nc == 1) {
-      // One logit per lane: the lowest lane holding the maximum is the
-      // lowest expert id among equal logits.
-      e = (int)__builtin_ctzll(__ballot(key[0] == m));
-    } else {
-      uint32_t idx = 0xffffffffu;
+    uint32_t idx = 0xffffffffu;
 #pragma unroll
-      for (int c = kPerLane - 1; c >= 0; --c)
-        if (c < nc && key[c] == m) idx = (uint32_t)(lane + 64 * c);
-      e = (int)wave_reduce_u32<false>(idx);
-    }
+    for (int c = kPerLane - 1; c >= 0; --c)
+      if (c < nc && key[c] == m) idx = (uint32_t)(lane + 64 * c);
+    const int e = (int)wave_reduce_u32<false>(idx);
     const int ce = e >> 6;
     float vw = v[0];
 #pragma unroll
@@ -179,6 +217,18 @@ __device__ __forceinline__ void wave_topk_select(const float* __restrict__ z, in
     }
   }
   st.zmax = zmax;
+}
+
+template <bool kCo>
+__device__ __forceinline__ void wave_topk_select(const float* __restrict__ z, int n_experts,
+                                                 int top_k, TopkState& st) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int c = 0; c < kPerLane; ++c) {
+    const int e = lane + 64 * c;
+    st.v[c] = e < n_experts ? ld_f32<kCo>(z + e) : 0.f;
+  }
+  wave_topk_select_loaded(n_experts, top_k, st);
 }
 
 template <bool kCoStore>
