@@ -90,13 +90,14 @@ typedef struct emoe_ws_layout {
   size_t active;        /* i32   [E]      active experts, ascending */
   size_t n_active;      /* i32   [1]      number of active experts */
   size_t tile_offsets;  /* i32   [E+1]    MFMA row-tile prefix sum */
-  size_t pair_pos;      /* i32   [T*k]    grouped position of each pair id (fused decode) */
+  size_t pair_pos;      /* i32   [T*k]    grouped position of each pair id */
   size_t act;           /* bf16  [T*k][d_ff]    phi(g)*u per pair, grouped order */
   size_t pair_out;      /* expert output per pair id, [T*k][d_model]: f32 on the GEMV
                            path, bf16 (in the first half of the field) on the MFMA path */
-  size_t x_bias;        /* f32   [T][d_model/128]   -136 * group sums of h (MFMA path) */
-  size_t act_bias;      /* f32   [T*k][d_ff/128]    -136 * group sums of act, grouped order
-                                                      (MFMA path) */
+  size_t x_bias;        /* f32   [d_model/128][T*k] -136 * group sums of each pair's token row
+                                                      of h, by grouped position (MFMA path) */
+  size_t act_bias;      /* f32   [d_ff/128][T*k]    -136 * group sums of act, by grouped
+                                                      position (MFMA path) */
   size_t chunk_counts;  /* i32   [ceil(T*k/64)][E]  pairs per expert in each 64-pair chunk
                                                       (grouping of large calls) */
   size_t total;         /* bytes needed */

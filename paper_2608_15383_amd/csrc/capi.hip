@@ -145,7 +145,7 @@ emoe_ws_layout make_layout(const emoe_dims& d, int32_t T) {
   L.pair_pos = take(P * 4);
   L.act = take(P * (size_t)d.d_ff * 2);
   L.pair_out = take(P * (size_t)d.d_model * 4);
-  L.x_bias = take((size_t)T * (d.d_model / EMOE_GROUP) * 4);
+  L.x_bias = take(P * (size_t)(d.d_model / EMOE_GROUP) * 4);
   L.act_bias = take(P * (size_t)(d.d_ff / EMOE_GROUP) * 4);
   L.chunk_counts = take((P + 63) / 64 * E * 4);
   L.total = off;
@@ -247,7 +247,7 @@ int32_t emoe_unpack_expert(const emoe_dims* dims, const void* record, int8_t* q_
   const int d = dims->d_model, f = dims->d_ff;
   const RecordLayout L = record_layout(d, f);
   const uint8_t* rec = static_cast<const uint8_t*>(record);
-  // Decode one matrix (N x K codes at `codes`, fp16 [N][K/128] at `sc`) into
+  // Decode one matrix (N x K codes at `codes`, fp16 scales at `sc`) into
   // row-major outputs; `row_of(n)` maps the stored row to the output row or -1.
   auto decode = [&](int N, int K, int64_t codes_off, int64_t sc_off, auto row_of, int8_t* q,
                     uint16_t* s) {
@@ -274,7 +274,7 @@ int32_t emoe_unpack_expert(const emoe_dims* dims, const void* record, int8_t* q_
       for (int n = 0; n < N; ++n) {
         const int out_row = row_of(n);
         if (out_row < 0) continue;
-        std::memcpy(s + (int64_t)out_row * G, sp + (int64_t)n * G, G * 2);
+        for (int g = 0; g < G; ++g) s[(int64_t)out_row * G + g] = sp[scale_index(n, g, G)];
       }
     }
   };
@@ -323,7 +323,7 @@ int32_t emoe_pack_expert(const emoe_dims* dims, const int8_t* q_gate, const uint
       const int8_t* qrow;
       const uint16_t* srow;
       src_of(n, qrow, srow);
-      std::memcpy(sp + (int64_t)n * G, srow, G * 2);
+      for (int g = 0; g < G; ++g) sp[scale_index(n, g, G)] = srow[g];
     }
     return EMOE_OK;
   };
@@ -365,7 +365,7 @@ int32_t emoe_route(const emoe_dims* dims, int32_t T, const uint16_t* h, const ui
     EMOE_LAUNCH(EMOE_K_TOPK, stream, launch_topk(T, E, k, renormalize, z, topk_ids, topk_w, stream));
   EMOE_LAUNCH(EMOE_K_GROUP, stream,
               launch_group(T * k, E, topk_ids, counts, offsets, sorted_pairs, active, n_active,
-                           nullptr, stream));
+                           nullptr, nullptr, stream));
   return EMOE_OK;
 }
 
@@ -605,7 +605,7 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
   const int P = T * k;
   // The MFMA kernels address activations with 32-bit buffer offsets.
   const bool mfma_fits = (int64_t)P * f * 2 <= INT32_MAX && (int64_t)T * d * 2 <= INT32_MAX &&
-                         c->record_bytes <= INT32_MAX;
+                         (int64_t)P * (d / EMOE_GROUP) * 4 <= INT32_MAX && c->record_bytes <= INT32_MAX;
   if (path == EMOE_PATH_AUTO)
     path = (P >= EMOE_MFMA_MIN_PAIRS_PER_EXPERT * E && mfma_fits) ? EMOE_PATH_MFMA : EMOE_PATH_GEMV;
   if (path == EMOE_PATH_MFMA && !mfma_fits)
@@ -676,17 +676,18 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
     EMOE_LAUNCH(EMOE_K_GROUP_COUNT, stream, launch_group_count(P, E, ids, chunk_counts, stream));
     EMOE_LAUNCH(EMOE_K_GROUP, stream,
                 launch_group_place(P, E, ids, chunk_counts, counts, offsets, sorted, active,
-                                   n_active, tiles, stream));
+                                   n_active, tiles, pair_pos, stream));
     ds.kernel_launches += 3;
   } else {
     EMOE_LAUNCH(EMOE_K_GROUP, stream,
-                launch_group(P, E, ids, counts, offsets, sorted, active, n_active, tiles, stream));
+                launch_group(P, E, ids, counts, offsets, sorted, active, n_active, tiles, pair_pos,
+                             stream));
     ds.kernel_launches += 2;
   }
   const GroupView gv{sorted, offsets, active, n_active, tiles};
   if (path == EMOE_PATH_MFMA) {
     // Accumulator start of the gate/up MFMA chains, once per call.
-    EMOE_LAUNCH(EMOE_K_ROW_BIAS, stream, launch_row_bias(T, d, h, x_bias, stream));
+    EMOE_LAUNCH(EMOE_K_ROW_BIAS, stream, launch_row_bias(T, d, k, h, pair_pos, x_bias, stream));
     ds.kernel_launches += 1;
   }
 

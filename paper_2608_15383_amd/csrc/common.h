@@ -40,11 +40,21 @@ constexpr int kMfmaRows = 64;       // token rows per MFMA row-tile
 // therefore fully coalesced, each dword expands to four bf16 pairs (k, k+1)
 // that line up with bf16 activations in memory, and the four dwords are the
 // B operands of four v_mfma_f32_16x16x32_bf16 steps.
-// Scales: fp16 [N][K/128] row-major after the codes.
+// Scales: fp16, after the codes, N*(K/128) of them in 128-byte lines: the 64
+// scales of rows 64c .. 64c+63 and group g fill line c*(K/128) + g, ordered by
+// (n%16, (n/16)%4), so the four row blocks a wavefront owns give each lane
+// its four scales as one 8-byte load (scale_index).  N is a multiple of 64
+// (d_model and d_ff are multiples of 128).
 // ---------------------------------------------------------------------------
 struct RecordLayout {
   int64_t w13_codes, w13_scales, w2_codes, w2_scales, bytes;
 };
+
+// Position (in fp16 units) of the scale of stored row n and group g of a
+// matrix with G groups per row.
+__host__ __device__ inline int64_t scale_index(int n, int g, int G) {
+  return ((int64_t)(n >> 6) * G + g) * 64 + (n & 15) * 4 + ((n >> 4) & 3);
+}
 
 __host__ __device__ inline RecordLayout record_layout(int d, int f) {
   RecordLayout r;
@@ -85,10 +95,7 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
 }
 
 __device__ __forceinline__ uint32_t f32_to_bf16_rne(float x) {
-  uint32_t u = __float_as_uint(x);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;  // NaN
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+  return __builtin_bit_cast(uint16_t, (__bf16)x);  // v_cvt_pk_bf16_f32, nearest even
 }
 
 __device__ __forceinline__ float half_bits_to_f32(uint16_t b) {
@@ -200,9 +207,12 @@ hipError_t launch_router_logits(int tokens, int n_experts, int d, const uint16_t
 hipError_t launch_topk(int tokens, int n_experts, int top_k, int renormalize, const float* logits,
                        int32_t* topk_ids, float* topk_w, hipStream_t stream);
 
+// Grouping by expert (Sec. 3.4 step 1) in one workgroup; pair_pos receives
+// the inverse permutation (grouped position of each pair id).
 hipError_t launch_group(int pairs, int n_experts, const int32_t* topk_ids, int32_t* counts,
                         int32_t* offsets, int32_t* sorted_pairs, int32_t* active,
-                        int32_t* n_active, int32_t* tile_offsets, hipStream_t stream);
+                        int32_t* n_active, int32_t* tile_offsets, int32_t* pair_pos,
+                        hipStream_t stream);
 
 // The same grouping over many workgroups, for large calls (pairs > 0): per
 // 64-pair chunk expert counts into chunk_counts [ceil(pairs/64)][E], then the
@@ -212,7 +222,7 @@ hipError_t launch_group_count(int pairs, int n_experts, const int32_t* topk_ids,
 hipError_t launch_group_place(int pairs, int n_experts, const int32_t* topk_ids,
                               const int32_t* chunk_counts, int32_t* counts, int32_t* offsets,
                               int32_t* sorted_pairs, int32_t* active, int32_t* n_active,
-                              int32_t* tile_offsets, hipStream_t stream);
+                              int32_t* tile_offsets, int32_t* pair_pos, hipStream_t stream);
 constexpr int kGroupWideMinPairs = 1024;  // smaller calls group in one workgroup
 
 // Number of wave-local expert indices a grouped launch must cover.
@@ -231,10 +241,14 @@ hipError_t launch_down_gemv(int d, int f, int top_k, int pairs, int n_experts,
                             const uint8_t* slot_bank, int64_t record_bytes, float* pair_out,
                             hipStream_t stream);
 
-// Grouped MFMA projections.  h_bias / act_bias: -136 * per-row sums of each
-// 128-input group of h (launch_row_bias) and of act (written by the gate/up
-// launch for the down launch).
-hipError_t launch_row_bias(int rows, int K, const uint16_t* x, float* bias, hipStream_t stream);
+// Grouped MFMA projections.  h_bias / act_bias: -136 * the sum of each
+// 128-input group of the projection's input row, fp32 [K/128][pairs] indexed
+// by grouped position (one contiguous run per group and row tile).  h_bias
+// comes from launch_row_bias (each token's sums go to the positions of its
+// top_k pairs, through pair_pos); act_bias is written by the gate/up launch
+// for the down launch.
+hipError_t launch_row_bias(int tokens, int K, int top_k, const uint16_t* x, const int32_t* pair_pos,
+                           float* bias, hipStream_t stream);
 
 hipError_t launch_gateup_mfma(int tokens, int d, int f, int top_k, int n_experts, const uint16_t* h,
                               const float* h_bias, const GroupView& gv, const WaveArg& wave,

@@ -107,8 +107,7 @@ __device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f,
   const int n_local = lane & 15;
   const int quarter = lane >> 4;
   const uint16_t* scales = reinterpret_cast<const uint16_t*>(rec + L.w13_scales);
-  const uint16_t* gate_sc = scales + (int64_t)(32 * b + n_local) * G;
-  const uint16_t* up_sc = scales + (int64_t)(32 * b + 16 + n_local) * G;
+  const int gate_n = 32 * b + n_local, up_n = gate_n + 16;
 
   for (int m0 = begin; m0 < end; m0 += kTokChunk) {
     const int mc = min(kTokChunk, end - m0);
@@ -131,8 +130,8 @@ __device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f,
         if (g < G) {
           cg[j] = *reinterpret_cast<const uint4*>(gate_codes + (int64_t)g * kTileBytes);
           cu[j] = *reinterpret_cast<const uint4*>(up_codes + (int64_t)g * kTileBytes);
-          sg[j] = half_bits_to_f32(gate_sc[g]);
-          su[j] = half_bits_to_f32(up_sc[g]);
+          sg[j] = half_bits_to_f32(scales[scale_index(gate_n, g, G)]);
+          su[j] = half_bits_to_f32(scales[scale_index(up_n, g, G)]);
         }
       }
 #pragma unroll
@@ -194,13 +193,13 @@ __device__ __forceinline__ void down_load_batch(const uint8_t* __restrict__ rec,
   const int G = f / kGroup;
   const RecordLayout L = record_layout(d, f);
   const uint8_t* codes = rec + L.w2_codes + (int64_t)rb * G * kTileBytes + 16 * lane;
-  const uint16_t* sc = reinterpret_cast<const uint16_t*>(rec + L.w2_scales) +
-                       (int64_t)(16 * rb + (lane & 15)) * G;
+  const uint16_t* sc = reinterpret_cast<const uint16_t*>(rec + L.w2_scales);
+  const int n = 16 * rb + (lane & 15);
 #pragma unroll
   for (int j = 0; j < kDownBatch; ++j) {
     if (g0 + j < G) {
       bt.c[j] = *reinterpret_cast<const uint4*>(codes + (int64_t)(g0 + j) * kTileBytes);
-      bt.s[j] = half_bits_to_f32(sc[g0 + j]);
+      bt.s[j] = half_bits_to_f32(sc[scale_index(n, g0 + j, G)]);
     }
   }
 }

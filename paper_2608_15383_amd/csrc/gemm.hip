@@ -2,15 +2,20 @@
 // (prefill / large batches), where each expert's projection is a dense
 // contraction over its token rows.
 //
-// A workgroup (8 wavefronts, one per SIMD pair) owns one row tile (up to 64
-// token rows of one expert, grouped order) and one column tile of 512 weight
-// rows; each wavefront owns 4 weight row-blocks (64 outputs) for all 64 rows.
+// A workgroup of kWaves wavefronts owns one row tile (up to 64 token rows of
+// one expert, grouped order) and one column tile of 64*kWaves weight rows;
+// each wavefront owns 4 weight row-blocks (64 outputs) for all 64 rows.  The
+// default shape is 4 wavefronts and a ring of 2 LDS stages (66 KB), so two
+// workgroups share a CU and their wavefronts, not barrier-aligned with each
+// other, fill each other's load and barrier gaps on the matrix cores.
 //  - Per 128-input group, the token rows (16 KB) and each wavefront's four
 //    packed weight tiles (4 KB) are copied from memory straight into LDS by
-//    buffer loads with the LDS destination (no register staging), in a ring of
-//    three stages, so every load is issued two groups ahead of its use.  The
-//    16-byte chunks of a token row are XOR-swizzled by the row index, which
-//    makes the MFMA A-fragment reads free of bank conflicts.
+//    buffer loads with the LDS destination (no register staging), one group
+//    ahead of its use.  The 16-byte chunks of a token row are XOR-swizzled by
+//    the row index, which makes the MFMA A-fragment reads free of bank
+//    conflicts.  The per-row bias of the group is one contiguous 256-byte run
+//    and the wavefront's 64 scales one 8-byte load per lane, so a group costs
+//    each wavefront 10 vector memory instructions.
 //  - Each dword of codes expands in registers to one B operand of
 //    v_mfma_f32_16x16x32_bf16 (record layout in common.h): the codes enter as
 //    bf16 (128 + u), and the chain of four MFMAs of a group starts from the
@@ -19,12 +24,18 @@
 //    the FP16 group scale in fp32; the dequantized weight s * q is never
 //    rounded (Sec. 3.2).
 //  - The stages are handed over with one barrier per group; waits count only
-//    this wavefront's outstanding loads, so the two younger stages stay in
-//    flight across it.
-// Consecutive workgroups cover the column tiles of one row tile.
+//    this wavefront's outstanding loads.
+// Work items (row tile, column tile) are dealt to the XCDs in contiguous
+// eighths, so the column tiles of a row tile and the row tiles of an expert
+// share one L2.
 #include <type_traits>
 
 #include "common.h"
+
+#ifndef EMOE_MFMA_WAVES
+#define EMOE_MFMA_WAVES 4
+#define EMOE_MFMA_STAGES 2
+#endif
 
 namespace emoe {
 namespace {
@@ -32,27 +43,43 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 8;
-constexpr int kThreads = 64 * kWaves;
 constexpr int kNPW = 4;                                   // 16-row weight blocks per wavefront
 constexpr int kRows = kMfmaRows;                          // 64 token rows per tile
-constexpr int kCols = kWaves * kNPW * kTileRows;          // 512 weight rows per workgroup
-constexpr int kStages = 3;
 constexpr int kChunks = kGroup / 8;                       // 16-byte chunks per row and group
-constexpr int kBatchLoads = 2 + kNPW + kNPW + 1;          // loads one thread issues per group
 constexpr float kCodeBias = 136.f;                        // 128 (magic number) + 8 (offset binary)
+constexpr int kXcds = 8;                                  // accelerator complex dies per device
 
-// One stage of the LDS ring.  The three stages are separate LDS variables, so
-// the compiler can tell the loads landing in one stage from the reads of
-// another and waits only for the stage being read.
+// Shape of a grouped-projection launch: kWaves wavefronts per workgroup, each
+// owning 4 weight row blocks (64 outputs) of a 64-token row tile, and a ring
+// of kStages LDS stages.
+template <int kWaves_, int kStages_>
+struct Shape {
+  static constexpr int kWaves = kWaves_;
+  static constexpr int kStages = kStages_;
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int kCols = kWaves * kNPW * kTileRows;   // weight rows per workgroup
+  static constexpr int kDma = kRows * kChunks / kThreads;   // token-row chunk copies per thread
+  static constexpr int kBatchLoads = kDma + kNPW + 2;        // loads per thread and group
+  // Workgroups per CU: two wavefronts share each SIMD either way.
+  static constexpr int kBlocksPerCu = 8 / kWaves;
+};
+
+// One stage of the LDS ring.  The stages are separate LDS variables, so the
+// compiler can tell the loads landing in one stage from the reads of another
+// and waits only for the stage being read.
+template <int kWaves>
 struct Stage {
   uint16_t a[kRows * kGroup];            // token rows of the group (swizzled chunks)
   uint8_t w[kWaves][kNPW][kTileBytes];   // each wavefront's four weight tiles
   float bias[kWaves][kRows];             // -136 * row sums of the group (a copy per wavefront)
 };
-static_assert(kStages * sizeof(Stage) <= 160 * 1024, "LDS");
-static_assert(kRows * (kCols / 2 + 8) * 2 <= sizeof(Stage), "gate/up epilogue tile");
-static_assert(kRows / 2 * (kCols + 8) * 2 <= sizeof(Stage), "down epilogue half tile");
+
+// Stage S of the ring of a kWaves-wide workgroup (one LDS variable each).
+template <int kWaves, int S>
+__device__ __forceinline__ Stage<kWaves>& stage_mem() {
+  __shared__ __attribute__((aligned(16))) Stage<kWaves> st;
+  return st;
+}
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
@@ -110,29 +137,45 @@ __device__ __forceinline__ float silu_fast(float x) {
 // W13, output act (bf16, grouped order) plus the bias table of act for the
 // down projection.  Otherwise: x = act [pairs][f] in grouped order, weights
 // W2, output pair_out (bf16, pair-id order).
-template <bool kGateUp>
-__global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
+template <bool kGateUp, typename Sh>
+__global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_kernel(
     int d, int f, int top_k, int n_experts, const uint16_t* __restrict__ x, uint32_t x_bytes,
-    const float* __restrict__ x_bias, uint32_t bias_bytes, GroupView gv, WaveArg wave,
-    const uint8_t* __restrict__ slot_bank, int64_t record_bytes, uint16_t* __restrict__ act_out,
-    float* __restrict__ act_bias_out, uint16_t* __restrict__ pair_out) {
-  __shared__ __attribute__((aligned(16))) Stage st0;
-  __shared__ __attribute__((aligned(16))) Stage st1;
-  __shared__ __attribute__((aligned(16))) Stage st2;
-  auto stage_of = [&](auto stage) __attribute__((always_inline)) -> Stage& {
-    constexpr int S = decltype(stage)::value;
-    if constexpr (S == 0) return st0;
-    else if constexpr (S == 1) return st1;
-    else return st2;
+    const float* __restrict__ x_bias, int pairs, GroupView gv, WaveArg wave,
+    const uint8_t* __restrict__ slot_bank, int64_t record_bytes, int n_ctiles,
+    uint16_t* __restrict__ act_out, float* __restrict__ act_bias_out, uint16_t* __restrict__ pair_out) {
+  constexpr int kWaves = Sh::kWaves;
+  constexpr int kStages = Sh::kStages;
+  constexpr int kCols = Sh::kCols;
+  constexpr int kDma = Sh::kDma;
+  constexpr int kBatchLoads = Sh::kBatchLoads;
+  using StageT = Stage<kWaves>;
+  static_assert(kStages * sizeof(StageT) * Sh::kBlocksPerCu <= 160 * 1024, "LDS");
+  static_assert(kRows * (kCols / 2 + 8) * 2 <= sizeof(StageT), "gate/up epilogue tile");
+  static_assert(kRows / 2 * (kCols + 8) * 2 <= sizeof(StageT), "down epilogue half tile");
+  auto stage_of = [&](auto stage) __attribute__((always_inline)) -> StageT& {
+    return stage_mem<kWaves, decltype(stage)::value>();
   };
+  StageT& st0 = stage_mem<kWaves, 0>();
+  StageT& st1 = stage_mem<kWaves, 1>();
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wi = __builtin_amdgcn_readfirstlane(tid >> 6);
 
+  // Work item -> (row tile, column tile).  Workgroup i runs on XCD i % 8;
+  // each XCD takes one contiguous eighth of the items in (row tile, column
+  // tile) order, so the column tiles of a row tile and the row tiles of an
+  // expert meet in one L2 and its token rows and weights cross the fabric
+  // about once.
+  const int n_items = gv.tile_offsets[n_experts] * n_ctiles;
+  const int per_xcd = (n_items + kXcds - 1) / kXcds;
+  const int xj = blockIdx.x / kXcds;
+  if (xj >= per_xcd) return;
+  const int item = (blockIdx.x % kXcds) * per_xcd + xj;
+  if (item >= n_items) return;
+  const int tile = item / n_ctiles;
+  const int ctile = item - tile * n_ctiles;
   // Row tile -> expert (largest e with tile_offsets[e] <= tile).
-  const int tile = blockIdx.y;
-  if (tile >= gv.tile_offsets[n_experts]) return;
   int lo = 0, hi = n_experts;
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
@@ -152,14 +195,14 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
   // A wavefront's 4 row blocks are all valid or all past the end (the number
   // of row blocks is a multiple of 8); a wavefront past the end loads row
   // block 0 so every wavefront issues the same loads, and computes nothing.
-  const int rb_raw = kNPW * (blockIdx.x * kWaves + wi);
+  const int rb_raw = kNPW * (ctile * kWaves + wi);
   const bool wvalid = rb_raw < n_blocks;
   const int rb0 = wvalid ? rb_raw : 0;
   const int n_local = lane & 15;
   const int quarter = lane >> 4;
 
   const __amdgpu_buffer_rsrc_t x_rsrc = make_rsrc(x, x_bytes);
-  const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(x_bias, bias_bytes);
+  const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(x_bias, (uint32_t)((int64_t)pairs * G * 4));
   const __amdgpu_buffer_rsrc_t w_rsrc = make_rsrc(rec, (uint32_t)record_bytes);
 
   // Source row of a tile row (rows past the tile's end repeat its last row;
@@ -168,39 +211,41 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
     const int mc = min(m, rows - 1);
     return kGateUp ? gv.sorted_pairs[row0 + mc] / top_k : row0 + mc;
   };
-  // Token-row chunks this thread copies: stage chunk (2*wi + j)*64 + lane is
-  // row m = 4*(2*wi + j) + lane/16, slot p = lane%16, holding chunk p ^ (m%16).
-  uint32_t a_off[2];
+  // Token-row chunks this thread copies: stage chunk (kDma*wi + j)*64 + lane
+  // is row m = 4*(kDma*wi + j) + lane/16, slot p = lane%16, holding chunk
+  // p ^ (m%16).
+  uint32_t a_off[kDma];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int m = 4 * (2 * wi + j) + (lane >> 4);
+  for (int j = 0; j < kDma; ++j) {
+    const int m = 4 * (kDma * wi + j) + (lane >> 4);
     const int c = (lane & 15) ^ (m & 15);
     a_off[j] = (uint32_t)src_row(m) * (uint32_t)(K * 2) + 16u * c;
   }
-  // Bias: every wavefront copies all 64 rows (lane = row) for itself.
-  const uint32_t b_off = (uint32_t)src_row(lane) * (uint32_t)(G * 4);
+  // Bias: [G][pairs] by grouped position, so a group's 64 row values are one
+  // contiguous run; every wavefront copies it (lane = row) for itself.
+  const uint32_t b_off = (uint32_t)(row0 + min(lane, rows - 1)) * 4u;
   const uint32_t w_off = (uint32_t)((kGateUp ? L.w13_codes : L.w2_codes) +
                                     (int64_t)rb0 * G * kTileBytes) + 16u * lane;
+  // Scales of the wavefront's four row blocks for one group: 128 bytes, the
+  // lane's four (blocks 0..3 of row n_local) in 8 consecutive bytes.
   const uint32_t s_off = (uint32_t)((kGateUp ? L.w13_scales : L.w2_scales) +
-                                    ((int64_t)16 * rb0 + n_local) * G * 2);
+                                    scale_index(16 * rb0, 0, G) * 2) + 8u * n_local;
 
-  uint16_t sc[kStages][kNPW];  // raw fp16 scales of the groups in flight
+  uint2 sc[kStages];  // raw fp16 scales of the groups in flight (block r: half r)
 
   // Issue every load of group g into stage S (same count in every thread).
   auto issue = [&](int g, auto stage) __attribute__((always_inline)) {
-    Stage& sm = stage_of(stage);
+    StageT& sm = stage_of(stage);
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
-      load_lds16(x_rsrc, &sm.a[(2 * wi + j) * 64 * 8], a_off[j], (uint32_t)g * kGroup * 2);
+    for (int j = 0; j < kDma; ++j)
+      load_lds16(x_rsrc, &sm.a[(kDma * wi + j) * 64 * 8], a_off[j], (uint32_t)g * kGroup * 2);
 #pragma unroll
     for (int r = 0; r < kNPW; ++r)
       load_lds16(w_rsrc, &sm.w[wi][r][0], w_off + (uint32_t)(r * G * kTileBytes),
-                   (uint32_t)g * kTileBytes);
-#pragma unroll
-    for (int r = 0; r < kNPW; ++r)
-      sc[decltype(stage)::value][r] = __builtin_amdgcn_raw_buffer_load_b16(w_rsrc, (int)(s_off + (uint32_t)(r * 16 * G * 2)),
-                                                      g * 2, 0);
-    load_lds4(b_rsrc, &sm.bias[wi][0], b_off, (uint32_t)g * 4);
+                 (uint32_t)g * kTileBytes);
+    sc[decltype(stage)::value] = __builtin_bit_cast(
+        uint2, __builtin_amdgcn_raw_buffer_load_b64(w_rsrc, (int)s_off, g * 128, 0));
+    load_lds4(b_rsrc, &sm.bias[wi][0], b_off, (uint32_t)g * (uint32_t)pairs * 4u);
   };
 
   // Dequantization constants, hidden from constant folding (the empty asm
@@ -217,7 +262,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
 
   auto compute = [&](auto stage) __attribute__((always_inline)) {
     constexpr int S = decltype(stage)::value;
-    const Stage& sm = stage_of(stage);
+    const StageT& sm = stage_of(stage);
     f32x4_t c0[4];
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
@@ -245,7 +290,8 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
     }
 #pragma unroll
     for (int r = 0; r < kNPW; ++r) {
-      const float s = half_bits_to_f32(sc[S][r]);
+      const uint32_t sw = r < 2 ? sc[S].x : sc[S].y;
+      const float s = half_bits_to_f32((r & 1) ? sw >> 16 : sw & 0xffffu);
 #pragma unroll
       for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
@@ -253,54 +299,77 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
     }
   };
 
-  // One group: refill the stage freed by the previous group (kMore), compute,
-  // then wait for the next group's loads, leaving the newest batch in flight.
-  // Issuing is decided at compile time so the wait counts stay exact.
+  // One group: refill the stage freed by the previous group with group
+  // g + kStages - 1 (kMore), compute, then wait for the next group's loads
+  // (with three stages the newest batch stays in flight).  Issuing is decided
+  // at compile time so the wait counts stay exact.
   auto step = [&](int g, auto stage, auto more) __attribute__((always_inline)) {
     constexpr int S = decltype(stage)::value;
     constexpr bool kMore = decltype(more)::value;
-    if constexpr (kMore) issue(g + 2, std::integral_constant<int, (S + 2) % kStages>());
+    if constexpr (kMore)
+      issue(g + kStages - 1, std::integral_constant<int, (S + kStages - 1) % kStages>());
     if (wvalid) compute(stage);
-    if constexpr (kMore) wait_loads<kBatchLoads>(); else wait_loads<0>();
+    if constexpr (kMore && kStages == 3) wait_loads<kBatchLoads>(); else wait_loads<0>();
     barrier();
   };
   using Yes = std::true_type;
   using No = std::false_type;
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
-  using S2 = std::integral_constant<int, 2>;
-  // Steps g .. g+lc-1 still issue; the last two do not.  Stages continue from 0.
-  auto tail = [&](int g, auto lc) __attribute__((always_inline)) {
-    constexpr int Lc = decltype(lc)::value;
-    if constexpr (Lc >= 1) step(g, S0(), Yes());
-    if constexpr (Lc >= 2) step(g + 1, S1(), Yes());
-    step(g + Lc, std::integral_constant<int, Lc % kStages>(), No());
-    step(g + Lc + 1, std::integral_constant<int, (Lc + 1) % kStages>(), No());
-  };
+  using S2 = std::integral_constant<int, 2 % kStages>;
 
-  issue(0, S0());
-  if (G > 1) {
-    issue(1, S1());
-    wait_loads<kBatchLoads>();
+  if constexpr (kStages == 3) {
+    // Steps g .. g+lc-1 still issue; the last two do not.  Stages continue
+    // from 0.
+    auto tail = [&](int g, auto lc) __attribute__((always_inline)) {
+      constexpr int Lc = decltype(lc)::value;
+      if constexpr (Lc >= 1) step(g, S0(), Yes());
+      if constexpr (Lc >= 2) step(g + 1, S1(), Yes());
+      step(g + Lc, std::integral_constant<int, Lc % kStages>(), No());
+      step(g + Lc + 1, std::integral_constant<int, (Lc + 1) % kStages>(), No());
+    };
+    issue(0, S0());
+    if (G > 1) {
+      issue(1, S1());
+      wait_loads<kBatchLoads>();
+    } else {
+      wait_loads<0>();
+    }
+    barrier();
+    if (G == 1) {
+      step(0, S0(), No());
+    } else {
+      // Groups 0 .. G-3 issue a later group; whole triples run in the loop.
+      const int n_issue = G - 2;
+      int g = 0;
+      for (; g + kStages <= n_issue; g += kStages) {
+        step(g, S0(), Yes());
+        step(g + 1, S1(), Yes());
+        step(g + 2, S2(), Yes());
+      }
+      const int left = n_issue - g;
+      if (left == 0) tail(g, std::integral_constant<int, 0>());
+      else if (left == 1) tail(g, std::integral_constant<int, 1>());
+      else tail(g, std::integral_constant<int, 2>());
+    }
   } else {
+    // Two stages: groups 0 .. G-2 issue the next group; pairs of steps run in
+    // the loop.
+    issue(0, S0());
     wait_loads<0>();
-  }
-  barrier();
-  if (G == 1) {
-    step(0, S0(), No());
-  } else {
-    // Groups 0 .. G-3 issue a later group; whole triples run in the loop.
-    const int n_issue = G - 2;
+    barrier();
+    const int n_issue = G - 1;
     int g = 0;
-    for (; g + kStages <= n_issue; g += kStages) {
+    for (; g + 2 <= n_issue; g += 2) {
       step(g, S0(), Yes());
       step(g + 1, S1(), Yes());
-      step(g + 2, S2(), Yes());
     }
-    const int left = n_issue - g;
-    if (left == 0) tail(g, std::integral_constant<int, 0>());
-    else if (left == 1) tail(g, std::integral_constant<int, 1>());
-    else tail(g, std::integral_constant<int, 2>());
+    if (n_issue - g == 1) {
+      step(g, S0(), Yes());
+      step(g + 1, S1(), No());
+    } else {
+      step(g, S0(), No());
+    }
   }
 
   // Epilogue.  Lane holds rows m = 16*mi + 4*quarter + j of output column
@@ -308,8 +377,9 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
   // (the stages are free now) and written as 16-byte chunks.
   if (kGateUp) {
     // act = silu(gate) * up (row block 2p is gate, 2p+1 up); the workgroup's
-    // 256 act columns start at 256 * blockIdx.x.
-    constexpr int kStride = 256 + 8;  // row pitch in bf16 (padded against bank conflicts)
+    // kCols/2 act columns start at kCols/2 * ctile.
+    constexpr int kActCols = kCols / 2;   // act columns of this workgroup
+    constexpr int kStride = kActCols + 8;  // row pitch in bf16 (padded against bank conflicts)
     uint16_t* tile_act = reinterpret_cast<uint16_t*>(&st0);
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
@@ -323,16 +393,18 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
               (uint16_t)f32_to_bf16_rne(silu_fast(gv_) * uv);
         }
     barrier();
-    // Thread t copies chunks (row t/32 + 16q, column chunk t%32) and sums
-    // each chunk; the 16 threads of one 128-column group then add their sums
-    // (butterfly), giving the bias of that row and group for the down kernel.
-    const int cc = tid & 31;
-    const int col = 256 * blockIdx.x + 8 * cc;
+    // Thread t copies chunks (row t/R + (kThreads/R)q, column chunk t%R, with
+    // R = kActCols/8 chunks per row) and sums each chunk; the 16 threads of
+    // one 128-column group then add their sums (butterfly), giving the bias
+    // of that row and group for the down kernel.
+    constexpr int R = kActCols / 8;
+    const int cc = tid % R;
+    const int col = kActCols * ctile + 8 * cc;
     const int Gf = f / kGroup;
     const int g = col / kGroup;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int m = (tid >> 5) + 16 * q;
+      const int m = tid / R + (Sh::kThreads / R) * q;
       const uint4 v = *reinterpret_cast<const uint4*>(&tile_act[m * kStride + 8 * cc]);
       const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
       float sum = 0.f;
@@ -347,7 +419,7 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
       sum += __shfl_xor(sum, 8);
       if (m < rows && col < f) {
         *reinterpret_cast<uint4*>(act_out + (int64_t)(row0 + m) * f + col) = v;
-        if ((tid & 15) == 0) act_bias_out[(int64_t)(row0 + m) * Gf + g] = -kCodeBias * sum;
+        if ((tid & 15) == 0) act_bias_out[(int64_t)g * pairs + row0 + m] = -kCodeBias * sum;
       }
     }
   } else {
@@ -366,11 +438,12 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
               (uint16_t)f32_to_bf16_rne(acc[r][mi][j]);
     }
     barrier();
-    const int cc = tid & 63;
-    const int col = kCols * blockIdx.x + 8 * cc;
+    constexpr int R = kCols / 8;   // chunks per output row
+    const int cc = tid % R;
+    const int col = kCols * ctile + 8 * cc;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
-      const int m = (tid >> 6) + 8 * q;
+      const int m = tid / R + (Sh::kThreads / R) * q;
       const uint16_t* t = m < 32 ? half0 : half1;
       if (m < rows && col < d) {
         const uint4 v = *reinterpret_cast<const uint4*>(&t[(m & 31) * kStride + 8 * cc]);
@@ -381,15 +454,18 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_mfma_kernel(
   }
 }
 
-// bias[row][g] = -136 * sum of x[row][128g .. 128g+127] (fp32, fixed order):
-// the accumulator start of the MFMA chains for the gate/up projection.
-__global__ __launch_bounds__(256) void row_bias_kernel(int rows, int K, const uint16_t* __restrict__ x,
+// For every token t and group g, -136 * sum of x[t][128g .. 128g+127] (fp32,
+// fixed order), stored at bias[g][pair_pos[t*top_k + j]] for j < top_k: the
+// accumulator start of the gate/up MFMA chains, by grouped position.
+__global__ __launch_bounds__(256) void row_bias_kernel(int tokens, int K, int top_k,
+                                                       const uint16_t* __restrict__ x,
+                                                       const int32_t* __restrict__ pair_pos,
                                                        float* __restrict__ bias) {
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= tokens) return;
   const int lane = lane_id();
-  const int G = K / kGroup;
-  const uint16_t* xr = x + (int64_t)row * K;
+  const int pairs = tokens * top_k;
+  const uint16_t* xr = x + (int64_t)t * K;
   for (int c0 = 0; c0 < K / 8; c0 += 64) {
     const int c = c0 + lane;
     float s = 0.f;
@@ -407,7 +483,14 @@ __global__ __launch_bounds__(256) void row_bias_kernel(int rows, int K, const ui
     s += __shfl_xor(s, 2);
     s += __shfl_xor(s, 4);
     s += __shfl_xor(s, 8);
-    if ((lane & 15) == 0 && c < K / 8) bias[(int64_t)row * G + c / kChunks] = -kCodeBias * s;
+    // Lanes 16u .. 16u+15 store group c0/16 + u at the positions of the
+    // token's pairs.
+    const int gl = lane >> 4;
+    const float sg = __shfl(s, 16 * gl);
+    const int g = c0 / kChunks + gl;
+    if (g < K / kGroup)
+      for (int j = lane & 15; j < top_k; j += 16)
+        bias[(int64_t)g * pairs + pair_pos[(int64_t)t * top_k + j]] = -kCodeBias * sg;
   }
 }
 
@@ -416,11 +499,23 @@ inline int max_row_tiles(int pairs, int n_experts) {
   return (pairs + kRows - 1) / kRows + e;
 }
 
+// Workgroups for n_ctiles column tiles and up to max_row_tiles row tiles: a
+// multiple of the XCD count, so every XCD gets its eighth of the items.
+inline int mfma_grid(int n_ctiles, int pairs, int n_experts) {
+  const int n = n_ctiles * max_row_tiles(pairs, n_experts);
+  return (n + kXcds - 1) / kXcds * kXcds;
+}
+
+// Launch shape of both projections.
+using MfmaShape = Shape<EMOE_MFMA_WAVES, EMOE_MFMA_STAGES>;
+
 }  // namespace
 
-hipError_t launch_row_bias(int rows, int K, const uint16_t* x, float* bias, hipStream_t stream) {
-  if (rows == 0) return hipSuccess;
-  launch(row_bias_kernel, dim3((rows + 3) / 4), dim3(256), stream, rows, K, x, bias);
+hipError_t launch_row_bias(int tokens, int K, int top_k, const uint16_t* x, const int32_t* pair_pos,
+                           float* bias, hipStream_t stream) {
+  if (tokens == 0) return hipSuccess;
+  launch(row_bias_kernel, dim3((tokens + 3) / 4), dim3(256), stream, tokens, K, top_k, x, pair_pos,
+         bias);
   return hipGetLastError();
 }
 
@@ -430,10 +525,12 @@ hipError_t launch_gateup_mfma(int tokens, int d, int f, int top_k, int n_experts
                               float* act_bias, hipStream_t stream) {
   const int pairs = tokens * top_k;
   if (pairs == 0) return hipSuccess;
-  dim3 grid((2 * f + kCols - 1) / kCols, max_row_tiles(pairs, n_experts));
-  launch(grouped_mfma_kernel<true>, grid, dim3(kThreads), stream, d, f, top_k, n_experts, h,
-         (uint32_t)((int64_t)tokens * d * 2), h_bias, (uint32_t)((int64_t)tokens * (d / kGroup) * 4),
-         gv, wave, slot_bank, record_bytes, act, act_bias, (uint16_t*)nullptr);
+  constexpr int kCols = MfmaShape::kCols;
+  const int n_ctiles = (2 * f + kCols - 1) / kCols;
+  launch(grouped_mfma_kernel<true, MfmaShape>, dim3(mfma_grid(n_ctiles, pairs, n_experts)),
+         dim3(MfmaShape::kThreads), stream, d, f, top_k, n_experts, h,
+         (uint32_t)((int64_t)tokens * d * 2), h_bias, pairs,
+         gv, wave, slot_bank, record_bytes, n_ctiles, act, act_bias, (uint16_t*)nullptr);
   return hipGetLastError();
 }
 
@@ -443,10 +540,12 @@ hipError_t launch_down_mfma(int tokens, int d, int f, int top_k, int n_experts, 
                             hipStream_t stream) {
   const int pairs = tokens * top_k;
   if (pairs == 0) return hipSuccess;
-  dim3 grid((d + kCols - 1) / kCols, max_row_tiles(pairs, n_experts));
-  launch(grouped_mfma_kernel<false>, grid, dim3(kThreads), stream, d, f, top_k, n_experts, act,
-         (uint32_t)((int64_t)pairs * f * 2), act_bias, (uint32_t)((int64_t)pairs * (f / kGroup) * 4),
-         gv, wave, slot_bank, record_bytes, (uint16_t*)nullptr, (float*)nullptr, pair_out);
+  constexpr int kCols = MfmaShape::kCols;
+  const int n_ctiles = (d + kCols - 1) / kCols;
+  launch(grouped_mfma_kernel<false, MfmaShape>, dim3(mfma_grid(n_ctiles, pairs, n_experts)),
+         dim3(MfmaShape::kThreads), stream, d, f, top_k, n_experts, act,
+         (uint32_t)((int64_t)pairs * f * 2), act_bias, pairs,
+         gv, wave, slot_bank, record_bytes, n_ctiles, (uint16_t*)nullptr, (float*)nullptr, pair_out);
   return hipGetLastError();
 }
 

@@ -97,7 +97,7 @@ __global__ __launch_bounds__(256) void quantize_kernel(int d, int f, int tiles_w
   if (quarter == 0) {
     const int n = rb * kTileRows + n_local;  // row in this matrix (W13 row order for W13)
     uint16_t* sc = reinterpret_cast<uint16_t*>(rec + scales_off);
-    sc[(int64_t)n * G + g] = zero ? (uint16_t)0 : __half_as_ushort(s16h);
+    sc[scale_index(n, g, G)] = zero ? (uint16_t)0 : __half_as_ushort(s16h);
   }
 }
 

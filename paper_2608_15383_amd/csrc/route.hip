@@ -95,10 +95,11 @@ constexpr int kGroupThreads = 1024;
 __global__ __launch_bounds__(kGroupThreads) void group_kernel(
     int pairs, int n_experts, const int32_t* __restrict__ ids, int32_t* __restrict__ counts,
     int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_pairs, int32_t* __restrict__ active,
-    int32_t* __restrict__ n_active, int32_t* __restrict__ tile_offsets) {
+    int32_t* __restrict__ n_active, int32_t* __restrict__ tile_offsets,
+    int32_t* __restrict__ pair_pos) {
   __shared__ GroupShared<kGroupThreads> sh;
   block_group<kGroupThreads, false>(sh, pairs, n_experts, ids, counts, offsets, sorted_pairs,
-                                    active, n_active, tile_offsets, nullptr);
+                                    active, n_active, tile_offsets, pair_pos);
 }
 
 // Grouping spread over many workgroups (large calls): 64-pair chunks, one per
@@ -135,7 +136,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void chunk_place_kernel(
     const int32_t* __restrict__ chunk_counts, int32_t* __restrict__ counts,
     int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_pairs,
     int32_t* __restrict__ active, int32_t* __restrict__ n_active,
-    int32_t* __restrict__ tile_offsets) {
+    int32_t* __restrict__ tile_offsets, int32_t* __restrict__ pair_pos) {
   __shared__ int part_all[kChunkWaves][EMOE_MAX_EXPERTS];
   __shared__ int part_pre[kChunkWaves][EMOE_MAX_EXPERTS];
   __shared__ int base[kChunkWaves][EMOE_MAX_EXPERTS];
@@ -228,7 +229,11 @@ __global__ __launch_bounds__(64 * kChunkWaves) void chunk_place_kernel(
   const int e = valid ? ids[i] : 0;
   const uint64_t m = match_expert(valid, e, bits);
   const int rank = __popcll(m & ((1ull << lane) - 1ull));
-  if (valid) sorted_pairs[base[wave][e] + rank] = i;
+  if (valid) {
+    const int pos = base[wave][e] + rank;
+    sorted_pairs[pos] = i;
+    pair_pos[i] = pos;
+  }
 }
 
 }  // namespace
@@ -245,11 +250,11 @@ hipError_t launch_group_count(int pairs, int n_experts, const int32_t* topk_ids,
 hipError_t launch_group_place(int pairs, int n_experts, const int32_t* topk_ids,
                               const int32_t* chunk_counts, int32_t* counts, int32_t* offsets,
                               int32_t* sorted_pairs, int32_t* active, int32_t* n_active,
-                              int32_t* tile_offsets, hipStream_t stream) {
+                              int32_t* tile_offsets, int32_t* pair_pos, hipStream_t stream) {
   const int n_wg = ((pairs + 63) / 64 + kChunkWaves - 1) / kChunkWaves;
   if (n_wg == 0) return hipSuccess;
   launch(chunk_place_kernel, dim3(n_wg), dim3(64 * kChunkWaves), stream, pairs, n_experts, topk_ids,
-         chunk_counts, counts, offsets, sorted_pairs, active, n_active, tile_offsets);
+         chunk_counts, counts, offsets, sorted_pairs, active, n_active, tile_offsets, pair_pos);
   return hipGetLastError();
 }
 
@@ -271,9 +276,10 @@ hipError_t launch_topk(int tokens, int n_experts, int top_k, int renormalize, co
 
 hipError_t launch_group(int pairs, int n_experts, const int32_t* topk_ids, int32_t* counts,
                         int32_t* offsets, int32_t* sorted_pairs, int32_t* active,
-                        int32_t* n_active, int32_t* tile_offsets, hipStream_t stream) {
+                        int32_t* n_active, int32_t* tile_offsets, int32_t* pair_pos,
+                        hipStream_t stream) {
   launch(group_kernel, dim3(1), dim3(kGroupThreads), stream, pairs, n_experts, topk_ids, counts,
-         offsets, sorted_pairs, active, n_active, tile_offsets);
+         offsets, sorted_pairs, active, n_active, tile_offsets, pair_pos);
   return hipGetLastError();
 }
 
