@@ -2,20 +2,21 @@
 // (prefill / large batches), where each expert's projection is a dense
 // contraction over its token rows.
 //
-// A workgroup of kWaves wavefronts owns one row tile (up to 64 token rows of
-// one expert, grouped order) and one column tile of 64*kWaves weight rows;
-// each wavefront owns 4 weight row-blocks (64 outputs) for all 64 rows.  The
-// default shape is 4 wavefronts and a ring of 2 LDS stages (66 KB), so two
-// workgroups share a CU and their wavefronts, not barrier-aligned with each
-// other, fill each other's load and barrier gaps on the matrix cores.
-//  - Per 128-input group, the token rows (16 KB) and each wavefront's four
-//    packed weight tiles (4 KB) are copied from memory straight into LDS by
-//    buffer loads with the LDS destination (no register staging), one group
-//    ahead of its use.  The 16-byte chunks of a token row are XOR-swizzled by
-//    the row index, which makes the MFMA A-fragment reads free of bank
-//    conflicts.  The per-row bias of the group is one contiguous 256-byte run
-//    and the wavefront's 64 scales one 8-byte load per lane, so a group costs
-//    each wavefront 10 vector memory instructions.
+// A workgroup of 4 wavefronts owns one row tile (up to 64 token rows of one
+// expert, grouped order) and one column tile of 256 weight rows; each
+// wavefront owns 4 weight row-blocks (64 outputs) for all 64 rows.  Two
+// workgroups share a CU (34 KB of LDS each, 256 VGPRs per lane), and their
+// wavefronts, not barrier-aligned with each other, fill each other's load
+// and barrier gaps on the matrix cores.
+//  - Per 128-input group, the token rows (16 KB, shared by the workgroup) are
+//    copied from memory straight into LDS by buffer loads with the LDS
+//    destination, and each wavefront's four packed weight tiles (its 16 bytes
+//    of each) go straight into registers; both one group ahead of their use,
+//    in a ring of two stages.  The 16-byte chunks of a token row are
+//    XOR-swizzled by the row index, which makes the MFMA A-fragment reads free
+//    of bank conflicts.  The per-row bias of the group is one contiguous
+//    256-byte run and the wavefront's 64 scales one 8-byte load per lane, so a
+//    group costs each wavefront 10 vector memory instructions.
 //  - Each dword of codes expands in registers to one B operand of
 //    v_mfma_f32_16x16x32_bf16 (record layout in common.h): the codes enter as
 //    bf16 (128 + u), and the chain of four MFMAs of a group starts from the
@@ -32,10 +33,6 @@
 
 #include "common.h"
 
-#ifndef EMOE_MFMA_WAVES
-#define EMOE_MFMA_WAVES 4
-#define EMOE_MFMA_STAGES 2
-#endif
 
 namespace emoe {
 namespace {
@@ -51,26 +48,23 @@ constexpr int kXcds = 8;                                  // accelerator complex
 
 // Shape of a grouped-projection launch: kWaves wavefronts per workgroup, each
 // owning 4 weight row blocks (64 outputs) of a 64-token row tile, and a ring
-// of kStages LDS stages.
-template <int kWaves_, int kStages_>
+// of two stages (LDS for the token rows, registers for the weights).
+template <int kWaves_>
 struct Shape {
   static constexpr int kWaves = kWaves_;
-  static constexpr int kStages = kStages_;
+  static constexpr int kStages = 2;
   static constexpr int kThreads = 64 * kWaves;
   static constexpr int kCols = kWaves * kNPW * kTileRows;   // weight rows per workgroup
   static constexpr int kDma = kRows * kChunks / kThreads;   // token-row chunk copies per thread
-  static constexpr int kBatchLoads = kDma + kNPW + 2;        // loads per thread and group
   // Workgroups per CU: two wavefronts share each SIMD either way.
   static constexpr int kBlocksPerCu = 8 / kWaves;
 };
 
 // One stage of the LDS ring.  The stages are separate LDS variables, so the
-// compiler can tell the loads landing in one stage from the reads of another
-// and waits only for the stage being read.
+// compiler can tell the loads landing in one stage from the reads of another.
 template <int kWaves>
 struct Stage {
   uint16_t a[kRows * kGroup];            // token rows of the group (swizzled chunks)
-  uint8_t w[kWaves][kNPW][kTileBytes];   // each wavefront's four weight tiles
   float bias[kWaves][kRows];             // -136 * row sums of the group (a copy per wavefront)
 };
 
@@ -147,7 +141,6 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   constexpr int kStages = Sh::kStages;
   constexpr int kCols = Sh::kCols;
   constexpr int kDma = Sh::kDma;
-  constexpr int kBatchLoads = Sh::kBatchLoads;
   using StageT = Stage<kWaves>;
   static_assert(kStages * sizeof(StageT) * Sh::kBlocksPerCu <= 160 * 1024, "LDS");
   static_assert(kRows * (kCols / 2 + 8) * 2 <= sizeof(StageT), "gate/up epilogue tile");
@@ -231,9 +224,13 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   const uint32_t s_off = (uint32_t)((kGateUp ? L.w13_scales : L.w2_scales) +
                                     scale_index(16 * rb0, 0, G) * 2) + 8u * n_local;
 
-  uint2 sc[kStages];  // raw fp16 scales of the groups in flight (block r: half r)
+  // Registers of the groups in flight: fp16 scales (block r in half r) and
+  // the codes of the four weight tiles (lane's 16 bytes of each).
+  uint2 sc[kStages];
+  uint4 wreg[kStages][kNPW];
 
-  // Issue every load of group g into stage S (same count in every thread).
+  // Issue every load of group g into stage S (same count in every thread):
+  // token rows and bias into LDS, weight codes and scales into registers.
   auto issue = [&](int g, auto stage) __attribute__((always_inline)) {
     StageT& sm = stage_of(stage);
 #pragma unroll
@@ -241,8 +238,8 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
       load_lds16(x_rsrc, &sm.a[(kDma * wi + j) * 64 * 8], a_off[j], (uint32_t)g * kGroup * 2);
 #pragma unroll
     for (int r = 0; r < kNPW; ++r)
-      load_lds16(w_rsrc, &sm.w[wi][r][0], w_off + (uint32_t)(r * G * kTileBytes),
-                 (uint32_t)g * kTileBytes);
+      wreg[decltype(stage)::value][r] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(w_rsrc, (int)(w_off + (uint32_t)(r * G * kTileBytes)),
+                   g * kTileBytes, 0));
     sc[decltype(stage)::value] = __builtin_bit_cast(
         uint2, __builtin_amdgcn_raw_buffer_load_b64(w_rsrc, (int)s_off, g * 128, 0));
     load_lds4(b_rsrc, &sm.bias[wi][0], b_off, (uint32_t)g * (uint32_t)pairs * 4u);
@@ -269,7 +266,7 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
       c0[mi] = *reinterpret_cast<const f32x4_t*>(&sm.bias[wi][16 * mi + 4 * quarter]);
     uint4 wc[kNPW];
 #pragma unroll
-    for (int r = 0; r < kNPW; ++r) wc[r] = *reinterpret_cast<const uint4*>(&sm.w[wi][r][16 * lane]);
+    for (int r = 0; r < kNPW; ++r) wc[r] = wreg[S][r];
     f32x4_t tmp[kNPW][4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -299,77 +296,35 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
     }
   };
 
-  // One group: refill the stage freed by the previous group with group
-  // g + kStages - 1 (kMore), compute, then wait for the next group's loads
-  // (with three stages the newest batch stays in flight).  Issuing is decided
-  // at compile time so the wait counts stay exact.
+  // One group: load the next group into the other stage, compute this one,
+  // then wait for the loads and hand the stages over.  Issuing is decided at
+  // compile time so the wait counts stay exact.
   auto step = [&](int g, auto stage, auto more) __attribute__((always_inline)) {
     constexpr int S = decltype(stage)::value;
-    constexpr bool kMore = decltype(more)::value;
-    if constexpr (kMore)
-      issue(g + kStages - 1, std::integral_constant<int, (S + kStages - 1) % kStages>());
+    if constexpr (decltype(more)::value) issue(g + 1, std::integral_constant<int, S ^ 1>());
     if (wvalid) compute(stage);
-    if constexpr (kMore && kStages == 3) wait_loads<kBatchLoads>(); else wait_loads<0>();
+    wait_loads<0>();
     barrier();
   };
   using Yes = std::true_type;
   using No = std::false_type;
   using S0 = std::integral_constant<int, 0>;
   using S1 = std::integral_constant<int, 1>;
-  using S2 = std::integral_constant<int, 2 % kStages>;
 
-  if constexpr (kStages == 3) {
-    // Steps g .. g+lc-1 still issue; the last two do not.  Stages continue
-    // from 0.
-    auto tail = [&](int g, auto lc) __attribute__((always_inline)) {
-      constexpr int Lc = decltype(lc)::value;
-      if constexpr (Lc >= 1) step(g, S0(), Yes());
-      if constexpr (Lc >= 2) step(g + 1, S1(), Yes());
-      step(g + Lc, std::integral_constant<int, Lc % kStages>(), No());
-      step(g + Lc + 1, std::integral_constant<int, (Lc + 1) % kStages>(), No());
-    };
-    issue(0, S0());
-    if (G > 1) {
-      issue(1, S1());
-      wait_loads<kBatchLoads>();
-    } else {
-      wait_loads<0>();
-    }
-    barrier();
-    if (G == 1) {
-      step(0, S0(), No());
-    } else {
-      // Groups 0 .. G-3 issue a later group; whole triples run in the loop.
-      const int n_issue = G - 2;
-      int g = 0;
-      for (; g + kStages <= n_issue; g += kStages) {
-        step(g, S0(), Yes());
-        step(g + 1, S1(), Yes());
-        step(g + 2, S2(), Yes());
-      }
-      const int left = n_issue - g;
-      if (left == 0) tail(g, std::integral_constant<int, 0>());
-      else if (left == 1) tail(g, std::integral_constant<int, 1>());
-      else tail(g, std::integral_constant<int, 2>());
-    }
+  issue(0, S0());
+  wait_loads<0>();
+  barrier();
+  // Groups 0 .. G-2 issue the next group; pairs of steps run in the loop.
+  int g = 0;
+  for (; g + 2 <= G - 1; g += 2) {
+    step(g, S0(), Yes());
+    step(g + 1, S1(), Yes());
+  }
+  if (G - 1 - g == 1) {
+    step(g, S0(), Yes());
+    step(g + 1, S1(), No());
   } else {
-    // Two stages: groups 0 .. G-2 issue the next group; pairs of steps run in
-    // the loop.
-    issue(0, S0());
-    wait_loads<0>();
-    barrier();
-    const int n_issue = G - 1;
-    int g = 0;
-    for (; g + 2 <= n_issue; g += 2) {
-      step(g, S0(), Yes());
-      step(g + 1, S1(), Yes());
-    }
-    if (n_issue - g == 1) {
-      step(g, S0(), Yes());
-      step(g + 1, S1(), No());
-    } else {
-      step(g, S0(), No());
-    }
+    step(g, S0(), No());
   }
 
   // Epilogue.  Lane holds rows m = 16*mi + 4*quarter + j of output column
@@ -507,7 +462,7 @@ inline int mfma_grid(int n_ctiles, int pairs, int n_experts) {
 }
 
 // Launch shape of both projections.
-using MfmaShape = Shape<EMOE_MFMA_WAVES, EMOE_MFMA_STAGES>;
+using MfmaShape = Shape<4>;
 
 }  // namespace
 
