@@ -106,8 +106,8 @@ struct emoe_cache {
   std::vector<hipEvent_t> release;  // [C] completion of the last wave using the slot
   hipEvent_t ready = nullptr;       // completion of the last batch of fills
   int32_t* counts_host = nullptr;   // pinned [E]: the batched expert-id transfer
-  DecodeSync* sync = nullptr;       // device: counters of the fused decode launches
-  DecodeProgress prog;              // host: totals that set each fused launch's targets
+  DecodeSync* sync = nullptr;       // device: hand-over data of the fused decode launches
+  DecodeProgress prog;              // host: epoch of the last fused launch
 };
 
 namespace {
@@ -439,9 +439,9 @@ int32_t emoe_cache_sync_timeouts(const emoe_cache* c, int64_t* timeouts) {
   *timeouts = 0;
   if (!c->sync) return EMOE_OK;
   EMOE_HIP(hipDeviceSynchronize());
-  DecodeSync s;
-  EMOE_HIP(hipMemcpy(&s, c->sync, sizeof s, hipMemcpyDeviceToHost));
-  *timeouts = s.timeouts;
+  uint32_t t = 0;
+  EMOE_HIP(hipMemcpy(&t, &c->sync->timeouts, sizeof t, hipMemcpyDeviceToHost));
+  *timeouts = t;
   return EMOE_OK;
 }
 

@@ -3,7 +3,7 @@
 // weighted combine in one kernel.
 //
 // On MI355X a kernel boundary costs about 2.4 us and a dependent round trip to
-// memory about 1.5 us under load, against roughly 5 us to stream the decode
+// memory about 1 us under load, against roughly 5 us to stream the decode
 // layer's 26 MB of packed weights.  The six-kernel sequence is therefore
 // replaced by one grid whose workgroups play three roles by index:
 //   [0, nR)        router items: logits of 4 experts for every token;
@@ -11,18 +11,19 @@
 //   [nR+nG, ...)   down items (output row-block rb of every token).
 // Every gate/up and down workgroup waits for the router items, reads the
 // logits and runs the top-k itself (cheap, and it saves the round trips of
-// publishing the selection).  Down items then prefetch their down tiles while
-// the gate/up items stream theirs, wait for all gate/up items, and add the k
-// expert outputs of each token in rank order.  Down item 0 finally writes the
-// routing and grouping arrays to the workspace, as the unfused path does.
+// publishing the selection); gate/up items stage the token rows in LDS while
+// they wait.  Down items prefetch their down tiles while the gate/up items
+// stream theirs, pick up each activation row as it is produced, and add the
+// k expert outputs of each token in rank order.  Down item 0 finally writes
+// the routing and grouping arrays to the workspace, as the unfused path does.
 //
-// A workgroup only waits for workgroups of lower index, which the hardware
-// dispatches first, and the grid is sized to be co-resident on an idle GPU.
-// Every wait is still bounded and counts a timeout instead of spinning
-// forever.  Data crossing workgroups is written and read device-coherently and
-// ordered by waiting for outstanding memory operations before a counter is
-// bumped, so no cache-wide fence is needed.  Counters only grow; the host
-// derives each launch's targets from its running totals.
+// Data crossing workgroups (logits, activation rows) travels as 64-bit words
+// tagged with the launch's epoch, written and read device-coherently: the
+// reader polls the data itself, so one store is both the payload and the
+// signal, and nothing needs resetting between launches.  A workgroup only
+// waits for workgroups of lower index, which the hardware dispatches first,
+// and the grid is sized to be co-resident on an idle GPU.  Every wait is
+// still bounded and counts a timeout instead of spinning forever.
 //
 // The arithmetic is that of the stand-alone kernels (device_route.h,
 // device_gemv.h), so the result is bit-identical to the unfused path.
@@ -38,26 +39,42 @@ namespace {
 constexpr uint32_t kSpinLimit = 1u << 20;
 constexpr int kPollSleep = 8;  // s_sleep units (64 clocks) between polls
 
-__device__ __forceinline__ bool reached(uint32_t v, uint32_t target) {
-  return (int32_t)(v - target) >= 0;  // modulo-2^32 comparison
-}
-
-// Wait (bounded) until the gate/up counters of pair pi reach their targets;
-// one wavefront (lanes 0 .. cpp-1 each poll one counter).
-__device__ __forceinline__ void wave_wait_pair(DecodeSync* sy, const DecodeArgs& a, int pi) {
+// Stage the activation rows of pairs p0, p0 + step, ... < P from the tagged
+// words (DecodeSync::act) in LDS act_lds ([pair][f] bf16), reading each row
+// until every word carries this launch's epoch (bounded); one wavefront.
+__device__ __forceinline__ void wave_stage_act_rows(DecodeSync* sy, const DecodeArgs& a, int p0,
+                                                    int step, int P, uint32_t* act_lds) {
+  constexpr int kWords = 8;  // words per lane per read
   const int lane = lane_id();
-  const int cpp = a.counters_per_pair;
-  const int c = pi * cpp + lane;
-  const uint32_t tgt = lane < cpp ? a.gate_target[c] : 0u;
-  uint32_t it = 0;
-  while (true) {
-    const bool ok = lane >= cpp || reached(ld_u32<true>(&sy->gate_done[c][0]), tgt);
-    if (__all(ok)) break;
-    if (++it > kSpinLimit) {
-      if (lane == 0) atomicAdd(&sy->timeouts, 1u);
-      break;
+  const int nw = a.f / 2;  // words per row, a multiple of 64
+  for (int pi = p0; pi < P; pi += step) {
+    const uint64_t* src = sy->act + (int64_t)pi * nw;
+    uint32_t* dst = act_lds + pi * nw;
+    for (int w0 = 0; w0 < nw; w0 += 64 * kWords) {
+      uint32_t it = 0;
+      while (true) {
+        uint64_t x[kWords];
+#pragma unroll
+        for (int k = 0; k < kWords; ++k) {
+          const int w = w0 + 64 * k + lane;
+          x[k] = w < nw ? __hip_atomic_load(src + w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                        : ((uint64_t)a.epoch << 32);
+        }
+        bool ok = true;
+#pragma unroll
+        for (int k = 0; k < kWords; ++k) {
+          const int w = w0 + 64 * k + lane;
+          ok = ok && (uint32_t)(x[k] >> 32) == a.epoch;
+          if (w < nw) dst[w] = (uint32_t)x[k];
+        }
+        if (__all(ok)) break;
+        if (++it > kSpinLimit) {
+          if (lane == 0) atomicAdd(&sy->timeouts, 1u);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(kPollSleep);
+      }
     }
-    __builtin_amdgcn_s_sleep(kPollSleep);
   }
 }
 
@@ -74,13 +91,6 @@ __device__ __forceinline__ void wave_copy_to_lds(const void* src, uint32_t bytes
         (int)voff, (int)off, 0, /*sc1*/ 16);
 }
 
-// Make this workgroup's coherent stores visible, then bump *p.
-__device__ __forceinline__ void block_signal(uint32_t* p) {
-  wait_memory();
-  __syncthreads();
-  if (threadIdx.x == 0) atomicAdd(p, 1u);
-}
-
 __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   __shared__ GroupShared<256> gsh;
   __shared__ GateUpShared gush;
@@ -89,6 +99,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   __shared__ float s_w[kFusedMaxPairs];
   __shared__ uint4 s_act[kFusedActLdsBytes / 16];
   __shared__ float s_xs[kFusedActLdsBytes / (2 * kGroup) * 4];  // [pair][group][quarter]
+  __shared__ uint64_t s_topk[kFusedMaxTokens][64];                // top-k scratch per token
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -122,13 +133,26 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     return;
   }
 
+  // Gate/up workgroups stage the token rows of h in LDS (s_act, which only
+  // down workgroups use otherwise) while the router runs: 256-byte chunks
+  // round-robin over the wavefronts.
+  const bool is_gate = blk < a.n_router + a.n_gate;
+  const uint16_t* h_lds = reinterpret_cast<const uint16_t*>(s_act);
+  if (is_gate) {
+    const uint32_t bytes = (uint32_t)a.tokens * (uint32_t)a.d * 2u;
+    for (uint32_t off = 256u * wi; off < bytes; off += 256u * kGemvWaves)
+      wave_copy_to_lds(reinterpret_cast<const uint8_t*>(a.h) + off, 256u,
+                       reinterpret_cast<uint8_t*>(s_act) + off);
+  }
+
   // Every other workgroup: wavefront wi < T waits for token wi's logits (this
   // launch's epoch in every tag) and selects its experts.
   const int replica = blk % kSyncLanes;
   TopkState st;
   if (wi < a.tokens) {
     if (a.logits_override) {
-      wave_topk_select<false>(a.logits_override + (int64_t)wi * a.n_experts, a.n_experts, a.top_k, st);
+      wave_topk_select<false>(a.logits_override + (int64_t)wi * a.n_experts, a.n_experts, a.top_k,
+                              st, s_topk[wi]);
     } else {
       const uint64_t* zt = sy->logits[replica] + wi * a.n_experts;
       uint32_t it = 0;
@@ -152,13 +176,14 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
         }
         __builtin_amdgcn_s_sleep(kPollSleep);
       }
-      wave_topk_select_loaded(a.n_experts, a.top_k, st);
+      wave_topk_select_loaded(a.n_experts, a.top_k, st, s_topk[wi]);
     }
     wave_topk_store_ids<false>(st, a.top_k, s_ids + wi * a.top_k);
   }
+  if (is_gate) wait_memory();  // the staged rows
   __syncthreads();
 
-  if (blk < a.n_router + a.n_gate) {
+  if (is_gate) {
     // ---------------------------------------------------------------- gate/up
     // Item = (pair pi, row-block pairs b0 ..): one token row of one expert.
     // The activation goes to act row pi (pair order).
@@ -170,11 +195,17 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     const int b1 = min(b0 + a.pairs_per_item, pairs_of_f);
     const int e = s_ids[pi];
     const int top_k = a.top_k;
+    // The activation goes out as tagged words (DecodeSync::act), which the
+    // down workgroups poll directly: the store is the signal.
+    const int d = a.d, f = a.f;
+    const uint64_t tag = (uint64_t)a.epoch << 32;
+    uint64_t* act_tag = sy->act;
     for (int b = b0; b < b1; ++b)
-      gateup_rows<true>(gush, a.d, a.f, a.h, [top_k](int s) { return s / top_k; }, pi, pi + 1,
-                        a.slot_bank + (int64_t)e * a.record_bytes, b, a.act);
-    const int cpp = a.counters_per_pair;
-    block_signal(&sy->gate_done[pi * cpp + (item % chunks) % cpp][0]);
+      gateup_rows(gush, a.d, a.f, [=](int s) { return h_lds + (s / top_k) * d; }, pi, pi + 1,
+                  a.slot_bank + (int64_t)e * a.record_bytes, b, [=](int s, int n, uint32_t v) {
+                    __hip_atomic_store(act_tag + ((s * f + n) >> 1), tag | v, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                  });
     return;
   }
 
@@ -193,15 +224,12 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   if (wi < a.tokens)
     wave_topk_weights<false>(st, a.n_experts, a.top_k, a.renormalize, s_w + wi * a.top_k);
 
-  // Pair by pair, as soon as its gate/up workgroups are done: copy its
-  // activation row to LDS, its per-(group, quarter) activation sums, then its
-  // expert output for this row block.  Wavefront wi owns pairs wi, wi+4, ...
+  // Each wavefront stages its pairs' activation rows in LDS as the gate/up
+  // workgroups produce them, then computes their per-(group, quarter)
+  // activation sums and their expert outputs for this row block.  Wavefront
+  // wi owns pairs wi, wi+4, ...
   const uint16_t* act_lds = reinterpret_cast<const uint16_t*>(s_act);
-  for (int pi = wi; pi < P; pi += kGemvWaves) {
-    wave_wait_pair(sy, a, pi);
-    wave_copy_to_lds(a.act + (int64_t)pi * a.f, (uint32_t)a.f * 2u, s_act + pi * (a.f / 8));
-  }
-  wait_memory();
+  wave_stage_act_rows(sy, a, wi, kGemvWaves, P, reinterpret_cast<uint32_t*>(s_act));
   for (int pi = wi; pi < P; pi += kGemvWaves) {
     for (int i = lane; i < G * 4; i += 64) {
       const int g = i >> 2, q = i & 3;
@@ -283,6 +311,7 @@ bool decode_fused_plan(DecodeArgs& a) {
   if (a.tokens < 1 || a.tokens > kFusedMaxTokens || a.tokens * a.top_k > kFusedMaxPairs)
     return false;
   if ((int64_t)a.tokens * a.top_k * a.f * 2 > kFusedActLdsBytes) return false;
+  if ((int64_t)a.tokens * a.d * 2 > kFusedActLdsBytes) return false;  // staged token rows
   const int P = a.tokens * a.top_k;
   const int pairs_of_f = a.f / kTileRows;
   a.n_router = a.logits_override ? 1 : (a.n_experts + 3) / 4;
@@ -293,11 +322,7 @@ bool decode_fused_plan(DecodeArgs& a) {
     const int n_gate = P * chunks;
     if (a.n_router + n_gate + a.n_down <= cap) {
       a.pairs_per_item = ppi;
-      a.items_per_pair = chunks;
       a.n_gate = n_gate;
-      int cpp = kGateCounters / P;  // >= 1: P <= kFusedMaxPairs = kGateCounters
-      if (cpp > chunks) cpp = chunks;
-      a.counters_per_pair = cpp;
       return true;
     }
   }
@@ -307,19 +332,9 @@ bool decode_fused_plan(DecodeArgs& a) {
 hipError_t launch_decode_fused(DecodeArgs& a, DecodeProgress& prog, hipStream_t stream) {
   a.epoch = prog.epoch + 1u;
   if (a.epoch == 0u) a.epoch = 1u;  // 0 is the zeroed memory's tag
-  // Pair pi's items i = 0 .. chunks-1 signal counter pi*cpp + i % cpp.
-  const int P = a.tokens * a.top_k, cpp = a.counters_per_pair, chunks = a.items_per_pair;
-  for (int c = 0; c < kGateCounters; ++c) {
-    const int j = c % cpp;
-    const uint32_t n = c < P * cpp ? (uint32_t)((chunks - j + cpp - 1) / cpp) : 0u;
-    a.gate_target[c] = prog.gate_total[c] + n;
-  }
   launch(decode_fused_kernel, dim3(a.n_router + a.n_gate + a.n_down), dim3(256), stream, a);
   const hipError_t e = hipGetLastError();
-  if (e == hipSuccess) {
-    prog.epoch = a.epoch;
-    for (int c = 0; c < kGateCounters; ++c) prog.gate_total[c] = a.gate_target[c];
-  }
+  if (e == hipSuccess) prog.epoch = a.epoch;
   return e;
 }
 

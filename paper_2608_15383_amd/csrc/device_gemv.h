@@ -28,6 +28,14 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
                                         __builtin_bit_cast(bf16x2_t, b), c, false);
 }
 
+// A loaded value made opaque here: the compiler cannot consume it (and so
+// wait for its load) any earlier, which keeps a prefetched batch's loads in
+// flight until the batch is used.
+__device__ __forceinline__ uint32_t at_use(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 __device__ __forceinline__ void dequant_dword(uint32_t dw, uint32_t* out) {
 #pragma unroll
   for (int p = 0; p < 4; ++p) out[p] = ((dw >> (4 * p)) & 0x000f000fu) | 0x43004300u;
@@ -70,15 +78,15 @@ struct GateUpShared {
 // One workgroup of kGemvWaves wavefronts computes the SwiGLU activation
 // phi(W_g h) * (W_u h) of gate/up row-block pair b (outputs 16b .. 16b+15) for
 // the rows s in [begin, end) of one expert whose packed record is `rec`;
-// token_of(s) is the token of row s and the result goes to act row s (bf16,
-// pairs of outputs per 32-bit store).  The wavefronts split the input
-// groups round-robin and meet in LDS in wavefront order.  Each row's result
-// depends only on that row, not on which rows share the pass.
-template <bool kCo, typename TokenOf>
-__device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f,
-                                            const uint16_t* __restrict__ h, TokenOf token_of,
-                                            int begin, int end, const uint8_t* __restrict__ rec,
-                                            int b, uint16_t* __restrict__ act);
+// x_row(s) points at the d activations of row s (global memory or LDS), and
+// store(s, n, v) receives outputs n, n+1 of row s (n even) as a bf16 pair in
+// v (low half: output n).  The wavefronts split the input groups round-robin
+// and meet in LDS in wavefront order.  Each row's result depends only on that
+// row, not on which rows share the pass.
+template <typename XRow, typename Store>
+__device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f, XRow x_row, int begin,
+                                            int end, const uint8_t* __restrict__ rec, int b,
+                                            Store store);
 
 // The grouped rows [begin, end) of one expert; the token of grouped row s is
 // sorted_pairs[s] / top_k.
@@ -88,16 +96,16 @@ __device__ __forceinline__ void gateup_block(GateUpShared& sh, int d, int f, int
                                              const int32_t* __restrict__ sorted_pairs, int begin,
                                              int end, const uint8_t* __restrict__ rec, int b,
                                              uint16_t* __restrict__ act) {
-  gateup_rows<kCo>(
-      sh, d, f, h, [&](int s) { return ld_i32<kCo>(sorted_pairs + s) / top_k; }, begin, end, rec,
-      b, act);
+  gateup_rows(
+      sh, d, f, [&](int s) { return h + (int64_t)(ld_i32<kCo>(sorted_pairs + s) / top_k) * d; },
+      begin, end, rec, b,
+      [&](int s, int n, uint32_t v) { st_u32<kCo>(act + (int64_t)s * f + n, v); });
 }
 
-template <bool kCo, typename TokenOf>
-__device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f,
-                                            const uint16_t* __restrict__ h, TokenOf token_of,
-                                            int begin, int end, const uint8_t* __restrict__ rec,
-                                            int b, uint16_t* __restrict__ act) {
+template <typename XRow, typename Store>
+__device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f, XRow x_row, int begin,
+                                            int end, const uint8_t* __restrict__ rec, int b,
+                                            Store store) {
   const int lane = lane_id();
   const int wi = threadIdx.x >> 6;
   const int G = d / kGroup;
@@ -106,32 +114,32 @@ __device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f,
   const uint8_t* up_codes = gate_codes + (int64_t)G * kTileBytes;
   const int n_local = lane & 15;
   const int quarter = lane >> 4;
-  const uint16_t* scales = reinterpret_cast<const uint16_t*>(rec + L.w13_scales);
-  const int gate_n = 32 * b + n_local, up_n = gate_n + 16;
+  // The gate and up rows of a lane (blocks 2b and 2b+1) have adjacent scales:
+  // one 32-bit word per group, gate in the low half.
+  const uint32_t* scales = reinterpret_cast<const uint32_t*>(rec + L.w13_scales);
+  const int gate_n = 32 * b + n_local;
 
   for (int m0 = begin; m0 < end; m0 += kTokChunk) {
     const int mc = min(kTokChunk, end - m0);
     const uint16_t* xrow[kTokChunk];
 #pragma unroll
-    for (int m = 0; m < kTokChunk; ++m) {
-      const int t = m < mc ? token_of(m0 + m) : 0;
-      xrow[m] = h + (int64_t)t * d + 8 * quarter;
-    }
+    for (int m = 0; m < kTokChunk; ++m) xrow[m] = x_row(m < mc ? m0 + m : m0) + 8 * quarter;
     float accg[kTokChunk], accu[kTokChunk];
 #pragma unroll
     for (int m = 0; m < kTokChunk; ++m) accg[m] = accu[m] = 0.f;
 
     for (int g0 = wi; g0 < G; g0 += kGemvWaves * kGateBatch) {
+      // The whole batch is loaded before any of it is used: scales stay raw
+      // fp16 bits until the arithmetic, so no load waits for another.
       uint4 cg[kGateBatch], cu[kGateBatch];
-      float sg[kGateBatch], su[kGateBatch];
+      uint32_t sgu[kGateBatch];
 #pragma unroll
       for (int j = 0; j < kGateBatch; ++j) {
         const int g = g0 + kGemvWaves * j;
         if (g < G) {
           cg[j] = *reinterpret_cast<const uint4*>(gate_codes + (int64_t)g * kTileBytes);
           cu[j] = *reinterpret_cast<const uint4*>(up_codes + (int64_t)g * kTileBytes);
-          sg[j] = half_bits_to_f32(scales[scale_index(gate_n, g, G)]);
-          su[j] = half_bits_to_f32(scales[scale_index(up_n, g, G)]);
+          sgu[j] = scales[scale_index(gate_n, g, G) >> 1];
         }
       }
 #pragma unroll
@@ -146,8 +154,8 @@ __device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f,
           float xs = 0.f;
           const float pg = lane_group_dot(cg[j], x, xs, true);
           const float pu = lane_group_dot(cu[j], x, xs, false);
-          accg[m] = fmaf(sg[j], fmaf(-136.f, xs, pg), accg[m]);
-          accu[m] = fmaf(su[j], fmaf(-136.f, xs, pu), accu[m]);
+          accg[m] = fmaf(half_bits_to_f32(sgu[j] & 0xffffu), fmaf(-136.f, xs, pg), accg[m]);
+          accu[m] = fmaf(half_bits_to_f32(sgu[j] >> 16), fmaf(-136.f, xs, pu), accu[m]);
         }
       }
     }
@@ -173,8 +181,7 @@ __device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f,
       }
       const uint32_t a16 = f32_to_bf16_rne(silu_mul(g, u));
       const uint32_t next = __shfl_down(a16, 1);
-      if (m < mc && (n_local & 1) == 0)
-        st_u32<kCo>(act + (int64_t)(m0 + m) * f + 16 * b + n_local, a16 | (next << 16));
+      if (m < mc && (n_local & 1) == 0) store(m0 + m, 16 * b + n_local, a16 | (next << 16));
     }
     __syncthreads();
   }
@@ -184,7 +191,7 @@ __device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f,
 // g0 .. g0+kDownBatch-1 (those < G).
 struct DownBatch {
   uint4 c[kDownBatch];
-  float s[kDownBatch];
+  uint16_t s[kDownBatch];  // raw fp16 scales: converted at use, so loads never wait on each other
 };
 
 __device__ __forceinline__ void down_load_batch(const uint8_t* __restrict__ rec, int d, int f,
@@ -199,7 +206,7 @@ __device__ __forceinline__ void down_load_batch(const uint8_t* __restrict__ rec,
   for (int j = 0; j < kDownBatch; ++j) {
     if (g0 + j < G) {
       bt.c[j] = *reinterpret_cast<const uint4*>(codes + (int64_t)(g0 + j) * kTileBytes);
-      bt.s[j] = half_bits_to_f32(sc[scale_index(n, g0 + j, G)]);
+      bt.s[j] = sc[scale_index(n, g0 + j, G)];
     }
   }
 }
@@ -223,7 +230,7 @@ __device__ __forceinline__ void down_apply_batch(const DownBatch& bt, int f, int
       for (int i = 0; i < 4; ++i) x[i] = xload(m, g * kGroup + 8 * quarter + 32 * i);
       float xs = 0.f;
       const float p = lane_group_dot(bt.c[j], x, xs, true);
-      acc[m] = fmaf(bt.s[j], fmaf(-136.f, xs, p), acc[m]);
+      acc[m] = fmaf(half_bits_to_f32(at_use(bt.s[j])), fmaf(-136.f, xs, p), acc[m]);
     }
   }
 }
@@ -261,7 +268,7 @@ __device__ __forceinline__ void down_apply_batch_xs(const DownBatch& bt, int f, 
       for (int i = 0; i < 4; ++i) x[i] = xload(m, g * kGroup + 8 * quarter + 32 * i);
       float unused = 0.f;
       const float p = lane_group_dot(bt.c[j], x, unused, false);
-      acc[m] = fmaf(bt.s[j], fmaf(-136.f, xsload(m, g), p), acc[m]);
+      acc[m] = fmaf(half_bits_to_f32(at_use(bt.s[j])), fmaf(-136.f, xsload(m, g), p), acc[m]);
     }
   }
 }

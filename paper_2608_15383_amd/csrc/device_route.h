@@ -127,8 +127,9 @@ struct TopkState {
 };
 
 // Selection from the logits already in st.v (lane l holds expert l + 64c in
-// register c).
-__device__ __forceinline__ void wave_topk_select_loaded(int n_experts, int top_k, TopkState& st) {
+// register c).  scratch: 64 words of LDS private to the wavefront, or null.
+__device__ __forceinline__ void wave_topk_select_loaded(int n_experts, int top_k, TopkState& st,
+                                                        uint64_t* scratch = nullptr) {
   const int lane = lane_id();
   const int nc = (n_experts + 63) / 64;  // logits per lane in use
   float* v = st.v;
@@ -142,6 +143,34 @@ __device__ __forceinline__ void wave_topk_select_loaded(int n_experts, int top_k
     key[c] = e < n_experts ? ((u & 0x80000000u) ? ~u : (u | 0x80000000u)) : 0u;
   }
   float zmax = 0.f;
+  if (nc == 1 && scratch) {
+    // At most 64 experts, one per lane, with LDS: every lane's rank is the
+    // number of larger keys.  The 64-bit key (order key, then 63 - lane, so
+    // the lower expert id wins a tie) is unique; every lane publishes its key,
+    // reads all 64 back (broadcast reads) and counts.  The selected lanes
+    // (rank < k) then drop (logit, expert) into slot rank, which lane j reads.
+    // Lanes past n_experts have order key 0 and rank below every expert.
+    const uint64_t mine = ((uint64_t)key[0] << 32) | (uint32_t)(63 - lane);
+    scratch[lane] = mine;
+    __builtin_amdgcn_wave_barrier();
+    int rank = 0;
+#pragma unroll
+    for (int j = 0; j < 64; j += 2) {
+      const uint64_t k0 = scratch[j], k1 = scratch[j + 1];
+      rank += (k0 > mine) + (k1 > mine);
+    }
+    __builtin_amdgcn_wave_barrier();
+    if (rank < top_k) scratch[rank] = ((uint64_t)__float_as_uint(v[0]) << 32) | (uint32_t)lane;
+    __builtin_amdgcn_wave_barrier();
+    if (lane < top_k) {
+      const uint64_t w = scratch[lane];
+      sel_id[0] = (int)(uint32_t)w;
+      sel_z[0] = __uint_as_float((uint32_t)(w >> 32));
+    }
+    st.zmax = __uint_as_float((uint32_t)(scratch[0] >> 32));
+    __builtin_amdgcn_wave_barrier();
+    return;
+  }
   if (nc == 1) {
     // At most 64 experts, one per lane.  Radix select of the k-th largest key
     // from the top bit down with ballots (lanes still tied on the bits seen
@@ -221,14 +250,15 @@ __device__ __forceinline__ void wave_topk_select_loaded(int n_experts, int top_k
 
 template <bool kCo>
 __device__ __forceinline__ void wave_topk_select(const float* __restrict__ z, int n_experts,
-                                                 int top_k, TopkState& st) {
+                                                 int top_k, TopkState& st,
+                                                 uint64_t* scratch = nullptr) {
   const int lane = lane_id();
 #pragma unroll
   for (int c = 0; c < kPerLane; ++c) {
     const int e = lane + 64 * c;
     st.v[c] = e < n_experts ? ld_f32<kCo>(z + e) : 0.f;
   }
-  wave_topk_select_loaded(n_experts, top_k, st);
+  wave_topk_select_loaded(n_experts, top_k, st, scratch);
 }
 
 template <bool kCoStore>
@@ -270,9 +300,9 @@ __device__ __forceinline__ void wave_topk_weights(const TopkState& st, int n_exp
 template <bool kCo, bool kCoStore = kCo>
 __device__ __forceinline__ void wave_topk(const float* __restrict__ z, int n_experts, int top_k,
                                           int renormalize, int32_t* __restrict__ ids_out,
-                                          float* __restrict__ w_out) {
+                                          float* __restrict__ w_out, uint64_t* scratch = nullptr) {
   TopkState st;
-  wave_topk_select<kCo>(z, n_experts, top_k, st);
+  wave_topk_select<kCo>(z, n_experts, top_k, st, scratch);
   wave_topk_store_ids<kCoStore>(st, top_k, ids_out);
   wave_topk_weights<kCoStore>(st, n_experts, top_k, renormalize, w_out);
 }

@@ -84,10 +84,12 @@ __global__ __launch_bounds__(256) void topk_kernel(int tokens, int n_experts, in
                                                    int renormalize, const float* __restrict__ logits,
                                                    int32_t* __restrict__ topk_ids,
                                                    float* __restrict__ topk_w) {
+  __shared__ uint64_t s_rank[4][64];  // per-wavefront top-k scratch
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= tokens) return;
   wave_topk<false>(logits + (int64_t)t * n_experts, n_experts, top_k, renormalize,
-            topk_ids + (int64_t)t * top_k, topk_w + (int64_t)t * top_k);
+                   topk_ids + (int64_t)t * top_k, topk_w + (int64_t)t * top_k,
+                   s_rank[threadIdx.x >> 6]);
 }
 
 constexpr int kGroupThreads = 1024;
