@@ -224,14 +224,12 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   if (wi < a.tokens)
     wave_topk_weights<false>(st, a.n_experts, a.top_k, a.renormalize, s_w + wi * a.top_k);
 
-  // Each wavefront stages its pairs' activation rows in LDS as the gate/up
-  // workgroups produce them, then computes their per-(group, quarter)
-  // activation sums and their expert outputs for this row block.  Wavefront
-  // wi owns pairs wi, wi+4, ...
   const uint16_t* act_lds = reinterpret_cast<const uint16_t*>(s_act);
-  wave_stage_act_rows(sy, a, wi, kGemvWaves, P, reinterpret_cast<uint32_t*>(s_act));
-  for (int pi = wi; pi < P; pi += kGemvWaves) {
-    for (int i = lane; i < G * 4; i += 64) {
+  uint32_t* act_lds32 = reinterpret_cast<uint32_t*>(s_act);
+  const int nw = a.f / 2;  // activation words per pair
+  // Per-(group, quarter) activation sums of pair pi, groups [g0, g1).
+  auto xs_sums = [&](int pi, int g0, int g1) {
+    for (int i = 4 * g0 + lane; i < 4 * g1; i += 64) {
       const int g = i >> 2, q = i & 3;
       uint4 x[4];
 #pragma unroll
@@ -239,9 +237,9 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
         x[k] = *reinterpret_cast<const uint4*>(act_lds + pi * a.f + g * kGroup + 8 * q + 32 * k);
       s_xs[pi * G * 4 + i] = lane_group_xsum(x);
     }
-  }
-  // Expert output of pair pi for this row block; `first` is its first batch
-  // of tiles (prefetched when has_first).
+  };
+  // Expert output of pair pi for this row block from its staged activation
+  // row; `first` is its first batch of tiles (prefetched when has_first).
   auto pair_output = [&](int pi, DownBatch first, bool has_first) {
     const uint8_t* rec = a.slot_bank + (int64_t)s_ids[pi] * a.record_bytes;
     auto xload = [&](int, int k) {
@@ -262,9 +260,25 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
       a.pair_out[(int64_t)pi * a.d + 16 * rb + lane] = o;
     }
   };
-  if (wi < P) pair_output(wi, pre0, true);
-  if (wi + kGemvWaves < P) pair_output(wi + kGemvWaves, pre1, true);
-  for (int pi = wi + 2 * kGemvWaves; pi < P; pi += kGemvWaves) pair_output(pi, pre0, false);
+  // Pair by pair as each activation row arrives (its first two pairs'
+  // tiles are prefetched), so computing one pair overlaps the wait for the
+  // next.
+  auto stage = [&](int pi) {
+    wave_stage_act_rows(sy, a, pi, kGemvWaves, pi + 1, act_lds32);
+    xs_sums(pi, 0, G);
+  };
+  if (wi < P) {
+    stage(wi);
+    pair_output(wi, pre0, true);
+  }
+  if (wi + kGemvWaves < P) {
+    stage(wi + kGemvWaves);
+    pair_output(wi + kGemvWaves, pre1, true);
+  }
+  for (int pi = wi + 2 * kGemvWaves; pi < P; pi += kGemvWaves) {
+    stage(pi);
+    pair_output(pi, pre0, false);
+  }
   __syncthreads();
   if (tid < 16 * a.tokens) {
     const int t = tid >> 4, n = tid & 15;
