@@ -1,7 +1,7 @@
 """Benchmark of the MI355X fused W4A16 routed-expert layer on one GPU.
 
-    python bench.py [--steps K] [--warmup W] [--workload decode|prefill|multiwave|stack]
-                    [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W]
+                    [--workload decode|prefill|multiwave|stack|copy] [--no-cpu-baseline]
 
 A step is one full layer call (route, group, grouped gate/up+SwiGLU, grouped
 down, combine) on OLMoE-shaped synthetic inputs (d_model 2048, d_ff 1024,
@@ -23,6 +23,9 @@ stack   : 16 layers x 64 experts (1024 packed records in one pinned host
           bank), a 16-slot cache per layer, 64 tokens per step, Zipf(1.1)
           expert popularity per layer (Gumbel top-8).  value = tokens/s over
           32 steps of 16 layer calls; H2D bytes and hit rates reported.
+copy    : calibration only (not a layer): a plain 1 GiB device-to-device copy of
+          known size, so hardware byte counters (FETCH_SIZE, WRITE_SIZE) read on
+          the layer kernels can be scaled to bytes.  value = copy GB/s.
 """
 from __future__ import annotations
 
@@ -41,6 +44,14 @@ METRIC = "fused W4A16 MoE layer: HBM GB/s + tokens/s (decode), TFLOP/s (prefill)
 D_MODEL, D_FF, N_EXPERTS, TOP_K = 2048, 1024, 64, 8
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_olmoe.md")
+# Source files each measured kernel is built from: a traffic figure read with
+# the hardware counters is reported only while these files are unchanged.
+KERNEL_SOURCES = {
+    "decode_fused": ["common.h", "decode.h", "decode.hip", "device_gemv.h", "device_route.h"],
+    "gateup_mfma": ["common.h", "gemm.hip"],
+    "down_mfma": ["common.h", "gemm.hip"],
+}
 
 
 def parse():
@@ -49,7 +60,7 @@ def parse():
     p.add_argument("--steps", type=int, default=None)
     p.add_argument("--warmup", type=int, default=None)
     p.add_argument("--workload", default="decode",
-                   choices=["decode", "prefill", "multiwave", "stack"])
+                   choices=["decode", "prefill", "multiwave", "stack", "copy"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
 
@@ -68,6 +79,30 @@ def w13_bytes():
 
 def w2_bytes():
     return D_MODEL * D_FF // 2 + D_MODEL * D_FF // 64
+
+
+def source_digest(kernel):
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2608_15383_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the FETCH_SIZE / WRITE_SIZE
+    passes recorded in profiles/hbm_traffic_olmoe.md (scaled by the copy
+    calibration there), or None when the kernel has no record or its sources
+    changed since the counters were read."""
+    if kernel not in KERNEL_SOURCES or not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            parts = line.split()
+            if len(parts) == 4 and parts[0] == "traffic" and parts[1] == kernel:
+                return int(parts[2]) if parts[3] == source_digest(kernel) else None
+    return None
 
 
 def make_bank(api, dm, torch, seed):
@@ -189,19 +224,21 @@ def bench_layer(args):
         k_bytes = n_distinct * w13_bytes() + T * D_MODEL * 2 + P * D_FF * 2
         k_flops = P * 2 * D_MODEL * 2 * D_FF
     elif dominant.startswith("down"):
-        k_bytes = n_distinct * w2_bytes() + P * D_FF * 2 + P * D_MODEL * 4
+        out_bytes = 2 if dominant.endswith("mfma") else 4  # bf16 / fp32 pair outputs
+        k_bytes = n_distinct * w2_bytes() + P * D_FF * 2 + P * D_MODEL * out_bytes
         k_flops = P * 2 * D_FF * D_MODEL
     else:
         k_bytes, k_flops = alg_bytes, flops
     if decode or "gemv" in dominant:
         ach = k_bytes / dur_s / 1e9
         roof = dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s", frac=ach / HBM_PEAK_GBS,
-                    traffic=None, kernel=dominant, alg_bytes_per_launch=k_bytes)
+                    traffic=measured_traffic(dominant), kernel=dominant,
+                    alg_bytes_per_launch=k_bytes)
     else:
         ach = k_flops / dur_s / 1e12
         roof = dict(bound="mfma", achieved=ach, peak=BF16_PEAK_TFLOPS, unit="TFLOP/s",
-                    frac=ach / BF16_PEAK_TFLOPS, traffic=None, kernel=dominant,
-                    alg_flops_per_launch=k_flops)
+                    frac=ach / BF16_PEAK_TFLOPS, traffic=measured_traffic(dominant), kernel=dominant,
+                    alg_flops_per_launch=k_flops, alg_bytes_per_launch=k_bytes)
 
     sec = ms * 1e-3
     if decode:
@@ -469,6 +506,31 @@ def bench_stack(args):
     print(json.dumps(out), flush=True)
 
 
+def bench_copy(args):
+    import torch
+
+    torch.cuda.init()
+    n = 1 << 29  # bf16 elements: 1 GiB read and 1 GiB written per copy
+    src = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    steps = args.steps or 5
+    for _ in range(args.warmup if args.warmup is not None else 1):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        dst.copy_(src)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    nbytes = 2 * n
+    print(json.dumps(dict(workload="copy", bytes_read_per_copy=nbytes, bytes_written_per_copy=nbytes,
+                          ms_per_copy=ms, value=2 * nbytes / (ms * 1e-3) / 1e9, unit="GB/s",
+                          steps=steps)), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -479,6 +541,8 @@ def main():
         bench_multiwave(args)
     elif args.workload == "stack":
         bench_stack(args)
+    elif args.workload == "copy":
+        bench_copy(args)
     else:
         bench_layer(args)
 
