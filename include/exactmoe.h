@@ -53,8 +53,8 @@ enum emoe_status {
  * pairs per expert, else the VALU weight-streaming GEMV.  The choice is made
  * once per call from (tokens, top_k, n_experts), so every wave of a call uses
  * the same arithmetic.  The MFMA path needs tokens*d_model*2 and
- * tokens*top_k*d_ff*2 below 2^31 bytes (AUTO takes the GEMV otherwise; an
- * explicit MFMA request fails with EMOE_ESHAPE). */
+ * tokens*top_k*d_ff*2 below 2^31 bytes and d_model, d_ff <= 8192 (AUTO takes
+ * the GEMV otherwise; an explicit MFMA request fails with EMOE_ESHAPE). */
 enum emoe_path { EMOE_PATH_AUTO = 0, EMOE_PATH_GEMV = 1, EMOE_PATH_MFMA = 2 };
 #define EMOE_MFMA_MIN_PAIRS_PER_EXPERT 32
 
@@ -94,12 +94,12 @@ typedef struct emoe_ws_layout {
   size_t act;           /* bf16  [T*k][d_ff]    phi(g)*u per pair, grouped order */
   size_t pair_out;      /* expert output per pair id, [T*k][d_model]: f32 on the GEMV
                            path, bf16 (in the first half of the field) on the MFMA path */
-  size_t x_bias;        /* f32   [d_model/128][T*k] -136 * group sums of each pair's token row
-                                                      of h, by grouped position (MFMA path) */
   size_t act_bias;      /* f32   [d_ff/128][T*k]    -136 * group sums of act, by grouped
                                                       position (MFMA path) */
   size_t chunk_counts;  /* i32   [ceil(T*k/64)][E]  pairs per expert in each 64-pair chunk
                                                       (grouping of large calls) */
+  size_t tok_bias;      /* f32   [T][d_model/128]   -136 * group sums of each token row of h
+                                                      (MFMA path) */
   size_t total;         /* bytes needed */
 } emoe_ws_layout;
 

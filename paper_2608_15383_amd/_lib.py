@@ -36,8 +36,8 @@ class Stats(C.Structure):
 class WsLayout(C.Structure):
     _fields_ = [(n, C.c_size_t) for n in ("logits", "topk_ids", "topk_w", "counts", "offsets",
                                           "sorted_pairs", "active", "n_active", "tile_offsets",
-                                          "pair_pos", "act", "pair_out", "x_bias", "act_bias",
-                                          "chunk_counts", "total")]
+                                          "pair_pos", "act", "pair_out", "act_bias",
+                                          "chunk_counts", "tok_bias", "total")]
 
 
 _vp = C.c_void_p

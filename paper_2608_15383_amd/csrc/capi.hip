@@ -145,9 +145,9 @@ emoe_ws_layout make_layout(const emoe_dims& d, int32_t T) {
   L.pair_pos = take(P * 4);
   L.act = take(P * (size_t)d.d_ff * 2);
   L.pair_out = take(P * (size_t)d.d_model * 4);
-  L.x_bias = take(P * (size_t)(d.d_model / EMOE_GROUP) * 4);
   L.act_bias = take(P * (size_t)(d.d_ff / EMOE_GROUP) * 4);
   L.chunk_counts = take((P + 63) / 64 * E * 4);
+  L.tok_bias = take((size_t)T * (d.d_model / EMOE_GROUP) * 4);
   L.total = off;
   return L;
 }
@@ -605,11 +605,13 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
   const int P = T * k;
   // The MFMA kernels address activations with 32-bit buffer offsets.
   const bool mfma_fits = (int64_t)P * f * 2 <= INT32_MAX && (int64_t)T * d * 2 <= INT32_MAX &&
-                         (int64_t)P * (d / EMOE_GROUP) * 4 <= INT32_MAX && c->record_bytes <= INT32_MAX;
+                         d / EMOE_GROUP <= kMfmaMaxGroups && f / EMOE_GROUP <= kMfmaMaxGroups &&
+                         c->record_bytes <= INT32_MAX;
   if (path == EMOE_PATH_AUTO)
     path = (P >= EMOE_MFMA_MIN_PAIRS_PER_EXPERT * E && mfma_fits) ? EMOE_PATH_MFMA : EMOE_PATH_GEMV;
   if (path == EMOE_PATH_MFMA && !mfma_fits)
-    return fail(EMOE_ESHAPE, "MFMA path: %d tokens exceed its 2 GiB activation addressing", T);
+    return fail(EMOE_ESHAPE, "MFMA path: %d tokens exceed its 2 GiB activation addressing, or "
+                             "d_model / d_ff exceed %d groups", T, kMfmaMaxGroups);
 
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   float* logits = reinterpret_cast<float*>(ws + L.logits);
@@ -623,7 +625,6 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
   int32_t* tiles = reinterpret_cast<int32_t*>(ws + L.tile_offsets);
   uint16_t* act = reinterpret_cast<uint16_t*>(ws + L.act);
   float* pair_out = reinterpret_cast<float*>(ws + L.pair_out);
-  float* x_bias = reinterpret_cast<float*>(ws + L.x_bias);
   float* act_bias = reinterpret_cast<float*>(ws + L.act_bias);
 
   int32_t* pair_pos = reinterpret_cast<int32_t*>(ws + L.pair_pos);
@@ -664,10 +665,17 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
     return EMOE_OK;
   }
 
-  // Route (Eq. 1) and group by expert.
+  // Route (Eq. 1) and group by expert.  On the MFMA path the router also sums
+  // each token row's input groups (the accumulator starts of the gate/up MFMA
+  // chains) when d is a multiple of 512; otherwise a separate pass forms them
+  // below.
   const float* z = logits_override ? logits_override : logits;
+  float* tok_bias = reinterpret_cast<float*>(ws + L.tok_bias);
+  const bool fused_bias = path == EMOE_PATH_MFMA && !logits_override && d % 512 == 0;
   if (!logits_override) {
-    EMOE_LAUNCH(EMOE_K_ROUTER, stream, launch_router_logits(T, E, d, h, w_router, logits, stream));
+    EMOE_LAUNCH(EMOE_K_ROUTER, stream,
+                launch_router_logits(T, E, d, h, w_router, logits, stream,
+                                     fused_bias ? tok_bias : nullptr));
     ds.kernel_launches += 1;
   }
   EMOE_LAUNCH(EMOE_K_TOPK, stream, launch_topk(T, E, k, renormalize, z, ids, wts, stream));
@@ -685,16 +693,16 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
     ds.kernel_launches += 2;
   }
   const GroupView gv{sorted, offsets, active, n_active, tiles};
-  if (path == EMOE_PATH_MFMA) {
+  if (path == EMOE_PATH_MFMA && !fused_bias) {
     // Accumulator start of the gate/up MFMA chains, once per call.
-    EMOE_LAUNCH(EMOE_K_ROW_BIAS, stream, launch_row_bias(T, d, k, h, pair_pos, x_bias, stream));
+    EMOE_LAUNCH(EMOE_K_ROW_BIAS, stream, launch_row_bias(T, d, h, tok_bias, stream));
     ds.kernel_launches += 1;
   }
 
   auto run_wave = [&](const WaveArg& wa) -> int32_t {
     if (path == EMOE_PATH_MFMA) {
       EMOE_LAUNCH(EMOE_K_GATEUP_MFMA, stream,
-                  launch_gateup_mfma(T, d, f, k, E, h, x_bias, gv, wa, c->slot_bank, c->record_bytes,
+                  launch_gateup_mfma(T, d, f, k, E, h, tok_bias, gv, wa, c->slot_bank, c->record_bytes,
                                      act, act_bias, stream));
       EMOE_LAUNCH(EMOE_K_DOWN_MFMA, stream,
                   launch_down_mfma(T, d, f, k, E, act, act_bias, gv, wa, c->slot_bank, c->record_bytes,

@@ -18,6 +18,7 @@ constexpr int kTileRows = 16;       // output rows per packed tile
 constexpr int kTileBytes = 1024;    // codes of one 16 x 128 tile (4 bits each)
 constexpr int kMaxWave = EMOE_MAX_EXPERTS;
 constexpr int kMfmaRows = 64;       // token rows per MFMA row-tile
+constexpr int kMfmaMaxGroups = 64;  // K / 128 of an MFMA projection (d, d_ff <= 8192)
 
 // ---------------------------------------------------------------------------
 // Packed expert record (our CDNA4 layout; the paper packs its own GPU's format
@@ -201,8 +202,11 @@ hipError_t launch_quantize(int d, int f, int n_experts, const uint16_t* w_gate,
                            const uint16_t* w_up, const uint16_t* w_down, uint8_t* records,
                            int32_t* range_flag, hipStream_t stream);
 
+// tok_bias (optional, d a multiple of 512): also -136 * the sum of each
+// 128-input group of every token row, fp32 [tokens][d/128].
 hipError_t launch_router_logits(int tokens, int n_experts, int d, const uint16_t* h,
-                                const uint16_t* w_router, float* logits, hipStream_t stream);
+                                const uint16_t* w_router, float* logits, hipStream_t stream,
+                                float* tok_bias = nullptr);
 
 hipError_t launch_topk(int tokens, int n_experts, int top_k, int renormalize, const float* logits,
                        int32_t* topk_ids, float* topk_w, hipStream_t stream);
@@ -242,13 +246,11 @@ hipError_t launch_down_gemv(int d, int f, int top_k, int pairs, int n_experts,
                             hipStream_t stream);
 
 // Grouped MFMA projections.  h_bias / act_bias: -136 * the sum of each
-// 128-input group of the projection's input row, fp32 [K/128][pairs] indexed
-// by grouped position (one contiguous run per group and row tile).  h_bias
-// comes from launch_row_bias (each token's sums go to the positions of its
-// top_k pairs, through pair_pos); act_bias is written by the gate/up launch
-// for the down launch.
-hipError_t launch_row_bias(int tokens, int K, int top_k, const uint16_t* x, const int32_t* pair_pos,
-                           float* bias, hipStream_t stream);
+// 128-input group of the projection's input rows: h_bias per token, fp32
+// [tokens][d/128] (from the router, or launch_row_bias); act_bias by grouped
+// position, fp32 [f/128][pairs], written by the gate/up launch for the down
+// launch.  Each workgroup gathers its row tile's values once.
+hipError_t launch_row_bias(int tokens, int K, const uint16_t* x, float* bias, hipStream_t stream);
 
 hipError_t launch_gateup_mfma(int tokens, int d, int f, int top_k, int n_experts, const uint16_t* h,
                               const float* h_bias, const GroupView& gv, const WaveArg& wave,

@@ -65,8 +65,10 @@ struct Shape {
 template <int kWaves>
 struct Stage {
   uint16_t a[kRows * kGroup];            // token rows of the group (swizzled chunks)
-  float bias[kWaves][kRows];             // -136 * row sums of the group (a copy per wavefront)
+  float spare[kWaves][kRows];            // room for the epilogue's padded output tile
 };
+
+constexpr int kMaxBiasGroups = kMfmaMaxGroups;
 
 // Stage S of the ring of a kWaves-wide workgroup (one LDS variable each).
 template <int kWaves, int S>
@@ -127,14 +129,16 @@ __device__ __forceinline__ float silu_fast(float x) {
   return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
-// kGateUp: x = h [tokens][d] gathered through the grouped pair ids, weights
-// W13, output act (bf16, grouped order) plus the bias table of act for the
-// down projection.  Otherwise: x = act [pairs][f] in grouped order, weights
-// W2, output pair_out (bf16, pair-id order).
+// kGateUp: x = h [tokens][d] gathered through the grouped pair ids, bias the
+// per-token table [tokens][d/128], weights W13, output act (bf16, grouped
+// order) plus the bias table of act for the down projection.  Otherwise:
+// x = act [pairs][f] in grouped order, bias act's table [f/128][pairs] by
+// grouped position, weights W2, output pair_out (bf16, pair-id order).
+// bias holds -136 * the sum of each 128-input group of each input row.
 template <bool kGateUp, typename Sh>
 __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_kernel(
     int d, int f, int top_k, int n_experts, const uint16_t* __restrict__ x, uint32_t x_bytes,
-    const float* __restrict__ x_bias, int pairs, GroupView gv, WaveArg wave,
+    const float* __restrict__ bias, int pairs, GroupView gv, WaveArg wave,
     const uint8_t* __restrict__ slot_bank, int64_t record_bytes, int n_ctiles,
     uint16_t* __restrict__ act_out, float* __restrict__ act_bias_out, uint16_t* __restrict__ pair_out) {
   constexpr int kWaves = Sh::kWaves;
@@ -150,6 +154,8 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   };
   StageT& st0 = stage_mem<kWaves, 0>();
   StageT& st1 = stage_mem<kWaves, 1>();
+  // The tile's bias, [group][row], gathered once in the prologue.
+  __shared__ __attribute__((aligned(16))) float bias_lds[kMaxBiasGroups][kRows];
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -195,7 +201,6 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   const int quarter = lane >> 4;
 
   const __amdgpu_buffer_rsrc_t x_rsrc = make_rsrc(x, x_bytes);
-  const __amdgpu_buffer_rsrc_t b_rsrc = make_rsrc(x_bias, (uint32_t)((int64_t)pairs * G * 4));
   const __amdgpu_buffer_rsrc_t w_rsrc = make_rsrc(rec, (uint32_t)record_bytes);
 
   // Source row of a tile row (rows past the tile's end repeat its last row;
@@ -214,9 +219,11 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
     const int c = (lane & 15) ^ (m & 15);
     a_off[j] = (uint32_t)src_row(m) * (uint32_t)(K * 2) + 16u * c;
   }
-  // Bias: [G][pairs] by grouped position, so a group's 64 row values are one
-  // contiguous run; every wavefront copies it (lane = row) for itself.
-  const uint32_t b_off = (uint32_t)(row0 + min(lane, rows - 1)) * 4u;
+  // Bias gather: thread t fills row t % 64 of every kWaves-th group from
+  // t / 64 on; its source row (a token for gate/up, a grouped position for
+  // down) is known now, so the gather overlaps the first group's loads.
+  const int b_row = tid & (kRows - 1);
+  const int b_src = src_row(b_row);
   const uint32_t w_off = (uint32_t)((kGateUp ? L.w13_codes : L.w2_codes) +
                                     (int64_t)rb0 * G * kTileBytes) + 16u * lane;
   // Scales of the wavefront's four row blocks for one group: 128 bytes, the
@@ -230,7 +237,7 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   uint4 wreg[kStages][kNPW];
 
   // Issue every load of group g into stage S (same count in every thread):
-  // token rows and bias into LDS, weight codes and scales into registers.
+  // token rows into LDS, weight codes and scales into registers.
   auto issue = [&](int g, auto stage) __attribute__((always_inline)) {
     StageT& sm = stage_of(stage);
 #pragma unroll
@@ -242,7 +249,6 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
                    g * kTileBytes, 0));
     sc[decltype(stage)::value] = __builtin_bit_cast(
         uint2, __builtin_amdgcn_raw_buffer_load_b64(w_rsrc, (int)s_off, g * 128, 0));
-    load_lds4(b_rsrc, &sm.bias[wi][0], b_off, (uint32_t)g * (uint32_t)pairs * 4u);
   };
 
   // Dequantization constants, hidden from constant folding (the empty asm
@@ -257,13 +263,13 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi) acc[r][mi] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  auto compute = [&](auto stage) __attribute__((always_inline)) {
+  auto compute = [&](int g, auto stage) __attribute__((always_inline)) {
     constexpr int S = decltype(stage)::value;
     const StageT& sm = stage_of(stage);
     f32x4_t c0[4];
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
-      c0[mi] = *reinterpret_cast<const f32x4_t*>(&sm.bias[wi][16 * mi + 4 * quarter]);
+      c0[mi] = *reinterpret_cast<const f32x4_t*>(&bias_lds[g][16 * mi + 4 * quarter]);
     uint4 wc[kNPW];
 #pragma unroll
     for (int r = 0; r < kNPW; ++r) wc[r] = wreg[S][r];
@@ -302,7 +308,7 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   auto step = [&](int g, auto stage, auto more) __attribute__((always_inline)) {
     constexpr int S = decltype(stage)::value;
     if constexpr (decltype(more)::value) issue(g + 1, std::integral_constant<int, S ^ 1>());
-    if (wvalid) compute(stage);
+    if (wvalid) compute(g, stage);
     wait_loads<0>();
     barrier();
   };
@@ -312,6 +318,9 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   using S1 = std::integral_constant<int, 1>;
 
   issue(0, S0());
+  // Gather the tile's bias while the first group loads.
+  for (int gg = wi; gg < G; gg += kWaves)
+    bias_lds[gg][b_row] = kGateUp ? bias[(int64_t)b_src * G + gg] : bias[(int64_t)gg * pairs + b_src];
   wait_loads<0>();
   barrier();
   // Groups 0 .. G-2 issue the next group; pairs of steps run in the loop.
@@ -409,17 +418,13 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   }
 }
 
-// For every token t and group g, -136 * sum of x[t][128g .. 128g+127] (fp32,
-// fixed order), stored at bias[g][pair_pos[t*top_k + j]] for j < top_k: the
-// accumulator start of the gate/up MFMA chains, by grouped position.
-__global__ __launch_bounds__(256) void row_bias_kernel(int tokens, int K, int top_k,
-                                                       const uint16_t* __restrict__ x,
-                                                       const int32_t* __restrict__ pair_pos,
+// bias[t][g] = -136 * sum of x[t][128g .. 128g+127] (fp32, fixed order): the
+// accumulator start of the gate/up MFMA chains of every pair of token t.
+__global__ __launch_bounds__(256) void row_bias_kernel(int tokens, int K, const uint16_t* __restrict__ x,
                                                        float* __restrict__ bias) {
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= tokens) return;
   const int lane = lane_id();
-  const int pairs = tokens * top_k;
   const uint16_t* xr = x + (int64_t)t * K;
   for (int c0 = 0; c0 < K / 8; c0 += 64) {
     const int c = c0 + lane;
@@ -438,14 +443,7 @@ __global__ __launch_bounds__(256) void row_bias_kernel(int tokens, int K, int to
     s += __shfl_xor(s, 2);
     s += __shfl_xor(s, 4);
     s += __shfl_xor(s, 8);
-    // Lanes 16u .. 16u+15 store group c0/16 + u at the positions of the
-    // token's pairs.
-    const int gl = lane >> 4;
-    const float sg = __shfl(s, 16 * gl);
-    const int g = c0 / kChunks + gl;
-    if (g < K / kGroup)
-      for (int j = lane & 15; j < top_k; j += 16)
-        bias[(int64_t)g * pairs + pair_pos[(int64_t)t * top_k + j]] = -kCodeBias * sg;
+    if ((lane & 15) == 0 && c < K / 8) bias[(int64_t)t * (K / kGroup) + c / kChunks] = -kCodeBias * s;
   }
 }
 
@@ -466,11 +464,9 @@ using MfmaShape = Shape<4>;
 
 }  // namespace
 
-hipError_t launch_row_bias(int tokens, int K, int top_k, const uint16_t* x, const int32_t* pair_pos,
-                           float* bias, hipStream_t stream) {
+hipError_t launch_row_bias(int tokens, int K, const uint16_t* x, float* bias, hipStream_t stream) {
   if (tokens == 0) return hipSuccess;
-  launch(row_bias_kernel, dim3((tokens + 3) / 4), dim3(256), stream, tokens, K, top_k, x, pair_pos,
-         bias);
+  launch(row_bias_kernel, dim3((tokens + 3) / 4), dim3(256), stream, tokens, K, x, bias);
   return hipGetLastError();
 }
 

@@ -25,7 +25,8 @@ typedef double f64x4_t __attribute__((ext_vector_type(4)));
 __global__ __launch_bounds__(256) void router_logits_kernel(int tokens, int n_experts, int d,
                                                             const uint16_t* __restrict__ h,
                                                             const uint16_t* __restrict__ wr,
-                                                            float* __restrict__ logits) {
+                                                            float* __restrict__ logits,
+                                                            float* __restrict__ tok_bias) {
   __shared__ double part[4][4][64];
   const int lane = lane_id();
   const int wave = threadIdx.x >> 6;
@@ -41,6 +42,10 @@ __global__ __launch_bounds__(256) void router_logits_kernel(int tokens, int n_ex
   // Loads run kAhead steps of 32 inputs ahead of the MFMAs.
   constexpr int kAhead = 4;
   const int n = kq / 32;
+  // With tok_bias (d a multiple of 512, so every iteration of the loop below
+  // is one 128-input group), the first expert tile's workgroups also sum each
+  // group of their token rows.
+  const bool sums = tok_bias != nullptr && blockIdx.y == 0;
   uint4 hb[kAhead], wb[kAhead];
 #pragma unroll
   for (int j = 0; j < kAhead; ++j) {
@@ -50,6 +55,7 @@ __global__ __launch_bounds__(256) void router_logits_kernel(int tokens, int n_ex
     }
   }
   for (int i = 0; i < n; i += kAhead) {
+    float gsum = 0.f;
 #pragma unroll
     for (int j = 0; j < kAhead; ++j) {
       if (i + j < n) {
@@ -62,7 +68,18 @@ __global__ __launch_bounds__(256) void router_logits_kernel(int tokens, int n_ex
         }
 #pragma unroll
         for (int s = 0; s < 8; ++s) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(hv[s], wv[s], acc, 0, 0, 0);
+        if (sums) {
+#pragma unroll
+          for (int s = 0; s < 8; ++s) gsum += (float)hv[s];
+        }
       }
+    }
+    if (sums) {
+      // The lane's 32 inputs of the group, then the four lanes of the row.
+      gsum += __shfl_xor(gsum, 16);
+      gsum += __shfl_xor(gsum, 32);
+      const int g = (wave * kq + 32 * i) / kGroup;
+      if (q == 0 && t0 + row < tokens) tok_bias[(int64_t)(t0 + row) * (d / kGroup) + g] = -136.f * gsum;
     }
   }
   // Lane l holds rows (tokens) l/16 + 4*r of column (expert) l%16 (the fp64
@@ -261,10 +278,13 @@ hipError_t launch_group_place(int pairs, int n_experts, const int32_t* topk_ids,
 }
 
 hipError_t launch_router_logits(int tokens, int n_experts, int d, const uint16_t* h,
-                                const uint16_t* w_router, float* logits, hipStream_t stream) {
+                                const uint16_t* w_router, float* logits, hipStream_t stream,
+                                float* tok_bias) {
   if (tokens == 0) return hipSuccess;
+  if (d % 512 != 0) tok_bias = nullptr;
   dim3 grid((tokens + 15) / 16, (n_experts + 15) / 16);
-  launch(router_logits_kernel, grid, dim3(256), stream, tokens, n_experts, d, h, w_router, logits);
+  launch(router_logits_kernel, grid, dim3(256), stream, tokens, n_experts, d, h, w_router, logits,
+         tok_bias);
   return hipGetLastError();
 }
 
