@@ -78,6 +78,45 @@ __device__ __forceinline__ void wave_stage_act_rows(DecodeSync* sy, const Decode
   }
 }
 
+// Token t's logits into st.v: from logits_override, or from the router
+// items' tagged words (replica `replica`), read until every word carries this
+// launch's epoch (bounded).
+__device__ __forceinline__ void load_logits(DecodeSync* sy, const DecodeArgs& a, int replica, int t,
+                                            TopkState& st) {
+  const int lane = lane_id();
+  const int E = a.n_experts;
+  if (a.logits_override) {
+#pragma unroll
+    for (int c = 0; c < kPerLane; ++c) {
+      const int e = lane + 64 * c;
+      st.v[c] = e < E ? a.logits_override[(int64_t)t * E + e] : 0.f;
+    }
+    return;
+  }
+  const uint64_t* zt = sy->logits[replica] + t * E;
+  uint32_t it = 0;
+  while (true) {
+    bool ok = true;
+#pragma unroll
+    for (int c = 0; c < kPerLane; ++c) {
+      const int e = lane + 64 * c;
+      if (e < E) {
+        const uint64_t x = __hip_atomic_load(zt + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ok = ok && (uint32_t)(x >> 32) == a.epoch;
+        st.v[c] = __uint_as_float((uint32_t)x);
+      } else {
+        st.v[c] = 0.f;
+      }
+    }
+    if (__all(ok)) break;
+    if (++it > kSpinLimit) {
+      if (lane == 0) atomicAdd(&sy->timeouts, 1u);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(kPollSleep);
+  }
+}
+
 // Copy `bytes` (a multiple of 256) from coherent global memory to LDS with
 // buffer loads that target LDS (one wavefront, 4 bytes per lane per load,
 // device-coherent: sc1).  Completion is this wavefront's vmcnt.
@@ -100,6 +139,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   __shared__ uint4 s_act[kFusedActLdsBytes / 16];
   __shared__ float s_xs[kFusedActLdsBytes / (2 * kGroup) * 4];  // [pair][group][quarter]
   __shared__ uint64_t s_topk[kFusedMaxTokens][64];                // top-k scratch per token
+  __shared__ int s_rank[kGemvWaves][64];                          // partial ranks (one token)
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -145,39 +185,33 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
                        reinterpret_cast<uint8_t*>(s_act) + off);
   }
 
-  // Every other workgroup: wavefront wi < T waits for token wi's logits (this
-  // launch's epoch in every tag) and selects its experts.
+  // Every other workgroup: token t's logits (this launch's epoch in every tag)
+  // and its selection.  One token: wavefront 0 loads the logits and publishes
+  // the rank keys, each wavefront counts, for every expert, the larger keys in
+  // its quarter of them, and wavefront 0 adds the counts.  Several tokens:
+  // wavefront t < T ranks token t alone.
   const int replica = blk % kSyncLanes;
   TopkState st;
-  if (wi < a.tokens) {
-    if (a.logits_override) {
-      wave_topk_select<false>(a.logits_override + (int64_t)wi * a.n_experts, a.n_experts, a.top_k,
-                              st, s_topk[wi]);
-    } else {
-      const uint64_t* zt = sy->logits[replica] + wi * a.n_experts;
-      uint32_t it = 0;
-      while (true) {
-        bool ok = true;
-#pragma unroll
-        for (int c = 0; c < kPerLane; ++c) {
-          const int e = lane + 64 * c;
-          if (e < a.n_experts) {
-            const uint64_t x = __hip_atomic_load(zt + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            ok = ok && (uint32_t)(x >> 32) == a.epoch;
-            st.v[c] = __uint_as_float((uint32_t)x);
-          } else {
-            st.v[c] = 0.f;
-          }
-        }
-        if (__all(ok)) break;
-        if (++it > kSpinLimit) {
-          if (lane == 0) atomicAdd(&sy->timeouts, 1u);
-          break;
-        }
-        __builtin_amdgcn_s_sleep(kPollSleep);
-      }
-      wave_topk_select_loaded(a.n_experts, a.top_k, st, s_topk[wi]);
+  if (a.tokens == 1 && a.n_experts <= 64) {
+    static_assert(kGemvWaves * 16 == 64, "a quarter of 64 keys per wavefront");
+    uint64_t* keys = s_topk[1];
+    if (wi == 0) {
+      load_logits(sy, a, replica, 0, st);
+      keys[lane] = topk_lane_key(st, a.n_experts);
     }
+    __syncthreads();
+    s_rank[wi][lane] = topk_count_greater<16>(keys + 16 * wi, keys[lane]);
+    __syncthreads();
+    if (wi == 0) {
+      int rank = 0;
+#pragma unroll
+      for (int w = 0; w < kGemvWaves; ++w) rank += s_rank[w][lane];
+      topk_select_ranked(rank, a.top_k, st, s_topk[0]);
+      wave_topk_store_ids<false>(st, a.top_k, s_ids);
+    }
+  } else if (wi < a.tokens) {
+    load_logits(sy, a, replica, wi, st);
+    wave_topk_select_loaded(a.n_experts, a.top_k, st, s_topk[wi]);
     wave_topk_store_ids<false>(st, a.top_k, s_ids + wi * a.top_k);
   }
   if (is_gate) wait_memory();  // the staged rows

@@ -126,6 +126,48 @@ struct TopkState {
   float zmax;
 };
 
+// At most 64 experts, one per lane: the lane's 64-bit rank key, the order key
+// of its logit above 63 - lane, so the key is unique and a larger logit, then
+// the lower expert id, compares greater.  Lanes past n_experts get order key
+// 0, below every expert.
+__device__ __forceinline__ uint64_t topk_lane_key(const TopkState& st, int n_experts) {
+  const int lane = lane_id();
+  const uint32_t u = __float_as_uint(st.v[0] + 0.0f);  // -0 -> +0
+  const uint32_t key = lane < n_experts ? ((u & 0x80000000u) ? ~u : (u | 0x80000000u)) : 0u;
+  return ((uint64_t)key << 32) | (uint32_t)(63 - lane);
+}
+
+// Number of keys[0 .. kN) (kN even) greater than mine: broadcast reads of the
+// published keys.
+template <int kN>
+__device__ __forceinline__ int topk_count_greater(const uint64_t* keys, uint64_t mine) {
+  int rank = 0;
+#pragma unroll
+  for (int j = 0; j < kN; j += 2) {
+    const uint64_t k0 = keys[j], k1 = keys[j + 1];
+    rank += (k0 > mine) + (k1 > mine);
+  }
+  return rank;
+}
+
+// At most 64 experts, one per lane, each lane knowing its rank among the keys
+// (0 = largest): the selected lanes (rank < k) drop (logit, expert) into slot
+// rank of the wavefront's 64 words of LDS scratch, which lane j reads.
+__device__ __forceinline__ void topk_select_ranked(int rank, int top_k, TopkState& st,
+                                                   uint64_t* scratch) {
+  const int lane = lane_id();
+  __builtin_amdgcn_wave_barrier();
+  if (rank < top_k) scratch[rank] = ((uint64_t)__float_as_uint(st.v[0]) << 32) | (uint32_t)lane;
+  __builtin_amdgcn_wave_barrier();
+  if (lane < top_k) {
+    const uint64_t w = scratch[lane];
+    st.sel_id[0] = (int)(uint32_t)w;
+    st.sel_z[0] = __uint_as_float((uint32_t)(w >> 32));
+  }
+  st.zmax = __uint_as_float((uint32_t)(scratch[0] >> 32));
+  __builtin_amdgcn_wave_barrier();
+}
+
 // Selection from the logits already in st.v (lane l holds expert l + 64c in
 // register c).  scratch: 64 words of LDS private to the wavefront, or null.
 __device__ __forceinline__ void wave_topk_select_loaded(int n_experts, int top_k, TopkState& st,
@@ -135,6 +177,16 @@ __device__ __forceinline__ void wave_topk_select_loaded(int n_experts, int top_k
   float* v = st.v;
   int* sel_id = st.sel_id;
   float* sel_z = st.sel_z;
+  if (nc == 1 && scratch) {
+    // At most 64 experts with LDS: every lane publishes its unique key, reads
+    // all 64 back and counts the larger ones, which is its rank.
+    const uint64_t mine = topk_lane_key(st, n_experts);
+    scratch[lane] = mine;
+    __builtin_amdgcn_wave_barrier();
+    const int rank = topk_count_greater<64>(scratch, mine);
+    topk_select_ranked(rank, top_k, st, scratch);
+    return;
+  }
   uint32_t key[kPerLane];  // 0 = not a candidate (keys of non-NaN floats are > 0)
 #pragma unroll
   for (int c = 0; c < kPerLane; ++c) {
@@ -143,34 +195,6 @@ __device__ __forceinline__ void wave_topk_select_loaded(int n_experts, int top_k
     key[c] = e < n_experts ? ((u & 0x80000000u) ? ~u : (u | 0x80000000u)) : 0u;
   }
   float zmax = 0.f;
-  if (nc == 1 && scratch) {
-    // At most 64 experts, one per lane, with LDS: every lane's rank is the
-    // number of larger keys.  The 64-bit key (order key, then 63 - lane, so
-    // the lower expert id wins a tie) is unique; every lane publishes its key,
-    // reads all 64 back (broadcast reads) and counts.  The selected lanes
-    // (rank < k) then drop (logit, expert) into slot rank, which lane j reads.
-    // Lanes past n_experts have order key 0 and rank below every expert.
-    const uint64_t mine = ((uint64_t)key[0] << 32) | (uint32_t)(63 - lane);
-    scratch[lane] = mine;
-    __builtin_amdgcn_wave_barrier();
-    int rank = 0;
-#pragma unroll
-    for (int j = 0; j < 64; j += 2) {
-      const uint64_t k0 = scratch[j], k1 = scratch[j + 1];
-      rank += (k0 > mine) + (k1 > mine);
-    }
-    __builtin_amdgcn_wave_barrier();
-    if (rank < top_k) scratch[rank] = ((uint64_t)__float_as_uint(v[0]) << 32) | (uint32_t)lane;
-    __builtin_amdgcn_wave_barrier();
-    if (lane < top_k) {
-      const uint64_t w = scratch[lane];
-      sel_id[0] = (int)(uint32_t)w;
-      sel_z[0] = __uint_as_float((uint32_t)(w >> 32));
-    }
-    st.zmax = __uint_as_float((uint32_t)(scratch[0] >> 32));
-    __builtin_amdgcn_wave_barrier();
-    return;
-  }
   if (nc == 1) {
     // At most 64 experts, one per lane.  Radix select of the k-th largest key
     // from the top bit down with ballots (lanes still tied on the bits seen

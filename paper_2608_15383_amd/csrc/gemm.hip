@@ -263,12 +263,15 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi) acc[r][mi] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  auto compute = [&](int g, auto stage) __attribute__((always_inline)) {
+  // kMB: row blocks holding tile rows (the last tile of an expert may fill
+  // fewer than 4; the blocks past its rows are skipped).
+  auto compute = [&](int g, auto stage, auto mb) __attribute__((always_inline)) {
     constexpr int S = decltype(stage)::value;
+    constexpr int kMB = decltype(mb)::value;
     const StageT& sm = stage_of(stage);
     f32x4_t c0[4];
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < kMB; ++mi)
       c0[mi] = *reinterpret_cast<const f32x4_t*>(&bias_lds[g][16 * mi + 4 * quarter]);
     uint4 wc[kNPW];
 #pragma unroll
@@ -278,7 +281,7 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
     for (int i = 0; i < 4; ++i) {
       bf16x8_t a[4];
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi) {
+      for (int mi = 0; mi < kMB; ++mi) {
         const int m = 16 * mi + n_local;
         a[mi] = *reinterpret_cast<const bf16x8_t*>(&sm.a[m * kGroup + 8 * ((4 * i + quarter) ^ n_local)]);
       }
@@ -287,7 +290,7 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
         const uint32_t dw = i == 0 ? wc[r].x : i == 1 ? wc[r].y : i == 2 ? wc[r].z : wc[r].w;
         const bf16x8_t b = dequant_b(dw, kMask, kMagic);
 #pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
+        for (int mi = 0; mi < kMB; ++mi)
           tmp[r][mi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], b, i == 0 ? c0[mi] : tmp[r][mi], 0, 0, 0);
       }
     }
@@ -296,7 +299,7 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
       const uint32_t sw = r < 2 ? sc[S].x : sc[S].y;
       const float s = half_bits_to_f32((r & 1) ? sw >> 16 : sw & 0xffffu);
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
+      for (int mi = 0; mi < kMB; ++mi)
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[r][mi][j] = fmaf(s, tmp[r][mi][j], acc[r][mi][j]);
     }
@@ -305,10 +308,10 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   // One group: load the next group into the other stage, compute this one,
   // then wait for the loads and hand the stages over.  Issuing is decided at
   // compile time so the wait counts stay exact.
-  auto step = [&](int g, auto stage, auto more) __attribute__((always_inline)) {
+  auto step = [&](int g, auto stage, auto more, auto mb) __attribute__((always_inline)) {
     constexpr int S = decltype(stage)::value;
     if constexpr (decltype(more)::value) issue(g + 1, std::integral_constant<int, S ^ 1>());
-    if (wvalid) compute(g, stage);
+    if (wvalid) compute(g, stage, mb);
     wait_loads<0>();
     barrier();
   };
@@ -324,17 +327,28 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   wait_loads<0>();
   barrier();
   // Groups 0 .. G-2 issue the next group; pairs of steps run in the loop.
-  int g = 0;
-  for (; g + 2 <= G - 1; g += 2) {
-    step(g, S0(), Yes());
-    step(g + 1, S1(), Yes());
-  }
-  if (G - 1 - g == 1) {
-    step(g, S0(), Yes());
-    step(g + 1, S1(), No());
-  } else {
-    step(g, S0(), No());
-  }
+  auto main_loop = [&](auto mb) __attribute__((always_inline)) {
+    int g = 0;
+    for (; g + 2 <= G - 1; g += 2) {
+      step(g, S0(), Yes(), mb);
+      step(g + 1, S1(), Yes(), mb);
+    }
+    if (G - 1 - g == 1) {
+      step(g, S0(), Yes(), mb);
+      step(g + 1, S1(), No(), mb);
+    } else {
+      step(g, S0(), No(), mb);
+    }
+  };
+  const int n_mb = (rows + 15) >> 4;
+  if (n_mb >= 4)
+    main_loop(std::integral_constant<int, 4>());
+  else if (n_mb == 3)
+    main_loop(std::integral_constant<int, 3>());
+  else if (n_mb == 2)
+    main_loop(std::integral_constant<int, 2>());
+  else
+    main_loop(std::integral_constant<int, 1>());
 
   // Epilogue.  Lane holds rows m = 16*mi + 4*quarter + j of output column
   // n_local of its row blocks.  Outputs are rounded to bf16, staged in LDS
