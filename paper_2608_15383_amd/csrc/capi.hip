@@ -573,6 +573,16 @@ int32_t emoe_fill_slots(emoe_cache* c, const int32_t* fill_expert, const int32_t
 // ------------------------------------------------------------------ forward
 namespace {
 
+// GEMV row chunks of a wave from the experts' row counts.
+void set_wave_chunks(WaveArg& wa, const int32_t* counts) {
+  int32_t acc = 0;
+  for (int i = 0; i < wa.n; ++i) {
+    wa.chunk0[i] = acc;
+    acc += (counts[wa.expert[i]] + kGemvRows - 1) / kGemvRows;
+  }
+  wa.chunk0[wa.n] = acc;
+}
+
 struct CacheSnapshot {
   std::vector<int32_t> slot_of, expert_of;
   std::vector<int64_t> stamp;
@@ -757,6 +767,7 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
       wa.n = n;
       for (int e = 0; e < E; ++e) wa.slot_of[e] = (int16_t)smap[e];
       for (int i = 0; i < n; ++i) wa.expert[i] = (int16_t)we[i];
+      set_wave_chunks(wa, c->counts_host);
       if (sequential) {
         for (int i = 0; i < n; ++i) {
           WaveArg one;
@@ -764,6 +775,7 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
           one.expert[0] = (int16_t)we[i];
           for (int e = 0; e < E; ++e) one.slot_of[e] = -1;
           one.slot_of[we[i]] = (int16_t)smap[we[i]];
+          set_wave_chunks(one, c->counts_host);
           if ((st = run_wave(one))) return st;
           ds.seq_expert_calls += 1;
         }

@@ -17,6 +17,7 @@ constexpr int kGroup = EMOE_GROUP;  // quantization group along K (Sec. 3.2)
 constexpr int kTileRows = 16;       // output rows per packed tile
 constexpr int kTileBytes = 1024;    // codes of one 16 x 128 tile (4 bits each)
 constexpr int kMaxWave = EMOE_MAX_EXPERTS;
+constexpr int kGemvRows = 8;  // activation rows of one expert per GEMV workgroup
 constexpr int kMfmaRows = 64;       // token rows per MFMA row-tile
 constexpr int kMfmaMaxGroups = 64;  // K / 128 of an MFMA projection (d, d_ff <= 8192)
 
@@ -77,6 +78,9 @@ struct WaveArg {
   int32_t n;
   int16_t expert[kMaxWave];
   int16_t slot_of[kMaxWave];
+  // GEMV row chunks (kGemvRows rows of one expert each): chunk0[i] = chunks
+  // of wave positions before i, chunk0[n] = all (n >= 0 only).
+  int32_t chunk0[kMaxWave + 1];
 };
 
 // Device-side views used by the grouped projection kernels.
@@ -162,17 +166,64 @@ __device__ __forceinline__ void wait_memory() {
 }
 
 // Resolve the wave-local expert index w to (expert, slot); false if unused.
-__device__ __forceinline__ bool resolve_wave_expert(const WaveArg& wave, const GroupView& gv,
-                                                    int w, int& expert, int& slot) {
-  if (wave.n < 0) {
-    if (w >= *gv.n_active) return false;
-    expert = gv.active[w];
-    slot = expert;
-  } else {
-    if (w >= wave.n) return false;
-    expert = wave.expert[w];
+// Workgroup y's chunk of an expert's grouped rows for the GEMV kernels: the
+// wave's experts in order (wave.expert, or the active list when n < 0), each
+// split into ceil(rows / kGemvRows) chunks of consecutive rows [begin, end).
+// False past the last chunk.  Every lane returns the same.
+__device__ __forceinline__ bool resolve_wave_chunk(const WaveArg& wave, const GroupView& gv, int y,
+                                                   int& expert, int& slot, int& begin, int& end) {
+  int c;
+  if (wave.n >= 0) {
+    if (y >= wave.chunk0[wave.n]) return false;
+    int lo = 0, hi = wave.n;  // chunk0[lo] <= y < chunk0[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (wave.chunk0[mid] <= y) lo = mid; else hi = mid;
+    }
+    expert = wave.expert[lo];
     slot = wave.slot_of[expert];
+    c = y - wave.chunk0[lo];
+  } else {
+    // Every active expert; lane l takes list positions 4l .. 4l+3.
+    const int n = *gv.n_active;
+    const int lane = lane_id();
+    int cnt[4], local = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int w = 4 * lane + i;
+      cnt[i] = 0;
+      if (w < n) {
+        const int e = gv.active[w];
+        cnt[i] = (gv.offsets[e + 1] - gv.offsets[e] + kGemvRows - 1) / kGemvRows;
+      }
+      local += cnt[i];
+    }
+    int incl = local;
+#pragma unroll
+    for (int dl = 1; dl < 64; dl <<= 1) {
+      const int t = __shfl_up(incl, dl);
+      if (lane >= dl) incl += t;
+    }
+    const int start = incl - local;
+    const uint64_t hit = __ballot(y >= start && y < incl);
+    if (hit == 0) return false;
+    const int src = (int)__builtin_ctzll(hit);
+    // Position within the source lane's four.
+    int i = 0, at = start;
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+      if (i == k && y >= at + cnt[k]) {
+        at += cnt[k];
+        i = k + 1;
+      }
+    i = __builtin_amdgcn_readlane(i, src);
+    at = __builtin_amdgcn_readlane(at, src);
+    expert = gv.active[4 * src + i];
+    slot = expert;
+    c = y - at;
   }
+  begin = gv.offsets[expert] + c * kGemvRows;
+  end = min(begin + kGemvRows, gv.offsets[expert + 1]);
   return true;
 }
 
@@ -230,9 +281,11 @@ hipError_t launch_group_place(int pairs, int n_experts, const int32_t* topk_ids,
 constexpr int kGroupWideMinPairs = 1024;  // smaller calls group in one workgroup
 
 // Number of wave-local expert indices a grouped launch must cover.
-inline int grid_experts(const WaveArg& wave, int n_experts, int pairs) {
-  if (wave.n >= 0) return wave.n;
-  return pairs < n_experts ? pairs : n_experts;
+// GEMV row chunks to launch: exact for a wave, else a bound (each active
+// expert adds at most one partial chunk).
+inline int grid_chunks(const WaveArg& wave, int n_experts, int pairs) {
+  if (wave.n >= 0) return wave.chunk0[wave.n];
+  return (pairs + kGemvRows - 1) / kGemvRows + (pairs < n_experts ? pairs : n_experts);
 }
 
 hipError_t launch_gateup_gemv(int d, int f, int top_k, int pairs, int n_experts,

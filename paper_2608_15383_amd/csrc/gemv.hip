@@ -11,8 +11,10 @@
 namespace emoe {
 namespace {
 
-// Workgroup = (gate/up row-block pair b, wave expert w).  Output: the SwiGLU
-// activation phi(g) * u as bf16 at each pair's grouped position.
+// Workgroup = (gate/up row-block pair b, row chunk y: up to kGemvRows rows of
+// one wave expert, so an expert with many rows spreads over many
+// workgroups).  Output: the SwiGLU activation phi(g) * u as bf16 at each
+// pair's grouped position.
 __global__ __launch_bounds__(256) void gateup_gemv_kernel(int d, int f, int top_k,
                                                           const uint16_t* __restrict__ h,
                                                           GroupView gv, WaveArg wave,
@@ -20,14 +22,13 @@ __global__ __launch_bounds__(256) void gateup_gemv_kernel(int d, int f, int top_
                                                           int64_t record_bytes,
                                                           uint16_t* __restrict__ act) {
   __shared__ GateUpShared sh;
-  int expert, slot;
-  if (!resolve_wave_expert(wave, gv, blockIdx.y, expert, slot)) return;
-  gateup_block<false>(sh, d, f, top_k, h, gv.sorted_pairs, gv.offsets[expert],
-                      gv.offsets[expert + 1], slot_bank + (int64_t)slot * record_bytes, blockIdx.x,
-                      act);
+  int expert, slot, begin, end;
+  if (!resolve_wave_chunk(wave, gv, blockIdx.y, expert, slot, begin, end)) return;
+  gateup_block<false>(sh, d, f, top_k, h, gv.sorted_pairs, begin, end,
+                      slot_bank + (int64_t)slot * record_bytes, blockIdx.x, act);
 }
 
-// Workgroup = (four 16-row blocks of the output, wave expert w); each
+// Workgroup = (four 16-row blocks of the output, row chunk y as above); each
 // wavefront owns one row block over the whole input (d_ff).  Output: fp32
 // expert output per pair id.
 __global__ __launch_bounds__(256) void down_gemv_kernel(int d, int f, int top_k,
@@ -38,10 +39,8 @@ __global__ __launch_bounds__(256) void down_gemv_kernel(int d, int f, int top_k,
                                                         float* __restrict__ pair_out) {
   (void)top_k;
   const int lane = lane_id();
-  int expert, slot;
-  if (!resolve_wave_expert(wave, gv, blockIdx.y, expert, slot)) return;
-  const int begin = gv.offsets[expert];
-  const int end = gv.offsets[expert + 1];
+  int expert, slot, begin, end;
+  if (!resolve_wave_chunk(wave, gv, blockIdx.y, expert, slot, begin, end)) return;
   const int G = f / kGroup;
   const int rb = blockIdx.x * kGemvWaves + (threadIdx.x >> 6);
   const uint8_t* rec = slot_bank + (int64_t)slot * record_bytes;
@@ -110,9 +109,9 @@ hipError_t launch_gateup_gemv(int d, int f, int top_k, int pairs, int n_experts,
                               const uint16_t* h, const GroupView& gv, const WaveArg& wave,
                               const uint8_t* slot_bank, int64_t record_bytes, uint16_t* act,
                               hipStream_t stream) {
-  const int ge = grid_experts(wave, n_experts, pairs);
-  if (ge == 0) return hipSuccess;
-  launch(gateup_gemv_kernel, dim3(f / kTileRows, ge), dim3(64 * kGemvWaves), stream, d, f, top_k,
+  const int gc = grid_chunks(wave, n_experts, pairs);
+  if (gc == 0) return hipSuccess;
+  launch(gateup_gemv_kernel, dim3(f / kTileRows, gc), dim3(64 * kGemvWaves), stream, d, f, top_k,
          h, gv, wave, slot_bank, record_bytes, act);
   return hipGetLastError();
 }
@@ -121,9 +120,9 @@ hipError_t launch_down_gemv(int d, int f, int top_k, int pairs, int n_experts,
                             const uint16_t* act, const GroupView& gv, const WaveArg& wave,
                             const uint8_t* slot_bank, int64_t record_bytes, float* pair_out,
                             hipStream_t stream) {
-  const int ge = grid_experts(wave, n_experts, pairs);
-  if (ge == 0) return hipSuccess;
-  launch(down_gemv_kernel, dim3(d / (kTileRows * kGemvWaves), ge), dim3(64 * kGemvWaves), stream,
+  const int gc = grid_chunks(wave, n_experts, pairs);
+  if (gc == 0) return hipSuccess;
+  launch(down_gemv_kernel, dim3(d / (kTileRows * kGemvWaves), gc), dim3(64 * kGemvWaves), stream,
          d, f, top_k, act, gv, wave, slot_bank, record_bytes, pair_out);
   return hipGetLastError();
 }
