@@ -175,8 +175,8 @@ int32_t emoe_route(const emoe_dims* dims, int32_t tokens, const uint16_t* h,
  * With both NULL the cache only plans (emoe_plan_waves / emoe_build_slot_map).
  * With a slot bank and C = E, emoe_cache_preload_all makes every expert
  * resident (its record already in slot e, or copied from the host bank).
- * With a slot bank and C < E a host bank is required; the cache creates one
- * copy stream (default priority) and one completion event per slot. */
+ * With a slot bank and C < E a host bank is required; the cache creates two
+ * copy streams (default priority) and one completion event per slot. */
 int32_t emoe_cache_create(const emoe_dims* dims, int32_t capacity, void* slot_bank,
                           const void* host_bank, emoe_cache** out);
 int32_t emoe_cache_destroy(emoe_cache* cache);
@@ -214,9 +214,9 @@ int32_t emoe_build_slot_map(emoe_cache* cache, const int32_t* wave_experts, int3
                             int32_t* n_fill, emoe_stats* stats);
 
 /* Host-bank slot fill (Sec. 3.3): copy each listed record from the pinned host
- * bank to its slot with hipMemcpyAsync on the cache's copy stream, each copy
- * first waiting for the slot's completion event; `stream` is then made to
- * wait for the copies.  No host synchronization. */
+ * bank to its slot with hipMemcpyAsync, alternating between the cache's two
+ * copy streams, each copy first waiting for the slot's completion event;
+ * `stream` is then made to wait for the copies.  No host synchronization. */
 int32_t emoe_fill_slots(emoe_cache* cache, const int32_t* fill_expert, const int32_t* fill_slot,
                         int32_t n_fill, hipStream_t stream);
 

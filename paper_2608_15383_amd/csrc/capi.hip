@@ -102,9 +102,13 @@ struct emoe_cache {
   std::vector<int64_t> stamp;       // [C]
   int64_t clock = 0;
   int device = -1;
-  hipStream_t copy_stream = nullptr;
-  std::vector<hipEvent_t> release;  // [C] completion of the last wave using the slot
-  hipEvent_t ready = nullptr;       // completion of the last batch of fills
+  // Fills alternate between two copy streams: one stream leaves a gap between
+  // consecutive record copies that the other fills (pinned H2D of 46 records
+  // of 3.24 MB: about 45 GB/s on one stream, 56 GB/s on two).
+  static constexpr int kCopyStreams = 2;
+  hipStream_t copy_stream[kCopyStreams] = {};
+  std::vector<hipEvent_t> release;           // [C] completion of the last wave using the slot
+  hipEvent_t ready[kCopyStreams] = {};       // completion of each stream's last fills
   int32_t* counts_host = nullptr;   // pinned [E]: the batched expert-id transfer
   DecodeSync* sync = nullptr;       // device: hand-over data of the fused decode launches
   DecodeProgress prog;              // host: epoch of the last fused launch
@@ -406,8 +410,10 @@ int32_t emoe_cache_create(const emoe_dims* dims, int32_t capacity, void* slot_ba
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&c->sync), sizeof(DecodeSync));
     if (e == hipSuccess) e = hipMemset(c->sync, 0, sizeof(DecodeSync));
     if (e == hipSuccess && host_bank) {
-      e = hipStreamCreateWithFlags(&c->copy_stream, hipStreamNonBlocking);
-      if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ready, hipEventDisableTiming);
+      for (int j = 0; j < emoe_cache::kCopyStreams && e == hipSuccess; ++j) {
+        e = hipStreamCreateWithFlags(&c->copy_stream[j], hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ready[j], hipEventDisableTiming);
+      }
       c->release.assign(capacity, nullptr);
       for (int s = 0; s < capacity && e == hipSuccess; ++s)
         e = hipEventCreateWithFlags(&c->release[s], hipEventDisableTiming);
@@ -423,11 +429,14 @@ int32_t emoe_cache_create(const emoe_dims* dims, int32_t capacity, void* slot_ba
 
 int32_t emoe_cache_destroy(emoe_cache* c) {
   if (!c) return EMOE_OK;
-  if (c->copy_stream) (void)hipStreamSynchronize(c->copy_stream);
+  for (hipStream_t cs : c->copy_stream)
+    if (cs) (void)hipStreamSynchronize(cs);
   for (hipEvent_t ev : c->release)
     if (ev) (void)hipEventDestroy(ev);
-  if (c->ready) (void)hipEventDestroy(c->ready);
-  if (c->copy_stream) (void)hipStreamDestroy(c->copy_stream);
+  for (int j = 0; j < emoe_cache::kCopyStreams; ++j) {
+    if (c->ready[j]) (void)hipEventDestroy(c->ready[j]);
+    if (c->copy_stream[j]) (void)hipStreamDestroy(c->copy_stream[j]);
+  }
   if (c->counts_host) (void)hipHostFree(c->counts_host);
   if (c->sync) (void)hipFree(c->sync);
   delete c;
@@ -549,7 +558,7 @@ int32_t emoe_fill_slots(emoe_cache* c, const int32_t* fill_expert, const int32_t
   if (!c) return fail(EMOE_EINVAL, "cache is NULL");
   if (n_fill == 0) return EMOE_OK;
   if (n_fill < 0 || !fill_expert || !fill_slot) return fail(EMOE_EINVAL, "bad fill list");
-  if (!c->slot_bank || !c->host_bank || !c->copy_stream)
+  if (!c->slot_bank || !c->host_bank || !c->copy_stream[0])
     return fail(EMOE_ESTATE, "cache has no slot bank / host bank");
   for (int i = 0; i < n_fill; ++i) {
     const int e = fill_expert[i], s = fill_slot[i];
@@ -558,13 +567,16 @@ int32_t emoe_fill_slots(emoe_cache* c, const int32_t* fill_expert, const int32_t
   }
   for (int i = 0; i < n_fill; ++i) {
     const int e = fill_expert[i], s = fill_slot[i];
-    EMOE_HIP(hipStreamWaitEvent(c->copy_stream, c->release[s], 0));
+    hipStream_t cs = c->copy_stream[i % emoe_cache::kCopyStreams];
+    EMOE_HIP(hipStreamWaitEvent(cs, c->release[s], 0));
     EMOE_HIP(hipMemcpyAsync(c->slot_bank + (int64_t)s * c->record_bytes,
                             c->host_bank + (int64_t)e * c->record_bytes, c->record_bytes,
-                            hipMemcpyHostToDevice, c->copy_stream));
+                            hipMemcpyHostToDevice, cs));
   }
-  EMOE_HIP(hipEventRecord(c->ready, c->copy_stream));
-  EMOE_HIP(hipStreamWaitEvent(stream, c->ready, 0));
+  for (int j = 0; j < emoe_cache::kCopyStreams && j < n_fill; ++j) {
+    EMOE_HIP(hipEventRecord(c->ready[j], c->copy_stream[j]));
+    EMOE_HIP(hipStreamWaitEvent(stream, c->ready[j], 0));
+  }
   return EMOE_OK;
 }
 
