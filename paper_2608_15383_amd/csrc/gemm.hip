@@ -156,6 +156,8 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   StageT& st1 = stage_mem<kWaves, 1>();
   // The tile's bias, [group][row], gathered once in the prologue.
   __shared__ __attribute__((aligned(16))) float bias_lds[kMaxBiasGroups][kRows];
+  // Down: the pair id of each tile row, read in the prologue for the epilogue.
+  __shared__ int pair_lds[kRows];
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -324,6 +326,7 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   // Gather the tile's bias while the first group loads.
   for (int gg = wi; gg < G; gg += kWaves)
     bias_lds[gg][b_row] = kGateUp ? bias[(int64_t)b_src * G + gg] : bias[(int64_t)gg * pairs + b_src];
+  if (!kGateUp && tid < kRows) pair_lds[tid] = gv.sorted_pairs[b_src];
   wait_loads<0>();
   barrier();
   // Groups 0 .. G-2 issue the next group; pairs of steps run in the loop.
@@ -425,7 +428,7 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
       const uint16_t* t = m < 32 ? half0 : half1;
       if (m < rows && col < d) {
         const uint4 v = *reinterpret_cast<const uint4*>(&t[(m & 31) * kStride + 8 * cc]);
-        const int pi = gv.sorted_pairs[row0 + m];
+        const int pi = pair_lds[m];
         *reinterpret_cast<uint4*>(pair_out + (int64_t)pi * d + col) = v;
       }
     }
