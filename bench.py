@@ -1,7 +1,7 @@
 """Benchmark of the MI355X fused W4A16 routed-expert layer on one GPU.
 
     python bench.py [--steps K] [--warmup W]
-                    [--workload decode|prefill|multiwave|stack|copy] [--no-cpu-baseline]
+                    [--workload decode|prefill|multiwave|stack|frontier|copy] [--no-cpu-baseline]
 
 A step is one full layer call (route, group, grouped gate/up+SwiGLU, grouped
 down, combine) on OLMoE-shaped synthetic inputs (d_model 2048, d_ff 1024,
@@ -23,6 +23,10 @@ stack   : 16 layers x 64 experts (1024 packed records in one pinned host
           bank), a 16-slot cache per layer, 64 tokens per step, Zipf(1.1)
           expert popularity per layer (Gumbel top-8).  value = tokens/s over
           32 steps of 16 layer calls; H2D bytes and hit rates reported.
+frontier: the stack's capacity and batch frontier: C in {8, 16, 32, 64} slots
+          per layer and T in {1, 2, 4, 8} tokens per step (C = 64: every
+          expert resident).  Tokens/s, hit rate and H2D bytes per token for
+          each point; value = tokens/s at C = 16, T = 1.
 copy    : calibration only (not a layer): a plain 1 GiB device-to-device copy of
           known size, so hardware byte counters (FETCH_SIZE, WRITE_SIZE) read on
           the layer kernels can be scaled to bytes.  value = copy GB/s.
@@ -60,7 +64,7 @@ def parse():
     p.add_argument("--steps", type=int, default=None)
     p.add_argument("--warmup", type=int, default=None)
     p.add_argument("--workload", default="decode",
-                   choices=["decode", "prefill", "multiwave", "stack", "copy"])
+                   choices=["decode", "prefill", "multiwave", "stack", "frontier", "copy"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     return p.parse_args()
 
@@ -506,6 +510,83 @@ def bench_stack(args):
     print(json.dumps(out), flush=True)
 
 
+def bench_frontier(args):
+    """Capacity and batch frontier of the 16-layer stack: C in {8, 16, 32, 64}
+    slots per layer, T in {1, 2, 4, 8} tokens per step, Zipf(1.1) routing."""
+    import torch
+    from paper_2608_15383_amd import api
+    from paper_2608_15383_amd.inputs import zipf_gumbel_logits
+
+    torch.cuda.init()
+    dm = api.dims(D_MODEL, D_FF, N_EXPERTS, TOP_K)
+    L = 16
+    steps = args.steps or 6
+    warmup = args.warmup if args.warmup is not None else 2
+    rec = api.expert_record_bytes(dm)
+    log("frontier: quantizing 16 x 64 experts into the pinned host bank")
+    host, weights = quantized_host_bank(api, dm, torch, [2000 + l for l in range(L)])
+    del weights
+    torch.cuda.empty_cache()
+    rng = np.random.default_rng(4)
+    perms = [rng.permutation(N_EXPERTS) for _ in range(L)]
+    gen = torch.Generator(device="cuda").manual_seed(9)
+    rows = []
+    for C in (8, 16, 32, 64):
+        banks = [torch.zeros(C * rec, dtype=torch.uint8, device="cuda") for _ in range(L)]
+        caches = []
+        for l in range(L):
+            c = api.Cache(dm, C, slot_bank=banks[l],
+                          host_bank=host[l * N_EXPERTS * rec:(l + 1) * N_EXPERTS * rec])
+            if C == N_EXPERTS:
+                c.preload_all()
+            caches.append(c)
+        for T in (1, 2, 4, 8):
+            n_steps = warmup + steps
+            z = torch.from_numpy(np.stack([np.stack([zipf_gumbel_logits(T, N_EXPERTS, 1.1, perms[l], rng)
+                                                     for l in range(L)]) for _ in range(n_steps)])
+                                 .astype(np.float32)).to("cuda")
+            h = torch.randn((T, D_MODEL), dtype=torch.bfloat16, device="cuda", generator=gen)
+            y = torch.empty_like(h)
+            ws = torch.empty(api.workspace_bytes(dm, T), dtype=torch.uint8, device="cuda")
+
+            def step(si, st):
+                for l in range(L):
+                    api.moe_forward(caches[l], h, None, y, ws, logits_override=z[si, l], stats=st)
+
+            for si in range(warmup):
+                step(si, api.Stats())
+            torch.cuda.synchronize()
+            st = api.Stats()
+            t0 = time.perf_counter()
+            for si in range(warmup, n_steps):
+                step(si, st)
+            torch.cuda.synchronize()
+            sec = time.perf_counter() - t0
+            tot = st.hits + st.misses
+            row = dict(slots=C, tokens=T, tokens_per_s=T * steps / sec, ms_per_step=1e3 * sec / steps,
+                       hit_rate=(st.hits / tot) if tot else 1.0,
+                       h2d_mb_per_token=st.h2d_bytes / (T * steps) / 1e6,
+                       h2d_gbs=st.h2d_bytes / sec / 1e9, waves_per_layer_call=st.waves / (steps * L),
+                       slot_gib=L * C * rec / 2 ** 30)
+            rows.append(row)
+            log(f"C={C:2d} T={T}: {row['tokens_per_s']:8.1f} tokens/s, hit rate {row['hit_rate']:.2f}, "
+                f"H2D {row['h2d_mb_per_token']:.1f} MB/token, {row['h2d_gbs']:.1f} GB/s")
+        for c in caches:
+            c.close()
+        del caches, banks
+        torch.cuda.empty_cache()
+    head = next(r for r in rows if r["slots"] == 16 and r["tokens"] == 1)
+    out = dict(metric=METRIC, value=head["tokens_per_s"], unit="tokens/s", n_gpus=1, steps=steps,
+               warmup=warmup, ms_per_step=head["ms_per_step"], higher_is_better=True,
+               scaling="weak", vs_baseline=None, dtype="bf16", data="synthetic",
+               config=dict(workload="olmoe_stack16_zipf1.1_frontier", layers=L, d_model=D_MODEL,
+                           d_ff=D_FF, n_experts=N_EXPERTS, top_k=TOP_K, group=128,
+                           value_at=dict(slots=16, tokens=1),
+                           weights="int4 group-128, fp16 scales"),
+               frontier=rows)
+    print(json.dumps(out), flush=True)
+
+
 def bench_copy(args):
     import torch
 
@@ -543,6 +624,8 @@ def main():
         bench_stack(args)
     elif args.workload == "copy":
         bench_copy(args)
+    elif args.workload == "frontier":
+        bench_frontier(args)
     else:
         bench_layer(args)
 
