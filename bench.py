@@ -258,6 +258,10 @@ def bench_layer(args):
                            rotated_banks=n_banks),
                tokens_per_s=T / sec, alg_bytes_per_step=alg_bytes, flops_per_step=flops,
                roofline=roof, kernels=kern)
+    if decode:
+        # The same bytes against what a plain device copy achieves on this GPU.
+        cp = device_copy_gbs(torch)
+        out["device_copy"] = dict(gbs=cp, layer_frac=value / cp, kernel_frac=roof["achieved"] / cp)
 
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
@@ -294,6 +298,22 @@ def quantized_host_bank(api, dm, torch, seeds):
         del bank, cache, weights
     torch.cuda.synchronize()
     return host, raw
+
+
+def device_copy_gbs(torch, n_bytes=1 << 30, steps=5):
+    """Bytes moved (read + written) per second by a plain device-to-device copy."""
+    src = torch.ones(n_bytes // 2, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    gbs = 2 * n_bytes * steps / (time.perf_counter() - t0) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return gbs
 
 
 def pinned_h2d_gbs(torch, host):
