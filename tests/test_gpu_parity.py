@@ -10,7 +10,7 @@ import torch
 
 import oracle as O
 from paper_2608_15383_amd import api
-from paper_2608_15383_amd._lib import EMOE_ERANGE, ExactMoEError
+from paper_2608_15383_amd._lib import EMOE_ERANGE, EMOE_ESHAPE, ExactMoEError
 from paper_2608_15383_amd.inputs import (LayerInputs, LayerShape, OLMOE, TINY, bf16_bits_to_f32,
                                           f32_to_bf16_bits, make_layer, spread_logits)
 from tests._gpu import TOL, Layer, LazyExperts, dev, host_bits, quantize, rel_err
@@ -170,6 +170,31 @@ def test_forward_ragged_and_degenerate_shapes(shape, tokens, path):
     y = layer.forward(lay.h, path=path)
     ref, _ = oracle_y(lay, LazyExperts(lay), shape.top_k)
     assert_close(y, ref, f"{shape} T={tokens} path={path}")
+
+
+@pytest.mark.parametrize("shape", [LayerShape(8192, 256, 3, 2), LayerShape(256, 8192, 3, 2)])
+def test_mfma_at_its_group_limit(shape):
+    """64 input groups (d_model or d_ff = 8192), the most the MFMA path's
+    per-tile bias table holds, against the oracle on a ragged token count."""
+    lay = make_layer(shape, 70, seed=17)
+    layer = Layer(dims_of(shape), lay, 70)
+    y = layer.forward(lay.h, path=MFMA)
+    ref, _ = oracle_y(lay, LazyExperts(lay), shape.top_k)
+    assert_close(y, ref, f"{shape} MFMA")
+
+
+def test_mfma_past_its_group_limit_is_a_shape_error():
+    """65 groups: an explicit MFMA request fails with EMOE_ESHAPE; the automatic
+    choice takes the GEMV path and still matches the oracle."""
+    shape = LayerShape(8320, 128, 2, 1)
+    lay = make_layer(shape, 9, seed=18)
+    layer = Layer(dims_of(shape), lay, 9)
+    with pytest.raises(ExactMoEError) as ei:
+        layer.forward(lay.h, path=MFMA)
+    assert ei.value.status == EMOE_ESHAPE
+    y = layer.forward(lay.h)
+    ref, _ = oracle_y(lay, LazyExperts(lay), shape.top_k)
+    assert_close(y, ref, f"{shape} automatic path")
 
 
 @pytest.mark.parametrize("shape,tokens", [(LayerShape(128, 128, 200, 5), 300),
