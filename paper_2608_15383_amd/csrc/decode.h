@@ -9,7 +9,9 @@ namespace emoe {
 constexpr int kFusedMaxTokens = 4;   // tokens per fused call (one top-k wavefront each)
 constexpr int kFusedMaxPairs = 32;   // token-expert pairs per fused call
 constexpr int kSyncLanes = 16;       // logit replicas
-constexpr int kFusedActLdsBytes = 32768;  // LDS staging of all pairs' activation rows
+constexpr int kFusedActLdsBytes = 32768;  // LDS: the token rows (gate/up) or one activation
+                                          // row per wavefront (down)
+constexpr int kFusedActWords = kFusedMaxPairs * 2048;  // activation words handed over (d_ff <= 4096)
 
 // Data the workgroups of one fused launch hand to each other, in device
 // memory owned by the cache (zeroed at creation).  Every word carries the
@@ -24,7 +26,7 @@ struct DecodeSync {
   uint64_t logits[kSyncLanes][kFusedMaxTokens * EMOE_MAX_EXPERTS];
   // Activation rows in pair order: word w of pair pi holds act[pi][2w .. 2w+1]
   // (bf16, low column in the low 16 bits) at pi * d_ff / 2 + w.
-  uint64_t act[kFusedActLdsBytes / 4];
+  uint64_t act[kFusedActWords];
 };
 
 // Host side: the epoch of the last launch on one cache (the memory starts

@@ -39,41 +39,38 @@ namespace {
 constexpr uint32_t kSpinLimit = 1u << 20;
 constexpr int kPollSleep = 8;  // s_sleep units (64 clocks) between polls
 
-// Stage the activation rows of pairs p0, p0 + step, ... < P from the tagged
-// words (DecodeSync::act) in LDS act_lds ([pair][f] bf16), reading each row
-// until every word carries this launch's epoch (bounded); one wavefront.
-__device__ __forceinline__ void wave_stage_act_rows(DecodeSync* sy, const DecodeArgs& a, int p0,
-                                                    int step, int P, uint32_t* act_lds) {
+// Stage the activation row of pair pi from the tagged words (DecodeSync::act)
+// in LDS at dst (f bf16), reading it until every word carries this launch's
+// epoch (bounded); one wavefront.
+__device__ __forceinline__ void wave_stage_act_row(DecodeSync* sy, const DecodeArgs& a, int pi,
+                                                   uint32_t* dst) {
   constexpr int kWords = 8;  // words per lane per read
   const int lane = lane_id();
   const int nw = a.f / 2;  // words per row, a multiple of 64
-  for (int pi = p0; pi < P; pi += step) {
-    const uint64_t* src = sy->act + (int64_t)pi * nw;
-    uint32_t* dst = act_lds + pi * nw;
-    for (int w0 = 0; w0 < nw; w0 += 64 * kWords) {
-      uint32_t it = 0;
-      while (true) {
-        uint64_t x[kWords];
+  const uint64_t* src = sy->act + (int64_t)pi * nw;
+  for (int w0 = 0; w0 < nw; w0 += 64 * kWords) {
+    uint32_t it = 0;
+    while (true) {
+      uint64_t x[kWords];
 #pragma unroll
-        for (int k = 0; k < kWords; ++k) {
-          const int w = w0 + 64 * k + lane;
-          x[k] = w < nw ? __hip_atomic_load(src + w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                        : ((uint64_t)a.epoch << 32);
-        }
-        bool ok = true;
-#pragma unroll
-        for (int k = 0; k < kWords; ++k) {
-          const int w = w0 + 64 * k + lane;
-          ok = ok && (uint32_t)(x[k] >> 32) == a.epoch;
-          if (w < nw) dst[w] = (uint32_t)x[k];
-        }
-        if (__all(ok)) break;
-        if (++it > kSpinLimit) {
-          if (lane == 0) atomicAdd(&sy->timeouts, 1u);
-          break;
-        }
-        __builtin_amdgcn_s_sleep(kPollSleep);
+      for (int k = 0; k < kWords; ++k) {
+        const int w = w0 + 64 * k + lane;
+        x[k] = w < nw ? __hip_atomic_load(src + w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                      : ((uint64_t)a.epoch << 32);
       }
+      bool ok = true;
+#pragma unroll
+      for (int k = 0; k < kWords; ++k) {
+        const int w = w0 + 64 * k + lane;
+        ok = ok && (uint32_t)(x[k] >> 32) == a.epoch;
+        if (w < nw) dst[w] = (uint32_t)x[k];
+      }
+      if (__all(ok)) break;
+      if (++it > kSpinLimit) {
+        if (lane == 0) atomicAdd(&sy->timeouts, 1u);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(kPollSleep);
     }
   }
 }
@@ -137,7 +134,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   __shared__ int32_t s_ids[kFusedMaxPairs];
   __shared__ float s_w[kFusedMaxPairs];
   __shared__ uint4 s_act[kFusedActLdsBytes / 16];
-  __shared__ float s_xs[kFusedActLdsBytes / (2 * kGroup) * 4];  // [pair][group][quarter]
+  __shared__ float s_xs[kGemvWaves][kFusedActLdsBytes / (2 * kGroup * kGemvWaves) * 4];  // [wave][group][quarter]
   __shared__ uint64_t s_topk[kFusedMaxTokens][64];                // top-k scratch per token
   __shared__ int s_rank[kGemvWaves][64];                          // partial ranks (one token)
 
@@ -258,9 +255,12 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   if (wi < a.tokens)
     wave_topk_weights<false>(st, a.n_experts, a.top_k, a.renormalize, s_w + wi * a.top_k);
 
-  const uint16_t* act_lds = reinterpret_cast<const uint16_t*>(s_act);
-  uint32_t* act_lds32 = reinterpret_cast<uint32_t*>(s_act);
-  const int nw = a.f / 2;  // activation words per pair
+  // Each wavefront stages the activation row of the pair it is computing in
+  // its own slot of s_act (f bf16), one pair after another.
+  const int slot = __builtin_amdgcn_readfirstlane(wi);  // uniform: scalar slot addresses
+  const uint16_t* act_lds = reinterpret_cast<const uint16_t*>(s_act) + slot * a.f;
+  uint32_t* act_lds32 = reinterpret_cast<uint32_t*>(s_act) + slot * (a.f / 2);
+  float* xs_w = s_xs[slot];
   // Per-(group, quarter) activation sums of pair pi, groups [g0, g1).
   auto xs_sums = [&](int pi, int g0, int g1) {
     for (int i = 4 * g0 + lane; i < 4 * g1; i += 64) {
@@ -268,8 +268,8 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
       uint4 x[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k)
-        x[k] = *reinterpret_cast<const uint4*>(act_lds + pi * a.f + g * kGroup + 8 * q + 32 * k);
-      s_xs[pi * G * 4 + i] = lane_group_xsum(x);
+        x[k] = *reinterpret_cast<const uint4*>(act_lds + g * kGroup + 8 * q + 32 * k);
+      xs_w[i] = lane_group_xsum(x);
     }
   };
   // Expert output of pair pi for this row block from its staged activation
@@ -277,9 +277,9 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   auto pair_output = [&](int pi, DownBatch first, bool has_first) {
     const uint8_t* rec = a.slot_bank + (int64_t)s_ids[pi] * a.record_bytes;
     auto xload = [&](int, int k) {
-      return *reinterpret_cast<const uint4*>(act_lds + pi * a.f + k);
+      return *reinterpret_cast<const uint4*>(act_lds + k);
     };
-    auto xsload = [&](int, int g) { return s_xs[(pi * G + g) * 4 + (lane >> 4)]; };
+    auto xsload = [&](int, int g) { return xs_w[g * 4 + (lane >> 4)]; };
     float acc[kTokChunk] = {0.f, 0.f, 0.f, 0.f};
     if (!has_first) down_load_batch(rec, a.d, a.f, rb, 0, first);
     down_apply_batch_xs(first, a.f, 0, xload, xsload, 1, acc);
@@ -298,7 +298,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   // tiles are prefetched), so computing one pair overlaps the wait for the
   // next.
   auto stage = [&](int pi) {
-    wave_stage_act_rows(sy, a, pi, kGemvWaves, pi + 1, act_lds32);
+    wave_stage_act_row(sy, a, pi, act_lds32);
     xs_sums(pi, 0, G);
   };
   if (wi < P) {
@@ -358,7 +358,8 @@ int fused_capacity() {
 bool decode_fused_plan(DecodeArgs& a) {
   if (a.tokens < 1 || a.tokens > kFusedMaxTokens || a.tokens * a.top_k > kFusedMaxPairs)
     return false;
-  if ((int64_t)a.tokens * a.top_k * a.f * 2 > kFusedActLdsBytes) return false;
+  if ((int64_t)kGemvWaves * a.f * 2 > kFusedActLdsBytes) return false;  // a row per wavefront
+  if ((int64_t)a.tokens * a.top_k * (a.f / 2) > kFusedActWords) return false;
   if ((int64_t)a.tokens * a.d * 2 > kFusedActLdsBytes) return false;  // staged token rows
   const int P = a.tokens * a.top_k;
   const int pairs_of_f = a.f / kTileRows;
