@@ -234,10 +234,11 @@ int32_t emoe_fill_slots(emoe_cache* cache, const int32_t* fill_expert, const int
  * host.  Otherwise it copies counts[E] to the host once (one batched expert-id
  * transfer) and synchronizes `stream` to plan the waves.  If a fill fails the
  * cache map is restored to its state before that wave.
- * With full residency, the GEMV path and at most 4 tokens (and 32 pairs) the
- * whole layer runs as one fused kernel launch with the same arithmetic (and
- * bit-identical results).  Calls on one cache must not overlap in time (use
- * one stream, or order the streams): the cache holds that launch's counters. */
+ * With full residency, the GEMV path, at most 4 tokens (and 32 pairs),
+ * d_ff <= 4096 and tokens*d_model <= 16384 the whole layer runs as one fused
+ * kernel launch with the same arithmetic (and bit-identical results).  Calls
+ * on one cache must not overlap in time (use one stream, or order the
+ * streams): the cache holds the words that launch's workgroups hand over. */
 int32_t emoe_moe_forward(emoe_cache* cache, int32_t tokens, const uint16_t* h,
                          const uint16_t* w_router, const float* logits_override,
                          int32_t renormalize, int32_t path, uint16_t* y, void* workspace,
