@@ -340,6 +340,27 @@ def test_skewed_multi_wave_with_hot_experts(olmoe):
     assert_close(y1[:8], ref, "Zipf batch, first 8 tokens")
 
 
+def test_mfma_multi_wave_equals_single_wave(olmoe):
+    """The MFMA path through a 16-slot cache (4 waves over all 64 experts, 256
+    tokens): every wave's grouped launches skip the row tiles of experts
+    outside the wave, and the result equals the single-wave call bit for bit."""
+    lay, layer, experts = olmoe
+    dm = layer.dm
+    sub = _sub(lay, 256)
+    y1 = layer.forward(sub.h, path=MFMA)
+    host = _host_bank(layer)
+    slots = torch.zeros(16 * api.expert_record_bytes(dm), dtype=torch.uint8, device="cuda:0")
+    cache = api.Cache(dm, 16, slot_bank=slots, host_bank=host)
+    st = api.Stats()
+    y = layer.forward(sub.h, cache=cache, stats=st, path=MFMA)
+    cache.close()
+    assert st.waves == 4
+    assert np.array_equal(y, y1)
+    ref, _ = oracle_y(sub, experts, 8, tokens=[0, 255])
+    assert_close(y[[0, 255]], ref, "MFMA multi-wave")
+    experts.cache.clear()
+
+
 def test_global_to_slot_map_permutation(olmoe):
     """Experts placed in permuted slots give the identical output (map preflight)."""
     lay, layer, _ = olmoe
