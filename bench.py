@@ -139,23 +139,49 @@ def oracle_baseline(weights, wr, h, k, alg_bytes, flops, unit, budget_s=12.0):
     needed = sorted(set(r.ids.reshape(-1).tolist()))
     experts = {e: O.quantize_expert(bf16_bits_to_f32(wg[e]), bf16_bits_to_f32(wu[e]),
                                     bf16_bits_to_f32(wd[e])) for e in needed}
-    calls, t0 = 0, time.perf_counter()
-    y = None
-    while True:
+    out = {}
+
+    def call():
         for ex in experts.values():
             ex._hat.clear()          # dequantize again each call, as the GPU path does
-        rr = O.route(hf, wrf, k)
-        y = O.moe_forward(hf, experts, rr)
+        out["y"] = O.moe_forward(hf, experts, O.route(hf, wrf, k))
+
+    calls, el = timed_calls(call, budget_s)
+    per_call = el / calls
+    value = alg_bytes / per_call / 1e9 if unit == "GB/s" else flops / per_call / 1e12
+    res = dict(value=value, unit=unit, cores=int(threads), kind="oracle",
+               sample=f"{calls} full layer calls of this workload ({hf.shape[0]} token(s)), "
+                      f"{el:.1f} s, numpy fp64 with dequantization each call",
+               seconds_per_call=per_call)
+    one = single_thread_rate(call, budget_s / 2)
+    if one is not None:
+        c1, e1 = one
+        per1 = e1 / c1
+        res["single_thread"] = dict(
+            value=alg_bytes / per1 / 1e9 if unit == "GB/s" else flops / per1 / 1e12,
+            cores=1, sample=f"{c1} calls, {e1:.1f} s, BLAS and OpenMP pools limited to 1 thread")
+    return out["y"], res
+
+
+def timed_calls(call, budget_s):
+    """Run call() until budget_s has passed (at most 1000 calls); (calls, seconds)."""
+    calls, t0 = 0, time.perf_counter()
+    while True:
+        call()
         calls += 1
         el = time.perf_counter() - t0
         if el >= budget_s or calls >= 1000:
-            break
-    per_call = el / calls
-    value = alg_bytes / per_call / 1e9 if unit == "GB/s" else flops / per_call / 1e12
-    return y, dict(value=value, unit=unit, cores=int(threads), kind="oracle",
-                   sample=f"{calls} full layer calls of this workload ({hf.shape[0]} token(s)), "
-                          f"{el:.1f} s, numpy fp64 with dequantization each call",
-                   seconds_per_call=per_call)
+            return calls, el
+
+
+def single_thread_rate(call, budget_s):
+    """The same oracle calls with every thread pool held to one thread, or None."""
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:
+        return None
+    with threadpool_limits(limits=1):
+        return timed_calls(call, budget_s)
 
 
 def bench_layer(args):
@@ -434,18 +460,20 @@ def oracle_multiwave(weights, T, head, budget_s=12.0):
     needed = sorted(set(r.ids.reshape(-1).tolist()))
     experts = {e: O.quantize_expert(bf16_bits_to_f32(wg[e]), bf16_bits_to_f32(wu[e]),
                                     bf16_bits_to_f32(wd[e])) for e in needed}
-    calls, t0 = 0, time.perf_counter()
-    while True:
+    def call():
         for ex in experts.values():
             ex._hat.clear()
         O.moe_forward(h, experts, O.route(h, None, TOP_K, logits_override=z))
-        calls += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or calls >= 1000:
-            break
-    return dict(value=T * calls / el, unit="tokens/s", cores=int(threads), kind="oracle",
-                sample=f"{calls} calls of the 16-token, 56-expert batch, {el:.1f} s, numpy fp64 "
-                       f"with dequantization each call")
+
+    calls, el = timed_calls(call, budget_s)
+    res = dict(value=T * calls / el, unit="tokens/s", cores=int(threads), kind="oracle",
+               sample=f"{calls} calls of the 16-token, 56-expert batch, {el:.1f} s, numpy fp64 "
+                      f"with dequantization each call")
+    one = single_thread_rate(call, budget_s / 2)
+    if one is not None:
+        res["single_thread"] = dict(value=T * one[0] / one[1], cores=1,
+                                    sample=f"{one[0]} calls, {one[1]:.1f} s, thread pools limited to 1")
+    return res
 
 
 def bench_stack(args):
