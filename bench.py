@@ -288,6 +288,12 @@ def bench_layer(args):
         # The same bytes against what a plain device copy achieves on this GPU.
         cp = device_copy_gbs(torch)
         out["device_copy"] = dict(gbs=cp, layer_frac=value / cp, kernel_frac=roof["achieved"] / cp)
+        # One call per bank captured into a HIP graph and replayed.
+        us, same = graph_replay(torch, lambda i: api.moe_forward(caches[i], h, wr, y, ws),
+                                n_banks, max(steps // n_banks, 1), y)
+        out["graph_replay"] = dict(us_per_call=us, gbs=alg_bytes / (us * 1e-6) / 1e9,
+                                   calls_per_graph=n_banks, equals_eager=same)
+        log(f"graph replay: {us:.2f} us per call, equal to eager: {same}")
 
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
@@ -340,6 +346,35 @@ def device_copy_gbs(torch, n_bytes=1 << 30, steps=5):
     del src, dst
     torch.cuda.empty_cache()
     return gbs
+
+
+def graph_replay(torch, call, n_calls, reps, y):
+    """Capture call(0 .. n_calls-1) into one HIP graph and replay it `reps`
+    times: (us per call, whether the last replay's y equals an eager call's)."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for i in range(n_calls):
+            call(i)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    eager = y.clone()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for i in range(n_calls):
+            call(i)
+    graph.replay()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        graph.replay()
+    t1.record()
+    torch.cuda.synchronize()
+    same = bool(torch.equal(y, eager))
+    del graph
+    return t0.elapsed_time(t1) * 1e3 / (reps * n_calls), same
 
 
 def pinned_h2d_gbs(torch, host):

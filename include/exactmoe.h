@@ -238,7 +238,12 @@ int32_t emoe_fill_slots(emoe_cache* cache, const int32_t* fill_expert, const int
  * d_ff <= 4096 and tokens*d_model <= 16384 the whole layer runs as one fused
  * kernel launch with the same arithmetic (and bit-identical results).  Calls
  * on one cache must not overlap in time (use one stream, or order the
- * streams): the cache holds the words that launch's workgroups hand over. */
+ * streams): the cache holds the words that launch's workgroups hand over.
+ * With full residency the call may be captured into a HIP graph: a captured
+ * fused launch numbers its hand-over words from device memory, so every
+ * replay is distinct, and replays and direct calls on one cache may be mixed
+ * in any order.  Without full residency the call synchronizes `stream` and
+ * cannot be captured. */
 int32_t emoe_moe_forward(emoe_cache* cache, int32_t tokens, const uint16_t* h,
                          const uint16_t* w_router, const float* logits_override,
                          int32_t renormalize, int32_t path, uint16_t* y, void* workspace,

@@ -111,7 +111,7 @@ struct emoe_cache {
   hipEvent_t ready[kCopyStreams] = {};       // completion of each stream's last fills
   int32_t* counts_host = nullptr;   // pinned [E]: the batched expert-id transfer
   DecodeSync* sync = nullptr;       // device: hand-over data of the fused decode launches
-  DecodeProgress prog;              // host: epoch of the last fused launch
+  DecodeProgress prog;              // host: epoch of the last direct fused launch
 };
 
 namespace {
@@ -409,6 +409,9 @@ int32_t emoe_cache_create(const emoe_dims* dims, int32_t capacity, void* slot_ba
                                            sizeof(int32_t) * dims->n_experts, hipHostMallocDefault);
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&c->sync), sizeof(DecodeSync));
     if (e == hipSuccess) e = hipMemset(c->sync, 0, sizeof(DecodeSync));
+    const uint32_t first_epoch = kDeviceEpoch0;  // returns once the zeroing is done, too
+    if (e == hipSuccess)
+      e = hipMemcpy(&c->sync->epoch, &first_epoch, sizeof first_epoch, hipMemcpyHostToDevice);
     if (e == hipSuccess && host_bank) {
       for (int j = 0; j < emoe_cache::kCopyStreams && e == hipSuccess; ++j) {
         e = hipStreamCreateWithFlags(&c->copy_stream[j], hipStreamNonBlocking);

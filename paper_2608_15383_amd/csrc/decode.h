@@ -1,5 +1,5 @@
 // Fused decode launch (decode.hip): arguments, the per-cache synchronization
-// block, the host-side launch epoch, and the planning rule.
+// block and the planning rule.
 #pragma once
 
 #include "common.h"
@@ -12,27 +12,33 @@ constexpr int kSyncLanes = 16;       // logit replicas
 constexpr int kFusedActLdsBytes = 32768;  // LDS: the token rows (gate/up) or one activation
                                           // row per wavefront (down)
 constexpr int kFusedActWords = kFusedMaxPairs * 2048;  // activation words handed over (d_ff <= 4096)
+constexpr int kFusedMaxBlocks = 1024;  // workgroups per fused launch
+constexpr uint32_t kDeviceEpoch0 = 0x80000000u;  // first epoch of captured launches
 
 // Data the workgroups of one fused launch hand to each other, in device
 // memory owned by the cache (zeroed at creation).  Every word carries the
 // launch's epoch in its high half and the payload in the low half: a reader
 // polls the data itself (one 64-bit store is seen whole or not at all), so no
-// counter, fence or reset is needed between launches.  `timeouts` counts
-// bounded waits that gave up.
+// per-word reset is needed between launches.  A launch made directly takes its
+// epoch from the host (1 .. kDeviceEpoch0 - 1, cycling; 0 is the zeroed
+// memory's tag and is never used).  A launch captured into a graph would
+// replay one argument forever, so it takes its epoch from `epoch` here
+// (kDeviceEpoch0 .. 2^32 - 1, cycling): every workgroup reads it at its start,
+// stores it in its own `arrived` word once it has used it, and router
+// workgroup 0, when every word of the grid holds it, stores the next one.
+// `timeouts` counts bounded waits that gave up.
 struct DecodeSync {
   uint32_t timeouts;
-  uint32_t pad1[15];
+  uint32_t pad0[15];
   // Replicated copies of the logits, [replica][token][expert].
   uint64_t logits[kSyncLanes][kFusedMaxTokens * EMOE_MAX_EXPERTS];
   // Activation rows in pair order: word w of pair pi holds act[pi][2w .. 2w+1]
   // (bf16, low column in the low 16 bits) at pi * d_ff / 2 + w.
   uint64_t act[kFusedActWords];
-};
-
-// Host side: the epoch of the last launch on one cache (the memory starts
-// zeroed, and epoch 0 is never used).
-struct DecodeProgress {
-  uint32_t epoch = 0;
+  uint32_t epoch;  // tag of the next captured launch (kDeviceEpoch0 after creation)
+  uint32_t pad1[15];
+  // Word b: the epoch that workgroup b of the latest launch used.
+  uint32_t arrived[kFusedMaxBlocks];
 };
 
 struct DecodeArgs {
@@ -58,12 +64,19 @@ struct DecodeArgs {
   // Filled by decode_fused_plan / launch_decode_fused.
   int n_router, n_gate, n_down;
   int pairs_per_item;             // gate/up row-block pairs per gate item
-  uint32_t epoch;                 // this launch's tag
+  uint32_t epoch;                 // this launch's tag; 0: read it from DecodeSync
+};
+
+// Host side: the epoch of the last direct launch on one cache.
+struct DecodeProgress {
+  uint32_t epoch = 0;
 };
 
 // Size the grid; false if the layer does not fit one co-resident fused launch.
 bool decode_fused_plan(DecodeArgs& a);
-// Take the next epoch from `prog`, launch, advance `prog` on success.
+// Launch a planned call on `stream` (no host synchronization): a direct
+// launch takes the next epoch from `prog`, a launch being captured into a
+// graph takes its epochs from device memory.
 hipError_t launch_decode_fused(DecodeArgs& a, DecodeProgress& prog, hipStream_t stream);
 
 }  // namespace emoe

@@ -20,7 +20,10 @@
 // Data crossing workgroups (logits, activation rows) travels as 64-bit words
 // tagged with the launch's epoch, written and read device-coherently: the
 // reader polls the data itself, so one store is both the payload and the
-// signal, and nothing needs resetting between launches.  A workgroup only
+// signal, and nothing needs resetting between launches.  The host numbers
+// launches itself; a launch captured into a graph instead takes its epoch
+// from device memory and advances it there, so that every replay has a new
+// one (the two kinds use disjoint halves of the tag space).  A workgroup only
 // waits for workgroups of lower index, which the hardware dispatches first,
 // and the grid is sized to be co-resident on an idle GPU.  Every wait is
 // still bounded and counts a timeout instead of spinning forever.
@@ -42,8 +45,8 @@ constexpr int kPollSleep = 8;  // s_sleep units (64 clocks) between polls
 // Stage the activation row of pair pi from the tagged words (DecodeSync::act)
 // in LDS at dst (f bf16), reading it until every word carries this launch's
 // epoch (bounded); one wavefront.
-__device__ __forceinline__ void wave_stage_act_row(DecodeSync* sy, const DecodeArgs& a, int pi,
-                                                   uint32_t* dst) {
+__device__ __forceinline__ void wave_stage_act_row(DecodeSync* sy, const DecodeArgs& a,
+                                                   uint32_t epoch, int pi, uint32_t* dst) {
   constexpr int kWords = 8;  // words per lane per read
   const int lane = lane_id();
   const int nw = a.f / 2;  // words per row, a multiple of 64
@@ -56,13 +59,13 @@ __device__ __forceinline__ void wave_stage_act_row(DecodeSync* sy, const DecodeA
       for (int k = 0; k < kWords; ++k) {
         const int w = w0 + 64 * k + lane;
         x[k] = w < nw ? __hip_atomic_load(src + w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                      : ((uint64_t)a.epoch << 32);
+                      : ((uint64_t)epoch << 32);
       }
       bool ok = true;
 #pragma unroll
       for (int k = 0; k < kWords; ++k) {
         const int w = w0 + 64 * k + lane;
-        ok = ok && (uint32_t)(x[k] >> 32) == a.epoch;
+        ok = ok && (uint32_t)(x[k] >> 32) == epoch;
         if (w < nw) dst[w] = (uint32_t)x[k];
       }
       if (__all(ok)) break;
@@ -78,8 +81,8 @@ __device__ __forceinline__ void wave_stage_act_row(DecodeSync* sy, const DecodeA
 // Token t's logits into st.v: from logits_override, or from the router
 // items' tagged words (replica `replica`), read until every word carries this
 // launch's epoch (bounded).
-__device__ __forceinline__ void load_logits(DecodeSync* sy, const DecodeArgs& a, int replica, int t,
-                                            TopkState& st) {
+__device__ __forceinline__ void load_logits(DecodeSync* sy, const DecodeArgs& a, uint32_t epoch,
+                                            int replica, int t, TopkState& st) {
   const int lane = lane_id();
   const int E = a.n_experts;
   if (a.logits_override) {
@@ -99,7 +102,7 @@ __device__ __forceinline__ void load_logits(DecodeSync* sy, const DecodeArgs& a,
       const int e = lane + 64 * c;
       if (e < E) {
         const uint64_t x = __hip_atomic_load(zt + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        ok = ok && (uint32_t)(x >> 32) == a.epoch;
+        ok = ok && (uint32_t)(x >> 32) == epoch;
         st.v[c] = __uint_as_float((uint32_t)x);
       } else {
         st.v[c] = 0.f;
@@ -112,6 +115,51 @@ __device__ __forceinline__ void load_logits(DecodeSync* sy, const DecodeArgs& a,
     }
     __builtin_amdgcn_s_sleep(kPollSleep);
   }
+}
+
+// The epoch of a captured launch, as the last one left it.  The same in every
+// lane; used as loaded, so the first wait for the load is at the first use.
+__device__ __forceinline__ uint32_t launch_epoch(DecodeSync* sy) {
+  return __hip_atomic_load(&sy->epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Record that workgroup blk has read this launch's epoch (one thread).  The
+// word is a plain store to the workgroup's own location, so nothing contends;
+// the empty asm takes the epoch as an operand, so the store is issued only
+// once the load of the old epoch has returned.
+__device__ __forceinline__ void arrive(DecodeSync* sy, uint32_t epoch, int blk) {
+  uint32_t e = epoch;
+  asm volatile("" : "+v"(e));
+  __hip_atomic_store(&sy->arrived[blk], e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Router workgroup 0, one wavefront: once every workgroup of the launch has
+// recorded this epoch (bounded wait), store the next one (skipping 0, the tag
+// of zeroed memory).  No
+// workgroup waits on this one after its logits are out, so the wait ends
+// whether or not the grid is co-resident.
+__device__ __forceinline__ void advance_epoch(DecodeSync* sy, uint32_t epoch, int n_blocks) {
+  constexpr int kPer = kFusedMaxBlocks / 64;
+  const int lane = lane_id();
+  uint32_t it = 0;
+  while (true) {
+    bool ok = true;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      const int b = lane + 64 * k;
+      if (b < n_blocks)
+        ok = ok && __hip_atomic_load(&sy->arrived[b], __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT) == epoch;
+    }
+    if (__all(ok)) break;
+    if (++it > kSpinLimit) {
+      if (lane == 0) atomicAdd(&sy->timeouts, 1u);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(kPollSleep);
+  }
+  const uint32_t next = epoch + 1u == 0u ? kDeviceEpoch0 : epoch + 1u;
+  if (lane == 0) __hip_atomic_store(&sy->epoch, next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Copy `bytes` (a multiple of 256) from coherent global memory to LDS with
@@ -127,6 +175,9 @@ __device__ __forceinline__ void wave_copy_to_lds(const void* src, uint32_t bytes
         (int)voff, (int)off, 0, /*sc1*/ 16);
 }
 
+// kDevEpoch: the launch is being captured into a graph and reads its epoch
+// from DecodeSync (a.epoch is 0); otherwise a.epoch is the host's number.
+template <bool kDevEpoch>
 __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   __shared__ GroupShared<256> gsh;
   __shared__ GateUpShared gush;
@@ -144,6 +195,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   const int blk = blockIdx.x;
   DecodeSync* sy = a.sync;
   const int P = a.tokens * a.top_k;
+  const uint32_t epoch = kDevEpoch ? launch_epoch(sy) : a.epoch;
 
   if (blk < a.n_router) {
     // ---------------------------------------------------------------- router
@@ -161,11 +213,15 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
           const uint32_t v = __float_as_uint((float)s[t][0]);
           const int at = t * a.n_experts + e0;
           if (lane < kSyncLanes)
-            __hip_atomic_store(&sy->logits[lane][at], ((uint64_t)a.epoch << 32) | v,
+            __hip_atomic_store(&sy->logits[lane][at], ((uint64_t)epoch << 32) | v,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           if (lane == kSyncLanes) st_u32<false>(a.logits + at, v);
         }
       }
+    }
+    if (kDevEpoch) {
+      if (tid == 0) arrive(sy, epoch, blk);
+      if (blk == 0 && wi == 0) advance_epoch(sy, epoch, (int)gridDim.x);
     }
     return;
   }
@@ -193,7 +249,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     static_assert(kGemvWaves * 16 == 64, "a quarter of 64 keys per wavefront");
     uint64_t* keys = s_topk[1];
     if (wi == 0) {
-      load_logits(sy, a, replica, 0, st);
+      load_logits(sy, a, epoch, replica, 0, st);
       keys[lane] = topk_lane_key(st, a.n_experts);
     }
     __syncthreads();
@@ -207,12 +263,17 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
       wave_topk_store_ids<false>(st, a.top_k, s_ids);
     }
   } else if (wi < a.tokens) {
-    load_logits(sy, a, replica, wi, st);
+    load_logits(sy, a, epoch, replica, wi, st);
     wave_topk_select_loaded(a.n_experts, a.top_k, st, s_topk[wi]);
     wave_topk_store_ids<false>(st, a.top_k, s_ids + wi * a.top_k);
   }
   if (is_gate) wait_memory();  // the staged rows
   __syncthreads();
+  // A read epoch has been waited for by now (the logits' tags): from here on
+  // a scalar.  Down workgroups record it before their first tile loads, so
+  // that no later wait covers the store; gate/up workgroups at their end.
+  const uint32_t ep = kDevEpoch ? __builtin_amdgcn_readfirstlane(epoch) : a.epoch;
+  if (kDevEpoch && !is_gate && tid == 0) arrive(sy, ep, blk);
 
   if (is_gate) {
     // ---------------------------------------------------------------- gate/up
@@ -229,7 +290,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     // The activation goes out as tagged words (DecodeSync::act), which the
     // down workgroups poll directly: the store is the signal.
     const int d = a.d, f = a.f;
-    const uint64_t tag = (uint64_t)a.epoch << 32;
+    const uint64_t tag = (uint64_t)ep << 32;
     uint64_t* act_tag = sy->act;
     for (int b = b0; b < b1; ++b)
       gateup_rows(gush, a.d, a.f, [=](int s) { return h_lds + (s / top_k) * d; }, pi, pi + 1,
@@ -237,6 +298,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
                     __hip_atomic_store(act_tag + ((s * f + n) >> 1), tag | v, __ATOMIC_RELAXED,
                                        __HIP_MEMORY_SCOPE_AGENT);
                   });
+    if (kDevEpoch && tid == 0) arrive(sy, ep, blk);
     return;
   }
 
@@ -298,7 +360,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   // tiles are prefetched), so computing one pair overlaps the wait for the
   // next.
   auto stage = [&](int pi) {
-    wave_stage_act_row(sy, a, pi, act_lds32);
+    wave_stage_act_row(sy, a, ep, pi, act_lds32);
     xs_sums(pi, 0, G);
   };
   if (wi < P) {
@@ -333,7 +395,8 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   }
 }
 
-// Co-resident workgroups of the fused kernel on the current device.
+// Co-resident workgroups of the fused kernel (either form) on the current
+// device.
 int fused_capacity() {
   static std::mutex mu;
   static int cap[64] = {};
@@ -341,14 +404,16 @@ int fused_capacity() {
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
   std::lock_guard<std::mutex> lk(mu);
   if (cap[dev] == 0) {
-    int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_fused_kernel, 256, 0) !=
-            hipSuccess ||
+    int per_cu = 0, per_cu_dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_fused_kernel<false>, 256,
+                                                     0) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_dev, decode_fused_kernel<true>, 256,
+                                                     0) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
       (void)hipGetLastError();
       return 0;
     }
-    cap[dev] = per_cu * cus;
+    cap[dev] = min(per_cu, per_cu_dev) * cus;
   }
   return cap[dev];
 }
@@ -369,7 +434,7 @@ bool decode_fused_plan(DecodeArgs& a) {
   for (int ppi = 1; ppi <= pairs_of_f; ppi *= 2) {
     const int chunks = (pairs_of_f + ppi - 1) / ppi;
     const int n_gate = P * chunks;
-    if (a.n_router + n_gate + a.n_down <= cap) {
+    if (a.n_router + n_gate + a.n_down <= min(cap, kFusedMaxBlocks)) {
       a.pairs_per_item = ppi;
       a.n_gate = n_gate;
       return true;
@@ -379,11 +444,21 @@ bool decode_fused_plan(DecodeArgs& a) {
 }
 
 hipError_t launch_decode_fused(DecodeArgs& a, DecodeProgress& prog, hipStream_t stream) {
-  a.epoch = prog.epoch + 1u;
-  if (a.epoch == 0u) a.epoch = 1u;  // 0 is the zeroed memory's tag
-  launch(decode_fused_kernel, dim3(a.n_router + a.n_gate + a.n_down), dim3(256), stream, a);
-  const hipError_t e = hipGetLastError();
-  if (e == hipSuccess) prog.epoch = a.epoch;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(stream, &cs);
+  if (e != hipSuccess) return e;
+  if (cs == hipStreamCaptureStatusNone) {
+    a.epoch = prog.epoch + 1u >= kDeviceEpoch0 ? 1u : prog.epoch + 1u;
+  } else {
+    a.epoch = 0u;  // replays number themselves in device memory
+  }
+  const dim3 grid(a.n_router + a.n_gate + a.n_down);
+  if (a.epoch != 0u)
+    launch(decode_fused_kernel<false>, grid, dim3(256), stream, a);
+  else
+    launch(decode_fused_kernel<true>, grid, dim3(256), stream, a);
+  e = hipGetLastError();
+  if (e == hipSuccess && a.epoch != 0u) prog.epoch = a.epoch;
   return e;
 }
 

@@ -371,11 +371,12 @@ __device__ __forceinline__ uint64_t match_expert(bool valid, int e, int bits) {
 // pairs per expert, a scan turns the counts into each wavefront's first
 // position per expert, and pass 2 places its pairs in order.
 template <int kThreads, bool kCo>
-__device__ void block_group(GroupShared<kThreads>& sh, int pairs, int n_experts,
-                            const int32_t* __restrict__ ids, int32_t* __restrict__ counts,
-                            int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_pairs,
-                            int32_t* __restrict__ active, int32_t* __restrict__ n_active,
-                            int32_t* __restrict__ tile_offsets, int32_t* __restrict__ pair_pos) {
+__device__ __forceinline__ void block_group(
+    GroupShared<kThreads>& sh, int pairs, int n_experts, const int32_t* __restrict__ ids,
+    int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ sorted_pairs, int32_t* __restrict__ active,
+    int32_t* __restrict__ n_active, int32_t* __restrict__ tile_offsets,
+    int32_t* __restrict__ pair_pos) {
   constexpr int kWaves = kThreads / 64;
   const int tid = threadIdx.x;
   const int lane = lane_id();

@@ -452,3 +452,44 @@ def test_fused_decode_repeated_calls_and_override():
     ref, _ = oracle_y(_sub(lay, 4), experts, 8, logits=z)
     assert_close(y, ref, "fused with override")
     assert layer.cache.sync_timeouts() == 0
+
+
+@pytest.mark.parametrize("tokens,path,launches", [(2, api.EMOE_PATH_AUTO, 1), (8, GEMV, None),
+                                                   (48, MFMA, None)])
+def test_resident_layer_replays_from_a_captured_graph(tokens, path, launches):
+    """A fully resident layer call captured into a HIP graph replays correctly,
+    replay after replay: the fused decode launch (2 tokens) takes its hand-over
+    epoch from device memory, not from its launch arguments.  Eager calls run
+    between the replays; every replay equals the eager call on the same input
+    bit for bit."""
+    lay = make_layer(OLMOE, tokens, seed=23)
+    layer = Layer(dims_of(OLMOE), lay, tokens)
+    rng = np.random.default_rng(29)
+    hs = [f32_to_bf16_bits(rng.standard_normal((tokens, OLMOE.d_model)).astype(np.float32))
+          for _ in range(3)]
+    h = dev(hs[0])
+    y = torch.empty_like(h)
+    st = api.Stats()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):   # first call outside the capture
+        api.moe_forward(layer.cache, h, layer.wr, y, layer.ws, path=path, stats=st)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    assert launches is None or st.kernel_launches == launches
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        api.moe_forward(layer.cache, h, layer.wr, y, layer.ws, path=path)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for i, hb in enumerate(hs):
+            expect = layer.forward(hb, path=path)
+            h.copy_(dev(hb))
+            graph.replay()
+            torch.cuda.synchronize()
+            got = bf16_bits_to_f32(host_bits(y))
+            assert np.array_equal(got, expect), (rep, i)
+    last = LayerInputs(lay.shape, lay.w_gate, lay.w_up, lay.w_down, lay.w_router, hs[-1])
+    ref, _ = oracle_y(last, LazyExperts(lay), OLMOE.top_k)
+    assert_close(got, ref, f"graph replay T={tokens}")
+    assert layer.cache.sync_timeouts() == 0
