@@ -172,6 +172,51 @@ def test_forward_ragged_and_degenerate_shapes(shape, tokens, path):
     assert_close(y, ref, f"{shape} T={tokens} path={path}")
 
 
+def _random_cases(n, seed, max_tokens=80):
+    """Seeded layer shapes within the documented limits: d_model, d_ff in
+    128 .. 1024, 1 .. 96 experts, top_k up to 16, 1 .. max_tokens tokens, and a
+    slot capacity between top_k and E."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(n):
+        d, f = 128 * int(rng.integers(1, 9)), 128 * int(rng.integers(1, 9))
+        e = int(rng.integers(1, 97))
+        k = int(rng.integers(1, min(e, 16) + 1))
+        t = int(rng.integers(1, max_tokens + 1))
+        cases.append((LayerShape(d, f, e, k), t, int(rng.integers(k, e + 1))))
+    return cases
+
+
+@pytest.mark.parametrize("shape,tokens,capacity",
+                         _random_cases(10, 41) + _random_cases(6, 43, max_tokens=4))
+def test_random_shapes_every_path(shape, tokens, capacity):
+    """Each path against the oracle on seeded random shapes; through a cache of
+    `capacity` slots (several waves when the call touches more experts) each
+    path equals its resident call bit for bit, and so does the sequential path.
+    With at most 4 tokens the resident default call is the fused decode launch
+    where it fits."""
+    lay = make_layer(shape, tokens, seed=shape.d_model + shape.n_experts + tokens)
+    layer = Layer(dims_of(shape), lay, tokens)
+    ref, _ = oracle_y(lay, LazyExperts(lay), shape.top_k)
+    resident = {}
+    for path in (GEMV, MFMA, api.EMOE_PATH_AUTO):
+        st = api.Stats()
+        resident[path] = layer.forward(lay.h, path=path, stats=st)
+        assert_close(resident[path], ref, f"{shape} T={tokens} path={path}")
+    k, f, d = shape.top_k, shape.d_ff, shape.d_model
+    fused = (tokens <= 4 and tokens * k <= 32 and 4 * f * 2 <= 32768
+             and tokens * d * 2 <= 32768 and tokens * k * f // 2 <= 32 * 2048)
+    assert (st.kernel_launches == 1) == fused
+    dm = layer.dm
+    slots = torch.zeros(capacity * api.expert_record_bytes(dm), dtype=torch.uint8, device="cuda:0")
+    cache = api.Cache(dm, capacity, slot_bank=slots, host_bank=_host_bank(layer))
+    for path in (GEMV, MFMA):
+        assert np.array_equal(layer.forward(lay.h, path=path, cache=cache), resident[path]), path
+    assert np.array_equal(layer.forward(lay.h, path=GEMV, cache=cache, sequential=True),
+                          resident[GEMV])
+    cache.close()
+
+
 @pytest.mark.parametrize("shape", [LayerShape(8192, 256, 3, 2), LayerShape(256, 8192, 3, 2)])
 def test_mfma_at_its_group_limit(shape):
     """64 input groups (d_model or d_ff = 8192), the most the MFMA path's
