@@ -179,6 +179,10 @@ int32_t emoe_route(const emoe_dims* dims, int32_t tokens, const uint16_t* h,
  * copy streams (default priority) and one completion event per slot. */
 int32_t emoe_cache_create(const emoe_dims* dims, int32_t capacity, void* slot_bank,
                           const void* host_bank, emoe_cache** out);
+/* Waits for the cache's copy streams and frees what the cache allocated
+ * (events, streams, the hand-over block of the fused decode launch).  Device
+ * work that uses the cache, including replays of graphs captured from its
+ * layer calls, must have finished and must not be enqueued again. */
 int32_t emoe_cache_destroy(emoe_cache* cache);
 /* C = E only: identity map, no replacement and no hit accounting afterwards.
  * Copies the host bank into the slot bank on `stream` when a host bank is
