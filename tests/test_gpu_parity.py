@@ -188,7 +188,8 @@ def _random_cases(n, seed, max_tokens=80):
 
 
 @pytest.mark.parametrize("shape,tokens,capacity",
-                         _random_cases(10, 41) + _random_cases(6, 43, max_tokens=4))
+                         _random_cases(10, 41) + _random_cases(6, 43, max_tokens=4)
+                         + _random_cases(6, 107, max_tokens=300))
 def test_random_shapes_every_path(shape, tokens, capacity):
     """Each path against the oracle on seeded random shapes; through a cache of
     `capacity` slots (several waves when the call touches more experts) each
