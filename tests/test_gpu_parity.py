@@ -500,9 +500,10 @@ def test_fused_decode_repeated_calls_and_override():
     assert layer.cache.sync_timeouts() == 0
 
 
-@pytest.mark.parametrize("tokens,path,launches", [(2, api.EMOE_PATH_AUTO, 1), (8, GEMV, None),
-                                                   (48, MFMA, None)])
-def test_resident_layer_replays_from_a_captured_graph(tokens, path, launches):
+@pytest.mark.parametrize("tokens,path,launches,override",
+                         [(2, api.EMOE_PATH_AUTO, 1, False), (3, api.EMOE_PATH_AUTO, 1, True),
+                          (8, GEMV, None, False), (48, MFMA, None, False)])
+def test_resident_layer_replays_from_a_captured_graph(tokens, path, launches, override):
     """A fully resident layer call captured into a HIP graph replays correctly,
     replay after replay: the fused decode launch (2 tokens) takes its hand-over
     epoch from device memory, not from its launch arguments.  Eager calls run
@@ -515,27 +516,30 @@ def test_resident_layer_replays_from_a_captured_graph(tokens, path, launches):
           for _ in range(3)]
     h = dev(hs[0])
     y = torch.empty_like(h)
+    z = spread_logits(tokens, 64, 8, 16, seed=5) if override else None
+    lo = dev(z) if override else None
     st = api.Stats()
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):   # first call outside the capture
-        api.moe_forward(layer.cache, h, layer.wr, y, layer.ws, path=path, stats=st)
+        api.moe_forward(layer.cache, h, layer.wr, y, layer.ws, logits_override=lo, path=path,
+                        stats=st)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     assert launches is None or st.kernel_launches == launches
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
-        api.moe_forward(layer.cache, h, layer.wr, y, layer.ws, path=path)
+        api.moe_forward(layer.cache, h, layer.wr, y, layer.ws, logits_override=lo, path=path)
     torch.cuda.synchronize()
     for rep in range(3):
         for i, hb in enumerate(hs):
-            expect = layer.forward(hb, path=path)
+            expect = layer.forward(hb, logits=z, path=path)
             h.copy_(dev(hb))
             graph.replay()
             torch.cuda.synchronize()
             got = bf16_bits_to_f32(host_bits(y))
             assert np.array_equal(got, expect), (rep, i)
     last = LayerInputs(lay.shape, lay.w_gate, lay.w_up, lay.w_down, lay.w_router, hs[-1])
-    ref, _ = oracle_y(last, LazyExperts(lay), OLMOE.top_k)
+    ref, _ = oracle_y(last, LazyExperts(lay), OLMOE.top_k, logits=z)
     assert_close(got, ref, f"graph replay T={tokens}")
     assert layer.cache.sync_timeouts() == 0
