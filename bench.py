@@ -66,6 +66,8 @@ def parse():
     p.add_argument("--workload", default="decode",
                    choices=["decode", "prefill", "multiwave", "stack", "frontier", "copy"])
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-prefill", action="store_true",
+                   help="decode only: skip the prefill sub-record")
     return p.parse_args()
 
 
@@ -184,36 +186,26 @@ def single_thread_rate(call, budget_s):
         return timed_calls(call, budget_s)
 
 
-def bench_layer(args):
-    import torch
-    from paper_2608_15383_amd import api
-
-    torch.cuda.init()
-    dm = api.dims(D_MODEL, D_FF, N_EXPERTS, TOP_K)
-    decode = args.workload == "decode"
-    T = 1 if decode else 2048
-    steps = args.steps or (400 if decode else 50)
-    warmup = args.warmup if args.warmup is not None else (40 if decode else 5)
-    n_banks = 16 if decode else 2
-    log(f"workload={args.workload} T={T} banks={n_banks} steps={steps} warmup={warmup}")
-
+def measure_resident(api, torch, dm, T, steps, warmup, n_banks, keep_first_weights=False):
+    """Time T-token layer calls over n_banks fully resident expert banks
+    (rotated call by call) and the dominant kernel of a separate profiled
+    pass.  Returns a dict (and bank-0 weights when asked, for the oracle)."""
     gen = torch.Generator(device="cuda").manual_seed(7)
     wr = (torch.randn((N_EXPERTS, D_MODEL), dtype=torch.bfloat16, device="cuda", generator=gen) * 0.02)
     h = torch.randn((T, D_MODEL), dtype=torch.bfloat16, device="cuda", generator=gen)
     y = torch.empty_like(h)
     ws = torch.empty(api.workspace_bytes(dm, T), dtype=torch.uint8, device="cuda")
-
     banks, caches, keep_weights = [], [], None
     for b in range(n_banks):
         bank, cache, weights = make_bank(api, dm, torch, 1000 + b)
         banks.append(bank)
         caches.append(cache)
-        if b == 0 and not args.no_cpu_baseline:
+        if b == 0 and keep_first_weights:
             keep_weights = tuple(w.view(torch.int16).cpu().numpy().view(np.uint16) for w in weights)
         del weights
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
-    log("banks ready")
+    log(f"T={T}: {n_banks} banks ready")
 
     # routing of this workload (identical across banks: same h and router)
     api.moe_forward(caches[0], h, wr, y, ws)
@@ -238,7 +230,7 @@ def bench_layer(args):
     t1.record()
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
-    log(f"timed {steps} steps: {ms * 1e3:.2f} us/step")
+    log(f"T={T}: timed {steps} steps: {ms * 1e3:.2f} us/step")
 
     # per-kernel durations with HIP events on the launch stream (separate pass)
     api.profile_begin(8 * steps)
@@ -259,7 +251,7 @@ def bench_layer(args):
         k_flops = P * 2 * D_FF * D_MODEL
     else:
         k_bytes, k_flops = alg_bytes, flops
-    if decode or "gemv" in dominant:
+    if T <= 4 or "gemv" in dominant:
         ach = k_bytes / dur_s / 1e9
         roof = dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s", frac=ach / HBM_PEAK_GBS,
                     traffic=measured_traffic(dominant), kernel=dominant,
@@ -269,6 +261,34 @@ def bench_layer(args):
         roof = dict(bound="mfma", achieved=ach, peak=BF16_PEAK_TFLOPS, unit="TFLOP/s",
                     frac=ach / BF16_PEAK_TFLOPS, traffic=measured_traffic(dominant), kernel=dominant,
                     alg_flops_per_launch=k_flops, alg_bytes_per_launch=k_bytes)
+    return dict(ms=ms, kern=kern, roofline=roof, n_distinct=n_distinct, alg_bytes=alg_bytes,
+                flops=flops, caches=caches, banks=banks, h=h, wr=wr, y=y, ws=ws,
+                keep_weights=keep_weights, run=run)
+
+
+def timeouts_of(caches):
+    """Bounded device waits of the fused decode launch that gave up (must be 0)."""
+    return int(sum(c.sync_timeouts() for c in caches))
+
+
+def bench_layer(args):
+    import torch
+    from paper_2608_15383_amd import api
+
+    torch.cuda.init()
+    dm = api.dims(D_MODEL, D_FF, N_EXPERTS, TOP_K)
+    decode = args.workload == "decode"
+    T = 1 if decode else 2048
+    steps = args.steps or (400 if decode else 50)
+    warmup = args.warmup if args.warmup is not None else (40 if decode else 5)
+    n_banks = 16 if decode else 2
+    log(f"workload={args.workload} T={T} banks={n_banks} steps={steps} warmup={warmup}")
+    m = measure_resident(api, torch, dm, T, steps, warmup, n_banks,
+                         keep_first_weights=not args.no_cpu_baseline)
+    ms, kern, roof = m["ms"], m["kern"], m["roofline"]
+    caches, h, wr, y, ws = m["caches"], m["h"], m["wr"], m["y"], m["ws"]
+    alg_bytes, flops, n_distinct = m["alg_bytes"], m["flops"], m["n_distinct"]
+    P = T * TOP_K
 
     sec = ms * 1e-3
     if decode:
@@ -294,6 +314,9 @@ def bench_layer(args):
         out["graph_replay"] = dict(us_per_call=us, gbs=alg_bytes / (us * 1e-6) / 1e9,
                                    calls_per_graph=n_banks, equals_eager=same)
         log(f"graph replay: {us:.2f} us per call, equal to eager: {same}")
+    # Every bounded wait of the fused decode launch must have been met: a
+    # timeout would mean some call's output is invalid (it is written as NaN).
+    out["sync_timeouts"] = timeouts_of(caches)
 
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
@@ -304,7 +327,7 @@ def bench_layer(args):
         wr_np = wr.view(torch.int16).cpu().numpy().view(np.uint16)
         if not decode:
             h_np = h_np[:8]            # bounded sample: 8 of the 2048 tokens
-        yref, cpu = oracle_baseline(keep_weights, wr_np, h_np, TOP_K,
+        yref, cpu = oracle_baseline(m["keep_weights"], wr_np, h_np, TOP_K,
                                     alg_bytes if decode else None,
                                     8 * TOP_K * (flops // P), unit)
         from paper_2608_15383_amd.inputs import bf16_bits_to_f32
@@ -313,7 +336,30 @@ def bench_layer(args):
         if not decode:
             cpu["sample"] += "; 8 tokens of the 2048-token batch"
         out["cpu_baseline"] = cpu
+    del m, caches
+    if decode and not args.no_prefill:
+        out["prefill"] = prefill_record(api, torch, dm)
+    if out["sync_timeouts"]:
+        print(json.dumps(out), file=sys.stderr, flush=True)
+        sys.exit(f"{out['sync_timeouts']} bounded device waits gave up: results invalid")
     print(json.dumps(out), flush=True)
+
+
+def prefill_record(api, torch, dm, steps=20, warmup=3):
+    """The prefill half of the metric (2048 tokens, every expert resident):
+    per-call time, expert TFLOP/s and the dominant MFMA kernel's roofline."""
+    torch.cuda.empty_cache()
+    m = measure_resident(api, torch, dm, 2048, steps, warmup, 2)
+    sec = m["ms"] * 1e-3
+    rec = dict(workload="olmoe_prefill", tokens=2048, steps=steps, warmup=warmup,
+               us_per_call=m["ms"] * 1e3, tflops=m["flops"] / sec / 1e12,
+               frac_of_bf16_peak=m["flops"] / sec / 1e12 / BF16_PEAK_TFLOPS,
+               tokens_per_s=2048 / sec, flops_per_call=m["flops"], roofline=m["roofline"],
+               kernels=m["kern"])
+    log(f"prefill: {rec['us_per_call']:.1f} us per call, {rec['tflops']:.0f} TFLOP/s")
+    del m
+    torch.cuda.empty_cache()
+    return rec
 
 
 def quantized_host_bank(api, dm, torch, seeds):
@@ -415,21 +461,27 @@ def bench_multiwave(args):
     ws = torch.empty(api.workspace_bytes(dm, T), dtype=torch.uint8, device="cuda")
     log(f"multiwave: host bank ready, pinned H2D {h2d_gbs:.1f} GB/s")
 
-    def one_call(z, state, sequential):
+    def one_call(z, state, sequential, profiled):
+        """One call from a fresh cache in `state`: end-to-end seconds (host
+        clock, fills included) of an unprofiled call, or the summed kernel
+        seconds of a profiled one (dispatch-level events around each launch
+        would otherwise inflate the many-launch sequential path's wall time)."""
         cache = api.Cache(dm, C, slot_bank=slots, host_bank=host)
         if state == "warm":
             _, fills = cache.build_slot_map(list(range(C)))
             cache.fill_slots(fills)
         torch.cuda.synchronize()
         st = api.Stats()
-        api.profile_begin(4096)
+        if profiled:
+            api.profile_begin(4096)
         t0 = time.perf_counter()
         api.moe_forward(cache, h, None, y, ws, logits_override=z, stats=st, sequential=sequential)
         torch.cuda.synchronize()
-        e2e = time.perf_counter() - t0
-        prof = api.profile_end(4096)
+        sec = time.perf_counter() - t0
+        if profiled:
+            sec = sum(t for _, t in api.profile_end(4096)) * 1e-3
         cache.close()
-        return e2e, sum(t for _, t in prof) * 1e-3, st, y.clone()
+        return sec, st, y.clone()
 
     cases, outs = [], {}
     for D in (40, 48, 56, 64):
@@ -437,13 +489,14 @@ def bench_multiwave(args):
         for state in ("cold", "warm"):
             row = dict(distinct_experts=D, state=state)
             for name, seq in (("fused", False), ("sequential", True)):
-                one_call(z, state, seq)                      # warm-up of this case
+                one_call(z, state, seq, False)               # warm-up of this case
                 e2e, kern, k_sum = [], [], None
                 for _ in range(reps):
-                    a, b, st, yy = one_call(z, state, seq)
+                    a, st, yy = one_call(z, state, seq, False)
                     e2e.append(a)
-                    kern.append(b)
                     k_sum = st
+                for _ in range(reps):
+                    kern.append(one_call(z, state, seq, True)[0])
                 outs[(D, state, name)] = yy
                 row[name] = dict(e2e_ms=1e3 * float(np.median(e2e)), kernel_ms=1e3 * float(np.median(kern)),
                                  waves=int(k_sum.waves), hits=int(k_sum.hits), misses=int(k_sum.misses),

@@ -219,8 +219,14 @@ int32_t emoe_build_slot_map(emoe_cache* cache, const int32_t* wave_experts, int3
 
 /* Host-bank slot fill (Sec. 3.3): copy each listed record from the pinned host
  * bank to its slot with hipMemcpyAsync, alternating between the cache's two
- * copy streams, each copy first waiting for the slot's completion event;
- * `stream` is then made to wait for the copies.  No host synchronization. */
+ * copy streams, each copy first waiting for the slot's completion event (the
+ * end of the last wave that computed on the slot), so a slot is never
+ * overwritten before its preceding computation finishes; `stream` is then
+ * made to wait for the copies.  No host synchronization on success.
+ * On a HIP failure (EMOE_EHIP) the call waits for the copies it did enqueue
+ * and marks every listed slot empty (no expert maps to it, stamp -1), since
+ * its record can no longer be trusted; nothing has been made to wait on
+ * `stream`. */
 int32_t emoe_fill_slots(emoe_cache* cache, const int32_t* fill_expert, const int32_t* fill_slot,
                         int32_t n_fill, hipStream_t stream);
 
@@ -236,8 +242,12 @@ int32_t emoe_fill_slots(emoe_cache* cache, const int32_t* fill_expert, const int
  *   path: an emoe_path value.
  * With a fully resident cache (C = E after preload) the call never blocks the
  * host.  Otherwise it copies counts[E] to the host once (one batched expert-id
- * transfer) and synchronizes `stream` to plan the waves.  If a fill fails the
- * cache map is restored to its state before that wave.
+ * transfer) and synchronizes `stream` to plan the waves.  If a wave's fill
+ * fails the call returns EMOE_EHIP without writing y: the slots of that
+ * wave's fill list are left empty (see emoe_fill_slots) and every other slot
+ * keeps the expert, stamp and clock it had before the wave, so the next call
+ * refills what it needs and computes on correct records.  Waves enqueued
+ * before the failing one still complete on `stream`.
  * With full residency, the GEMV path, at most 4 tokens (and 32 pairs),
  * d_ff <= 4096 and tokens*d_model <= 16384 the whole layer runs as one fused
  * kernel launch with the same arithmetic (and bit-identical results).  Calls
@@ -262,6 +272,20 @@ int32_t emoe_moe_forward_sequential(emoe_cache* cache, int32_t tokens, const uin
                                     int32_t renormalize, int32_t path, uint16_t* y,
                                     void* workspace, size_t workspace_bytes,
                                     hipStream_t stream, emoe_stats* stats);
+
+/* ---------------------------------------------------------------- test hooks */
+/* Failure injection for tests of the fill error path (Sec. 3.3 slot reuse):
+ * after `copies` more slot copies have been enqueued by emoe_fill_slots (in
+ * any cache, process-wide), the next one fails on the host with
+ * hipErrorInvalidValue before it is enqueued; -1 disarms.  Nothing faults on
+ * the device. */
+int32_t emoe_test_fail_copy_after(int64_t copies);
+/* Race-window widening for tests of event-ordered slot reuse (Sec. 3.3):
+ * before each wave's projections, the layer calls on this cache enqueue a
+ * kernel on `stream` that spins for `microseconds` (0..1000; 0 = off) and
+ * exits, so a fill that did not wait for the slot's completion event would
+ * overwrite records still being read.  Off by default. */
+int32_t emoe_test_set_wave_delay(emoe_cache* cache, int32_t microseconds);
 
 /* ---------------------------------------------------------------- kernel timing */
 /* Kernels launched by the layer calls, as reported by emoe_profile_end. */

@@ -71,6 +71,8 @@ SIGNATURES = {
                                 C.POINTER(Stats)]),
     "emoe_moe_forward_sequential": (_i32, [_vp, _i32, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
                                            C.c_size_t, _vp, C.POINTER(Stats)]),
+    "emoe_test_fail_copy_after": (_i32, [C.c_int64]),
+    "emoe_test_set_wave_delay": (_i32, [_vp, _i32]),
     "emoe_profile_begin": (_i32, [_i32]),
     "emoe_profile_end": (_i32, [_vp, _vp, _i32, _i32p]),
 }

@@ -128,6 +128,10 @@ class Cache:
         check(lib().emoe_cache_sync_timeouts(self.handle, C.byref(n)))
         return n.value
 
+    def set_wave_delay(self, microseconds: int) -> None:
+        """emoe_test_set_wave_delay: spin before each wave's projections (test hook)."""
+        check(lib().emoe_test_set_wave_delay(self.handle, int(microseconds)))
+
     def plan_waves(self, counts) -> list[list[int]]:
         e = self.dims.n_experts
         cnt = np.ascontiguousarray(counts, np.int32)
@@ -170,6 +174,11 @@ def moe_forward_sequential(cache: Cache, h, w_router, y, workspace, **kw) -> Non
     moe_forward(cache, h, w_router, y, workspace, sequential=True, **kw)
 
 
+def test_fail_copy_after(copies: int) -> None:
+    """emoe_test_fail_copy_after: make the slot copy after `copies` more fail (-1 disarms)."""
+    check(lib().emoe_test_fail_copy_after(int(copies)))
+
+
 def profile_begin(max_kernels: int) -> None:
     """emoe_profile_begin: time each kernel the layer calls launch from this thread."""
     check(lib().emoe_profile_begin(max_kernels))
@@ -188,4 +197,4 @@ def profile_end(max_out: int = 1 << 16) -> list[tuple[str, float]]:
 __all__ = ["Dims", "Stats", "WsLayout", "ExactMoEError", "EMOE_PATH_AUTO", "EMOE_PATH_GEMV",
            "EMOE_PATH_MFMA", "dims", "check_dims", "expert_record_bytes", "workspace_layout",
            "workspace_bytes", "quantize_experts", "unpack_expert", "pack_expert", "route", "Cache",
-           "moe_forward", "moe_forward_sequential", "profile_begin", "profile_end", "lib"]
+           "moe_forward", "moe_forward_sequential", "test_fail_copy_after", "profile_begin", "profile_end", "lib"]

@@ -3,6 +3,7 @@
 // slot reuse (Sec. 3.3), wave planning and the per-wave execution loop of
 // Sec. 3.4, and the sequential per-expert comparison path.
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -112,9 +113,19 @@ struct emoe_cache {
   int32_t* counts_host = nullptr;   // pinned [E]: the batched expert-id transfer
   DecodeSync* sync = nullptr;       // device: hand-over data of the fused decode launches
   DecodeProgress prog;              // host: epoch of the last direct fused launch
+  int32_t wave_delay_us = 0;        // test hook: spin before each wave's projections
 };
 
 namespace {
+
+// Mark slot s empty: its record is no longer trusted, so no expert maps to it
+// and it is the first victim of the next miss.
+void vacate_slot(emoe_cache* c, int s) {
+  const int old = c->expert_of[s];
+  if (old >= 0 && c->slot_of[old] == s) c->slot_of[old] = -1;
+  c->expert_of[s] = -1;
+  c->stamp[s] = -1;
+}
 
 int32_t check_dims(const emoe_dims* d) {
   if (!d) return fail(EMOE_EINVAL, "dims is NULL");
@@ -170,6 +181,19 @@ int32_t range_flag_for_current_device(int32_t** out) {
   return EMOE_OK;
 }
 
+// Test hook emoe_test_fail_copy_after: number of slot copies that still
+// succeed before one fails (-1: none fails).  Process-wide.
+std::atomic<int64_t> g_copies_before_failure{-1};
+
+// True when the copy about to be enqueued must fail instead (consumes the hook).
+bool take_injected_copy_failure() {
+  int64_t left = g_copies_before_failure.load();
+  while (left >= 0) {
+    if (g_copies_before_failure.compare_exchange_weak(left, left - 1)) return left == 0;
+  }
+  return false;
+}
+
 void add_stats(emoe_stats* s, const emoe_stats& d) {
   if (!s) return;
   s->layer_calls += d.layer_calls;
@@ -180,6 +204,28 @@ void add_stats(emoe_stats* s, const emoe_stats& d) {
   s->grouped_gemm_calls += d.grouped_gemm_calls;
   s->seq_expert_calls += d.seq_expert_calls;
   s->kernel_launches += d.kernel_launches;
+}
+
+// Test hook: one wavefront that spins for `ticks` of the constant-rate wall
+// clock and exits.  Bounded twice: by the clock, and by a poll count that
+// covers the delay even if the clock stood still (each poll sleeps 512
+// shader clocks, at least 0.2 us).
+__global__ void delay_kernel(uint64_t ticks, uint64_t max_polls) {
+  const uint64_t t0 = wall_clock64();
+  for (uint64_t it = 0; it < max_polls; ++it) {
+    if (wall_clock64() - t0 >= ticks) break;
+    __builtin_amdgcn_s_sleep(8);
+  }
+}
+
+hipError_t launch_delay(int32_t us, hipStream_t stream) {
+  int dev = 0, khz = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+  if (e != hipSuccess) return e;
+  const uint64_t ticks = (uint64_t)us * (uint64_t)(khz > 0 ? khz : 100000) / 1000u;
+  hipLaunchKernelGGL(delay_kernel, dim3(1), dim3(64), 0, stream, ticks, (uint64_t)us * 5u + 64u);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -506,7 +552,8 @@ int32_t emoe_build_slot_map(emoe_cache* c, const int32_t* wave, int32_t n, int32
   if (!c || (n > 0 && !wave) || !slot_map || !n_fill) return fail(EMOE_EINVAL, "NULL argument");
   const int E = c->dims.n_experts, C = c->capacity;
   if (n < 0 || n > C) return fail(EMOE_ECAPACITY, "wave of %d experts exceeds capacity %d", n, C);
-  std::vector<char> seen(E, 0);
+  // Fixed-size scratch on the stack: the layer calls allocate nothing.
+  char seen[EMOE_MAX_EXPERTS] = {};
   for (int i = 0; i < n; ++i) {
     if (wave[i] < 0 || wave[i] >= E) return fail(EMOE_EINVAL, "expert %d out of range", wave[i]);
     if (seen[wave[i]]++) return fail(EMOE_EINVAL, "expert %d repeated in a wave", wave[i]);
@@ -520,7 +567,7 @@ int32_t emoe_build_slot_map(emoe_cache* c, const int32_t* wave, int32_t n, int32
   if (n > 0 && (!fill_expert || !fill_slot)) return fail(EMOE_EINVAL, "NULL fill list");
   emoe_stats d{};
   c->clock += 1;
-  std::vector<char> prot(C, 0);
+  char prot[EMOE_MAX_EXPERTS] = {};
   for (int i = 0; i < n; ++i) {
     const int s = c->slot_of[wave[i]];
     if (s >= 0) {
@@ -529,11 +576,9 @@ int32_t emoe_build_slot_map(emoe_cache* c, const int32_t* wave, int32_t n, int32
       c->stamp[s] = c->clock;
     }
   }
-  std::vector<int32_t> missing;
-  for (int i = 0; i < n; ++i)
-    if (c->slot_of[wave[i]] < 0) missing.push_back(wave[i]);
-  std::sort(missing.begin(), missing.end());
-  for (int e : missing) {
+  // Misses in ascending expert id: `seen` marks the wave's experts.
+  for (int e = 0; e < E; ++e) {
+    if (!seen[e] || c->slot_of[e] >= 0) continue;
     int victim = -1;
     for (int s = 0; s < C; ++s) {
       if (prot[s]) continue;
@@ -568,19 +613,37 @@ int32_t emoe_fill_slots(emoe_cache* c, const int32_t* fill_expert, const int32_t
     if (e < 0 || e >= c->dims.n_experts || s < 0 || s >= c->capacity)
       return fail(EMOE_EINVAL, "fill (%d -> %d) out of range", e, s);
   }
-  for (int i = 0; i < n_fill; ++i) {
+  hipError_t e_hip = hipSuccess;
+  const char* what = "";
+  for (int i = 0; i < n_fill && e_hip == hipSuccess; ++i) {
     const int e = fill_expert[i], s = fill_slot[i];
     hipStream_t cs = c->copy_stream[i % emoe_cache::kCopyStreams];
-    EMOE_HIP(hipStreamWaitEvent(cs, c->release[s], 0));
-    EMOE_HIP(hipMemcpyAsync(c->slot_bank + (int64_t)s * c->record_bytes,
-                            c->host_bank + (int64_t)e * c->record_bytes, c->record_bytes,
-                            hipMemcpyHostToDevice, cs));
+    e_hip = hipStreamWaitEvent(cs, c->release[s], 0);
+    what = "hipStreamWaitEvent(copy stream, slot release)";
+    if (e_hip == hipSuccess && take_injected_copy_failure()) {
+      e_hip = hipErrorInvalidValue;
+      what = "hipMemcpyAsync (failure injected by emoe_test_fail_copy_after)";
+    }
+    if (e_hip == hipSuccess) {
+      e_hip = hipMemcpyAsync(c->slot_bank + (int64_t)s * c->record_bytes,
+                             c->host_bank + (int64_t)e * c->record_bytes, c->record_bytes,
+                             hipMemcpyHostToDevice, cs);
+      what = "hipMemcpyAsync(slot <- host bank)";
+    }
   }
-  for (int j = 0; j < emoe_cache::kCopyStreams && j < n_fill; ++j) {
-    EMOE_HIP(hipEventRecord(c->ready[j], c->copy_stream[j]));
-    EMOE_HIP(hipStreamWaitEvent(stream, c->ready[j], 0));
+  for (int j = 0; j < emoe_cache::kCopyStreams && j < n_fill && e_hip == hipSuccess; ++j) {
+    e_hip = hipEventRecord(c->ready[j], c->copy_stream[j]);
+    if (e_hip == hipSuccess) e_hip = hipStreamWaitEvent(stream, c->ready[j], 0);
+    what = "hipEventRecord / hipStreamWaitEvent(fills ready)";
   }
-  return EMOE_OK;
+  if (e_hip == hipSuccess) return EMOE_OK;
+  // Some copies may have been enqueued and may (partly) have overwritten their
+  // slots, and `stream` does not wait for them.  Let them finish, then mark
+  // every listed slot empty, so that no later call takes a partly written
+  // slot for a resident expert and no later fill races an earlier one.
+  for (hipStream_t cs : c->copy_stream) (void)hipStreamSynchronize(cs);
+  for (int i = 0; i < n_fill; ++i) vacate_slot(c, fill_slot[i]);
+  return hip_fail(e_hip, what);
 }
 
 }  // extern "C"
@@ -598,10 +661,36 @@ void set_wave_chunks(WaveArg& wa, const int32_t* counts) {
   wa.chunk0[wa.n] = acc;
 }
 
+// Slot contents and recency before a wave, kept to undo the wave's map
+// update when its fills fail (fixed size: the layer calls allocate nothing).
 struct CacheSnapshot {
-  std::vector<int32_t> slot_of, expert_of;
-  std::vector<int64_t> stamp;
+  int32_t expert_of[EMOE_MAX_EXPERTS];
+  int64_t stamp[EMOE_MAX_EXPERTS];
   int64_t clock;
+  void take(const emoe_cache* c) {
+    std::copy(c->expert_of.begin(), c->expert_of.end(), expert_of);
+    std::copy(c->stamp.begin(), c->stamp.end(), stamp);
+    clock = c->clock;
+  }
+  // A failed wave: slots in its fill list were vacated by emoe_fill_slots
+  // (their records may be partly overwritten); every other slot gets back its
+  // expert and stamp, and the clock its value, as if the wave never ran.
+  void restore_except_filled(emoe_cache* c, const int32_t* fill_slot, int n_fill) const {
+    char filled[EMOE_MAX_EXPERTS] = {};
+    for (int i = 0; i < n_fill; ++i) filled[fill_slot[i]] = 1;
+    std::fill(c->slot_of.begin(), c->slot_of.end(), -1);
+    for (int s = 0; s < c->capacity; ++s) {
+      if (filled[s]) {
+        c->expert_of[s] = -1;
+        c->stamp[s] = -1;
+      } else {
+        c->expert_of[s] = expert_of[s];
+        c->stamp[s] = stamp[s];
+      }
+      if (c->expert_of[s] >= 0) c->slot_of[c->expert_of[s]] = s;
+    }
+    c->clock = clock;
+  }
 };
 
 int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t* w_router,
@@ -754,26 +843,29 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
     // One batched expert-id transfer per layer (Sec. 1), then the waves of Sec. 3.4.
     EMOE_HIP(hipMemcpyAsync(c->counts_host, counts, sizeof(int32_t) * E, hipMemcpyDeviceToHost, stream));
     EMOE_HIP(hipStreamSynchronize(stream));
-    std::vector<int32_t> wexp(E), woff(E + 1), smap(E), fexp(E), fslot(E);
+    int32_t wexp[EMOE_MAX_EXPERTS], woff[EMOE_MAX_EXPERTS + 1], smap[EMOE_MAX_EXPERTS];
+    int32_t fexp[EMOE_MAX_EXPERTS], fslot[EMOE_MAX_EXPERTS];
     int32_t n_waves = 0;
-    if ((st = emoe_plan_waves(c, c->counts_host, wexp.data(), woff.data(), &n_waves))) return st;
+    if ((st = emoe_plan_waves(c, c->counts_host, wexp, woff, &n_waves))) return st;
+    CacheSnapshot snap;
     for (int w = 0; w < n_waves; ++w) {
       const int n = woff[w + 1] - woff[w];
-      const int32_t* we = wexp.data() + woff[w];
-      CacheSnapshot snap{c->slot_of, c->expert_of, c->stamp, c->clock};
+      const int32_t* we = wexp + woff[w];
+      snap.take(c);
       emoe_stats wstats{};
       int32_t n_fill = 0;
-      if ((st = emoe_build_slot_map(c, we, n, smap.data(), fexp.data(), fslot.data(), &n_fill, &wstats)))
-        return st;
+      if ((st = emoe_build_slot_map(c, we, n, smap, fexp, fslot, &n_fill, &wstats))) return st;
       if (!c->resident_all) {
-        st = emoe_fill_slots(c, fexp.data(), fslot.data(), n_fill, stream);
+        st = emoe_fill_slots(c, fexp, fslot, n_fill, stream);
         if (st) {
-          c->slot_of = snap.slot_of;
-          c->expert_of = snap.expert_of;
-          c->stamp = snap.stamp;
-          c->clock = snap.clock;
+          snap.restore_except_filled(c, fslot, n_fill);
           return st;
         }
+      }
+      if (c->wave_delay_us > 0) {
+        // Test hook: hold the wave's projections back (bounded spin on `stream`).
+        EMOE_HIP(launch_delay(c->wave_delay_us, stream));
+        ds.kernel_launches += 1;
       }
       ds.hits += wstats.hits;
       ds.misses += wstats.misses;
@@ -829,6 +921,20 @@ int32_t emoe_moe_forward_sequential(emoe_cache* cache, int32_t tokens, const uin
                                     hipStream_t stream, emoe_stats* stats) {
   return forward_impl(cache, tokens, h, w_router, logits_override, renormalize, path, y, workspace,
                       workspace_bytes, stream, stats, true);
+}
+
+int32_t emoe_test_fail_copy_after(int64_t copies) {
+  if (copies < -1) return fail(EMOE_EINVAL, "copies=%lld < -1", (long long)copies);
+  g_copies_before_failure.store(copies);
+  return EMOE_OK;
+}
+
+int32_t emoe_test_set_wave_delay(emoe_cache* c, int32_t microseconds) {
+  if (!c) return fail(EMOE_EINVAL, "cache is NULL");
+  if (microseconds < 0 || microseconds > 1000)
+    return fail(EMOE_EINVAL, "wave delay %d us outside [0, 1000]", microseconds);
+  c->wave_delay_us = microseconds;
+  return EMOE_OK;
 }
 
 int32_t emoe_profile_begin(int32_t max_kernels) {

@@ -45,12 +45,13 @@ constexpr int kPollSleep = 8;  // s_sleep units (64 clocks) between polls
 // Stage the activation row of pair pi from the tagged words (DecodeSync::act)
 // in LDS at dst (f bf16), reading it until every word carries this launch's
 // epoch (bounded); one wavefront.
-__device__ __forceinline__ void wave_stage_act_row(DecodeSync* sy, const DecodeArgs& a,
+__device__ __forceinline__ bool wave_stage_act_row(DecodeSync* sy, const DecodeArgs& a,
                                                    uint32_t epoch, int pi, uint32_t* dst) {
   constexpr int kWords = 8;  // words per lane per read
   const int lane = lane_id();
   const int nw = a.f / 2;  // words per row, a multiple of 64
   const uint64_t* src = sy->act + (int64_t)pi * nw;
+  bool timed_out = false;
   for (int w0 = 0; w0 < nw; w0 += 64 * kWords) {
     uint32_t it = 0;
     while (true) {
@@ -71,17 +72,19 @@ __device__ __forceinline__ void wave_stage_act_row(DecodeSync* sy, const DecodeA
       if (__all(ok)) break;
       if (++it > kSpinLimit) {
         if (lane == 0) atomicAdd(&sy->timeouts, 1u);
+        timed_out = true;
         break;
       }
       __builtin_amdgcn_s_sleep(kPollSleep);
     }
   }
+  return timed_out;
 }
 
 // Token t's logits into st.v: from logits_override, or from the router
 // items' tagged words (replica `replica`), read until every word carries this
 // launch's epoch (bounded).
-__device__ __forceinline__ void load_logits(DecodeSync* sy, const DecodeArgs& a, uint32_t epoch,
+__device__ __forceinline__ bool load_logits(DecodeSync* sy, const DecodeArgs& a, uint32_t epoch,
                                             int replica, int t, TopkState& st) {
   const int lane = lane_id();
   const int E = a.n_experts;
@@ -91,7 +94,7 @@ __device__ __forceinline__ void load_logits(DecodeSync* sy, const DecodeArgs& a,
       const int e = lane + 64 * c;
       st.v[c] = e < E ? a.logits_override[(int64_t)t * E + e] : 0.f;
     }
-    return;
+    return false;
   }
   const uint64_t* zt = sy->logits[replica] + t * E;
   uint32_t it = 0;
@@ -108,10 +111,10 @@ __device__ __forceinline__ void load_logits(DecodeSync* sy, const DecodeArgs& a,
         st.v[c] = 0.f;
       }
     }
-    if (__all(ok)) break;
+    if (__all(ok)) return false;
     if (++it > kSpinLimit) {
       if (lane == 0) atomicAdd(&sy->timeouts, 1u);
-      break;
+      return true;
     }
     __builtin_amdgcn_s_sleep(kPollSleep);
   }
@@ -188,6 +191,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   __shared__ float s_xs[kGemvWaves][kFusedActLdsBytes / (2 * kGroup * kGemvWaves) * 4];  // [wave][group][quarter]
   __shared__ uint64_t s_topk[kFusedMaxTokens][64];                // top-k scratch per token
   __shared__ int s_rank[kGemvWaves][64];                          // partial ranks (one token)
+  __shared__ int s_late[2][kGemvWaves];  // per wavefront: a bounded wait gave up (route, down)
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -245,11 +249,12 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   // wavefront t < T ranks token t alone.
   const int replica = blk % kSyncLanes;
   TopkState st;
+  bool late = false;  // a bounded wait of this wavefront gave up
   if (a.tokens == 1 && a.n_experts <= 64) {
     static_assert(kGemvWaves * 16 == 64, "a quarter of 64 keys per wavefront");
     uint64_t* keys = s_topk[1];
     if (wi == 0) {
-      load_logits(sy, a, epoch, replica, 0, st);
+      late = load_logits(sy, a, epoch, replica, 0, st);
       keys[lane] = topk_lane_key(st, a.n_experts);
     }
     __syncthreads();
@@ -263,12 +268,16 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
       wave_topk_store_ids<false>(st, a.top_k, s_ids);
     }
   } else if (wi < a.tokens) {
-    load_logits(sy, a, epoch, replica, wi, st);
+    late = load_logits(sy, a, epoch, replica, wi, st);
     wave_topk_select_loaded(a.n_experts, a.top_k, st, s_topk[wi]);
     wave_topk_store_ids<false>(st, a.top_k, s_ids + wi * a.top_k);
   }
   if (is_gate) wait_memory();  // the staged rows
+  if (lane == 0) s_late[0][wi] = late;
   __syncthreads();
+  // Logits that never arrived leave this workgroup's selection invalid: its
+  // outputs become NaN rather than passing as valid results.
+  const bool route_late = s_late[0][0] | s_late[0][1] | s_late[0][2] | s_late[0][3];
   // A read epoch has been waited for by now (the logits' tags): from here on
   // a scalar.  Down workgroups record it before their first tile loads, so
   // that no later wait covers the store; gate/up workgroups at their end.
@@ -291,12 +300,13 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     // down workgroups poll directly: the store is the signal.
     const int d = a.d, f = a.f;
     const uint64_t tag = (uint64_t)ep << 32;
+    const uint32_t nan_mask = route_late ? 0x7fc07fc0u : 0u;  // bf16 NaN pair
     uint64_t* act_tag = sy->act;
     for (int b = b0; b < b1; ++b)
       gateup_rows(gush, a.d, a.f, [=](int s) { return h_lds + (s / top_k) * d; }, pi, pi + 1,
                   a.slot_bank + (int64_t)e * a.record_bytes, b, [=](int s, int n, uint32_t v) {
-                    __hip_atomic_store(act_tag + ((s * f + n) >> 1), tag | v, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(act_tag + ((s * f + n) >> 1), tag | v | nan_mask,
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                   });
     if (kDevEpoch && tid == 0) arrive(sy, ep, blk);
     return;
@@ -359,8 +369,9 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   // Pair by pair as each activation row arrives (its first two pairs'
   // tiles are prefetched), so computing one pair overlaps the wait for the
   // next.
+  bool act_late = false;
   auto stage = [&](int pi) {
-    wave_stage_act_row(sy, a, ep, pi, act_lds32);
+    act_late |= wave_stage_act_row(sy, a, ep, pi, act_lds32);
     xs_sums(pi, 0, G);
   };
   if (wi < P) {
@@ -375,13 +386,16 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     stage(pi);
     pair_output(pi, pre0, false);
   }
+  if (lane == 0) s_late[1][wi] = act_late;
   __syncthreads();
   if (tid < 16 * a.tokens) {
     const int t = tid >> 4, n = tid & 15;
     float acc = 0.f;
     for (int j = 0; j < a.top_k; ++j)
       acc = fmaf(s_w[t * a.top_k + j], o_lds[t * a.top_k + j][n], acc);
-    a.y[(int64_t)t * a.d + 16 * rb + n] = (uint16_t)f32_to_bf16_rne(acc);
+    const bool late_any =
+        route_late | s_late[1][0] | s_late[1][1] | s_late[1][2] | s_late[1][3];
+    a.y[(int64_t)t * a.d + 16 * rb + n] = late_any ? 0x7fc0 : (uint16_t)f32_to_bf16_rne(acc);
   }
 
   if (rb == 0) {

@@ -50,6 +50,17 @@ class LazyExperts:
         return self.cache[e]
 
 
+def dims_of(shape) -> api.Dims:
+    return api.dims(shape.d_model, shape.d_ff, shape.n_experts, shape.top_k)
+
+
+def assert_close_rel(y, ref, label=""):
+    """max|y - ref| <= TOL * max|ref| (prints both error measures)."""
+    mx, mean = rel_err(y, ref)
+    print(f"{label}: max|err|/max|ref| = {mx:.3e}, mean rel = {mean:.3e}", flush=True)
+    assert mx <= TOL, (label, mx)
+
+
 def rel_err(y: np.ndarray, ref: np.ndarray):
     """(max|err| / max|ref|, mean|err| / mean|ref|)."""
     err = np.abs(y.astype(np.float64) - ref)

@@ -319,7 +319,7 @@ def _host_bank(layer):
     return host
 
 
-@pytest.mark.parametrize("distinct", [40, 48, 64])
+@pytest.mark.parametrize("distinct", [40, 48, 56, 64])
 def test_multi_wave_equals_single_wave(olmoe, distinct):
     """16 tokens touching `distinct` experts through a 16-slot cache (3-4 waves)."""
     lay, layer, experts = olmoe
@@ -443,6 +443,24 @@ def test_prefill_full_size_sampled(olmoe):
     toks = [0, 1000, 2047]
     ref = O.moe_forward(lay.f32("h"), experts, r, tokens=toks)
     assert_close(y[toks], ref, "prefill tokens")
+    experts.cache.clear()
+
+
+def test_prefill_full_size_whole_expert_and_every_row(olmoe):
+    """T = 2048 at full size: every pair of the busiest expert (all of its
+    64-row tiles, the ragged last one included) against the oracle, and all
+    2048 output rows against the GEMV path's."""
+    lay, layer, experts = olmoe
+    y = layer.forward(lay.h, path=MFMA)
+    r = O.route(lay.f32("h"), lay.f32("w_router"), 8)
+    gr = O.group_by_expert(r.ids, 64)
+    e = int(np.argmax(gr.counts))
+    seg = gr.sorted_pairs[gr.offsets[e]:gr.offsets[e + 1]]
+    assert len(seg) > 4 * 64
+    po = layer.pair_out(16384, mfma=True)
+    assert_close(po[seg], O.pair_outputs(lay.f32("h"), experts, r, seg), f"all pairs of expert {e}")
+    y_g = layer.forward(lay.h, path=GEMV)
+    assert_close(y, y_g.astype(np.float64), "T=2048 MFMA vs GEMV, every row")
     experts.cache.clear()
 
 
