@@ -273,6 +273,27 @@ int32_t emoe_moe_forward_sequential(emoe_cache* cache, int32_t tokens, const uin
                                     void* workspace, size_t workspace_bytes,
                                     hipStream_t stream, emoe_stats* stats);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * layer call as emoe_moe_forward, with the workspace taken from a fixed
+ * device array inside the library instead of a caller buffer.  The call
+ * allocates nothing (no hipMalloc, hipFree or other allocating routine, no
+ * host heap).  The array holds EMOE_NOALLOC_SCRATCH_BYTES on every GPU the
+ * library runs on, until the process ends; a call whose
+ * emoe_workspace_bytes(dims, tokens) exceeds it fails with EMOE_EINVAL before
+ * anything is enqueued (about 400 tokens at d_model 2048, d_ff 1024, 64
+ * experts, top-8).  Nothing in the array needs to start at zero: every call
+ * writes each part it reads.  All calls on one GPU share that GPU's array and
+ * it keeps the last call's contents, so calls that overlap in time on one GPU
+ * (any cache, any stream) race; order them.  The cache must have a slot bank
+ * (its creation looks up the array's device address).  Results equal
+ * emoe_moe_forward's bit for bit. */
+#define EMOE_NOALLOC_SCRATCH_BYTES (32u << 20)
+int32_t emoe_moe_forward_noalloc(emoe_cache* cache, int32_t tokens, const uint16_t* h,
+                                 const uint16_t* w_router, const float* logits_override,
+                                 int32_t renormalize, int32_t path, uint16_t* y,
+                                 hipStream_t stream, emoe_stats* stats);
+
 /* ---------------------------------------------------------------- test hooks */
 /* Failure injection for tests of the fill error path (Sec. 3.3 slot reuse):
  * after `copies` more slot copies have been enqueued by emoe_fill_slots (in

@@ -17,6 +17,7 @@ EMOE_GROUP = 128
 EMOE_MAX_EXPERTS = 256
 EMOE_PATH_AUTO, EMOE_PATH_GEMV, EMOE_PATH_MFMA = 0, 1, 2
 EMOE_MFMA_MIN_PAIRS_PER_EXPERT = 32
+EMOE_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 class Dims(C.Structure):
@@ -71,6 +72,8 @@ SIGNATURES = {
                                 C.POINTER(Stats)]),
     "emoe_moe_forward_sequential": (_i32, [_vp, _i32, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
                                            C.c_size_t, _vp, C.POINTER(Stats)]),
+    "emoe_moe_forward_noalloc": (_i32, [_vp, _i32, _vp, _vp, _vp, _i32, _i32, _vp, _vp,
+                                        C.POINTER(Stats)]),
     "emoe_test_fail_copy_after": (_i32, [C.c_int64]),
     "emoe_test_set_wave_delay": (_i32, [_vp, _i32]),
     "emoe_profile_begin": (_i32, [_i32]),

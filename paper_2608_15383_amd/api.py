@@ -170,6 +170,16 @@ def moe_forward(cache: Cache, h, w_router, y, workspace, logits_override=None,
              C.byref(stats) if stats is not None else None))
 
 
+def moe_forward_noalloc(cache: Cache, h, w_router, y, logits_override=None,
+                        renormalize: bool = True, path: int = EMOE_PATH_AUTO,
+                        stats: Stats | None = None, stream=None) -> None:
+    """emoe_moe_forward_noalloc: the layer call with the library's own scratch workspace."""
+    check(lib().emoe_moe_forward_noalloc(cache.handle, h.shape[0], _ptr(h), _ptr(w_router),
+                                         _ptr(logits_override), int(bool(renormalize)), path,
+                                         _ptr(y), _stream(stream),
+                                         C.byref(stats) if stats is not None else None))
+
+
 def moe_forward_sequential(cache: Cache, h, w_router, y, workspace, **kw) -> None:
     moe_forward(cache, h, w_router, y, workspace, sequential=True, **kw)
 
@@ -197,4 +207,4 @@ def profile_end(max_out: int = 1 << 16) -> list[tuple[str, float]]:
 __all__ = ["Dims", "Stats", "WsLayout", "ExactMoEError", "EMOE_PATH_AUTO", "EMOE_PATH_GEMV",
            "EMOE_PATH_MFMA", "dims", "check_dims", "expert_record_bytes", "workspace_layout",
            "workspace_bytes", "quantize_experts", "unpack_expert", "pack_expert", "route", "Cache",
-           "moe_forward", "moe_forward_sequential", "test_fail_copy_after", "profile_begin", "profile_end", "lib"]
+           "moe_forward", "moe_forward_noalloc", "moe_forward_sequential", "test_fail_copy_after", "profile_begin", "profile_end", "lib"]

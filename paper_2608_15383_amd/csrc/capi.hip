@@ -114,9 +114,34 @@ struct emoe_cache {
   DecodeSync* sync = nullptr;       // device: hand-over data of the fused decode launches
   DecodeProgress prog;              // host: epoch of the last direct fused launch
   int32_t wave_delay_us = 0;        // test hook: spin before each wave's projections
+  void* scratch = nullptr;          // device address of this device's no-alloc workspace
 };
 
+// Workspace of emoe_moe_forward_noalloc: one fixed array per device, held
+// until the process ends.  Host code never passes `scratch` itself (on the
+// host it is only a stand-in for the symbol); it uses the device address that
+// hipGetSymbolAddress returns for the current device, looked up once per
+// device at set-up (emoe_cache_create) and kept in g_scratch_addr.
+static __device__ __align__(256) uint8_t scratch[EMOE_NOALLOC_SCRATCH_BYTES];
+
 namespace {
+
+std::mutex g_scratch_mu;
+void* g_scratch_addr[64] = {};
+
+// Device address of this device's scratch array (dev must be current).
+hipError_t scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return hipSuccess;
+}
 
 // Mark slot s empty: its record is no longer trusted, so no expert maps to it
 // and it is the first victim of the next miss.
@@ -458,6 +483,7 @@ int32_t emoe_cache_create(const emoe_dims* dims, int32_t capacity, void* slot_ba
     const uint32_t first_epoch = kDeviceEpoch0;  // returns once the zeroing is done, too
     if (e == hipSuccess)
       e = hipMemcpy(&c->sync->epoch, &first_epoch, sizeof first_epoch, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = scratch_address(c->device, &c->scratch);
     if (e == hipSuccess && host_bank) {
       for (int j = 0; j < emoe_cache::kCopyStreams && e == hipSuccess; ++j) {
         e = hipStreamCreateWithFlags(&c->copy_stream[j], hipStreamNonBlocking);
@@ -921,6 +947,23 @@ int32_t emoe_moe_forward_sequential(emoe_cache* cache, int32_t tokens, const uin
                                     hipStream_t stream, emoe_stats* stats) {
   return forward_impl(cache, tokens, h, w_router, logits_override, renormalize, path, y, workspace,
                       workspace_bytes, stream, stats, true);
+}
+
+int32_t emoe_moe_forward_noalloc(emoe_cache* cache, int32_t tokens, const uint16_t* h,
+                                 const uint16_t* w_router, const float* logits_override,
+                                 int32_t renormalize, int32_t path, uint16_t* y,
+                                 hipStream_t stream, emoe_stats* stats) {
+  if (!cache) return fail(EMOE_EINVAL, "cache is NULL");
+  if (!cache->slot_bank || !cache->scratch) return fail(EMOE_ESTATE, "no slot bank attached");
+  if (tokens < 0) return fail(EMOE_EINVAL, "tokens=%d < 0", tokens);
+  const size_t need = make_layout(cache->dims, tokens).total;
+  if (need > (size_t)EMOE_NOALLOC_SCRATCH_BYTES)
+    return fail(EMOE_EINVAL,
+                "%d tokens need %zu workspace bytes; the no-allocation call's scratch holds %zu "
+                "(use emoe_moe_forward with a caller workspace)",
+                tokens, need, (size_t)EMOE_NOALLOC_SCRATCH_BYTES);
+  return forward_impl(cache, tokens, h, w_router, logits_override, renormalize, path, y,
+                      cache->scratch, (size_t)EMOE_NOALLOC_SCRATCH_BYTES, stream, stats, false);
 }
 
 int32_t emoe_test_fail_copy_after(int64_t copies) {
