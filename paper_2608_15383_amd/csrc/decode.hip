@@ -209,18 +209,14 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     if (!a.logits_override) {
       const int e0 = 4 * blk + wi;
       if (e0 < a.n_experts) {
-        double s[kFusedMaxTokens][1];
-        wave_router_sums<kFusedMaxTokens, 1>(a.tokens, a.n_experts, a.d, 0, e0, a.h, a.w_router, s);
-#pragma unroll
-        for (int t = 0; t < kFusedMaxTokens; ++t) {
-          if (t >= a.tokens) break;
-          const uint32_t v = __float_as_uint((float)s[t][0]);
+        wave_router_dot(a.tokens, a.d, e0, a.h, a.w_router, [&](int t, double sum) {
+          const uint32_t v = __float_as_uint((float)sum);
           const int at = t * a.n_experts + e0;
           if (lane < kSyncLanes)
             __hip_atomic_store(&sy->logits[lane][at], ((uint64_t)epoch << 32) | v,
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           if (lane == kSyncLanes) st_u32<false>(a.logits + at, v);
-        }
+        });
       }
     }
     if (kDevEpoch) {

@@ -36,18 +36,27 @@ __device__ __forceinline__ uint32_t at_use(uint32_t v) {
   return v;
 }
 
+// Mask and magic are hidden from constant folding (the empty asm statements
+// emit nothing; identical ones are merged), mask in an SGPR and magic in a
+// VGPR, so each pair is one v_and_or_b32 (gfx9 VOP3 takes no literal).
 __device__ __forceinline__ void dequant_dword(uint32_t dw, uint32_t* out) {
+  uint32_t mask = 0x000f000fu, magic = 0x43004300u;
+  asm("" : "+s"(mask));
+  asm("" : "+v"(magic));
 #pragma unroll
-  for (int p = 0; p < 4; ++p) out[p] = ((dw >> (4 * p)) & 0x000f000fu) | 0x43004300u;
+  for (int p = 0; p < 4; ++p) out[p] = ((dw >> (4 * p)) & mask) | magic;
 }
 
 // Dot product of one lane's 32 codes of a group (its row, its inputs) with the
 // 32 matching activations x (4 x uint4): returns sum (128 + u) x and, when
-// want_xs, adds sum x to xs.
+// want_xs, adds sum x to xs.  Four independent accumulators (one per code
+// dword) and two for sum x keep the dependent chains short; the partial sums
+// are added in a fixed order, so every caller gets the same bits.
 __device__ __forceinline__ float lane_group_dot(const uint4 codes, const uint4* x, float& xs,
                                                 bool want_xs) {
   const uint32_t c[4] = {codes.x, codes.y, codes.z, codes.w};
-  float acc = 0.f;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  float xsum[2] = {0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     uint32_t wp[4];
@@ -55,11 +64,12 @@ __device__ __forceinline__ float lane_group_dot(const uint4 codes, const uint4* 
     const uint32_t xv[4] = {x[i].x, x[i].y, x[i].z, x[i].w};
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
-      acc = dot2(wp[p], xv[p], acc);
-      if (want_xs) xs = dot2(kOnesBf16x2, xv[p], xs);
+      acc[i] = dot2(wp[p], xv[p], acc[i]);
+      if (want_xs) xsum[i & 1] = dot2(kOnesBf16x2, xv[p], xsum[i & 1]);
     }
   }
-  return acc;
+  if (want_xs) xs += xsum[0] + xsum[1];
+  return (acc[0] + acc[1]) + (acc[2] + acc[3]);
 }
 
 __device__ __forceinline__ void load_x32(const uint16_t* row, uint4* x) {
@@ -142,20 +152,30 @@ __device__ __forceinline__ void gateup_rows(GateUpShared& sh, int d, int f, XRow
           sgu[j] = scales[scale_index(gate_n, g, G) >> 1];
         }
       }
+      // Row by row over the batch's groups (each row's sum still runs in
+      // group order), the next group's activations read while this one's
+      // are used, so their load latency is not paid group after group.
 #pragma unroll
-      for (int j = 0; j < kGateBatch; ++j) {
-        const int g = g0 + kGemvWaves * j;
-        if (g >= G) break;
+      for (int m = 0; m < kTokChunk; ++m) {
+        if (m >= mc) break;
+        uint4 xc[4];
+        load_x32(xrow[m] + g0 * kGroup, xc);
 #pragma unroll
-        for (int m = 0; m < kTokChunk; ++m) {
-          if (m >= mc) break;
-          uint4 x[4];
-          load_x32(xrow[m] + g * kGroup, x);
+        for (int j = 0; j < kGateBatch; ++j) {
+          const int g = g0 + kGemvWaves * j;
+          if (g >= G) break;
+          const bool more = j + 1 < kGateBatch && g + kGemvWaves < G;
+          uint4 xn[4];
+          if (more) load_x32(xrow[m] + (g + kGemvWaves) * kGroup, xn);
           float xs = 0.f;
-          const float pg = lane_group_dot(cg[j], x, xs, true);
-          const float pu = lane_group_dot(cu[j], x, xs, false);
+          const float pg = lane_group_dot(cg[j], xc, xs, true);
+          const float pu = lane_group_dot(cu[j], xc, xs, false);
           accg[m] = fmaf(half_bits_to_f32(sgu[j] & 0xffffu), fmaf(-136.f, xs, pg), accg[m]);
           accu[m] = fmaf(half_bits_to_f32(sgu[j] >> 16), fmaf(-136.f, xs, pu), accu[m]);
+          if (more) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) xc[i] = xn[i];
+          }
         }
       }
     }
@@ -211,26 +231,42 @@ __device__ __forceinline__ void down_load_batch(const uint8_t* __restrict__ rec,
   }
 }
 
+// This lane's 32 activations of group g of row m (4 x uint4) through xload.
+template <typename XLoad>
+__device__ __forceinline__ void load_x_group(XLoad xload, int m, int g, uint4* x) {
+  const int quarter = lane_id() >> 4;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) x[i] = xload(m, g * kGroup + 8 * quarter + 32 * i);
+}
+
 // acc[m] += contribution of the loaded batch to activation rows m < mc;
-// xload(m, k) returns the 8 bf16 activations k .. k+7 of row m.
+// xload(m, k) returns the 8 bf16 activations k .. k+7 of row m.  Row by row,
+// groups in order; the next group's activations are read while this one's
+// are used.
 template <typename XLoad>
 __device__ __forceinline__ void down_apply_batch(const DownBatch& bt, int f, int g0, XLoad xload,
                                                  int mc, float* acc) {
-  const int quarter = lane_id() >> 4;
   const int G = f / kGroup;
+  if (g0 >= G) return;
 #pragma unroll
-  for (int j = 0; j < kDownBatch; ++j) {
-    const int g = g0 + j;
-    if (g >= G) break;
+  for (int m = 0; m < kTokChunk; ++m) {
+    if (m >= mc) break;
+    uint4 xc[4];
+    load_x_group(xload, m, g0, xc);
 #pragma unroll
-    for (int m = 0; m < kTokChunk; ++m) {
-      if (m >= mc) break;
-      uint4 x[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) x[i] = xload(m, g * kGroup + 8 * quarter + 32 * i);
+    for (int j = 0; j < kDownBatch; ++j) {
+      const int g = g0 + j;
+      if (g >= G) break;
+      const bool more = j + 1 < kDownBatch && g + 1 < G;
+      uint4 xn[4];
+      if (more) load_x_group(xload, m, g + 1, xn);
       float xs = 0.f;
-      const float p = lane_group_dot(bt.c[j], x, xs, true);
+      const float p = lane_group_dot(bt.c[j], xc, xs, true);
       acc[m] = fmaf(half_bits_to_f32(at_use(bt.s[j])), fmaf(-136.f, xs, p), acc[m]);
+      if (more) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) xc[i] = xn[i];
+      }
     }
   }
 }
@@ -238,14 +274,14 @@ __device__ __forceinline__ void down_apply_batch(const DownBatch& bt, int f, int
 // Sum of the 32 activations x (4 x uint4) of one lane's inputs of a group, in
 // the order lane_group_dot accumulates it.
 __device__ __forceinline__ float lane_group_xsum(const uint4* x) {
-  float xs = 0.f;
+  float xsum[2] = {0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const uint32_t xv[4] = {x[i].x, x[i].y, x[i].z, x[i].w};
 #pragma unroll
-    for (int p = 0; p < 4; ++p) xs = dot2(kOnesBf16x2, xv[p], xs);
+    for (int p = 0; p < 4; ++p) xsum[i & 1] = dot2(kOnesBf16x2, xv[p], xsum[i & 1]);
   }
-  return xs;
+  return 0.f + (xsum[0] + xsum[1]);
 }
 
 // down_apply_batch with the activation sums precomputed: xsload(m, g) is
@@ -254,21 +290,35 @@ template <typename XLoad, typename XsLoad>
 __device__ __forceinline__ void down_apply_batch_xs(const DownBatch& bt, int f, int g0,
                                                     XLoad xload, XsLoad xsload, int mc,
                                                     float* acc) {
-  const int quarter = lane_id() >> 4;
   const int G = f / kGroup;
+  if (g0 >= G) return;
 #pragma unroll
-  for (int j = 0; j < kDownBatch; ++j) {
-    const int g = g0 + j;
-    if (g >= G) break;
+  for (int m = 0; m < kTokChunk; ++m) {
+    if (m >= mc) break;
+    uint4 xc[4];
+    load_x_group(xload, m, g0, xc);
 #pragma unroll
-    for (int m = 0; m < kTokChunk; ++m) {
-      if (m >= mc) break;
-      uint4 x[4];
+    for (int j = 0; j < kDownBatch; ++j) {
+      const int g = g0 + j;
+      if (g >= G) break;
+      // The first half of the next group's activations is read before this
+      // group's arithmetic, the second half after (register budget).
+      const bool more = j + 1 < kDownBatch && g + 1 < G;
+      const int quarter = lane_id() >> 4;
+      uint4 xn[2];
+      if (more) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) x[i] = xload(m, g * kGroup + 8 * quarter + 32 * i);
+        for (int i = 0; i < 2; ++i) xn[i] = xload(m, (g + 1) * kGroup + 8 * quarter + 32 * i);
+      }
       float unused = 0.f;
-      const float p = lane_group_dot(bt.c[j], x, unused, false);
+      const float p = lane_group_dot(bt.c[j], xc, unused, false);
       acc[m] = fmaf(half_bits_to_f32(at_use(bt.s[j])), fmaf(-136.f, xsload(m, g), p), acc[m]);
+      if (more) {
+        xc[0] = xn[0];
+        xc[1] = xn[1];
+#pragma unroll
+        for (int i = 2; i < 4; ++i) xc[i] = xload(m, (g + 1) * kGroup + 8 * quarter + 32 * i);
+      }
     }
   }
 }

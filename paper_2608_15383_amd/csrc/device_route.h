@@ -67,6 +67,69 @@ __device__ __forceinline__ void wave_router_sums(int tokens, int n_experts, int 
     for (int b = 0; b < NE; ++b) acc[a][b] = wave_sum_f64(acc[a][b]);
 }
 
+// Sum of a double over the wavefront with DPP lane moves (quad swaps, the
+// half-row and row mirrors, then the two row broadcasts), no LDS round trip;
+// the total is read from lane 63 and returned in every lane.  Lanes that a
+// move does not reach add 0.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ double dpp_add_f64(double v) {
+  const int lo = __double2loint(v), hi = __double2hiint(v);
+  const int lo2 = __builtin_amdgcn_update_dpp(0, lo, kCtrl, kRowMask, 0xF, false);
+  const int hi2 = __builtin_amdgcn_update_dpp(0, hi, kCtrl, kRowMask, 0xF, false);
+  return v + __hiloint2double(hi2, lo2);
+}
+
+__device__ __forceinline__ double wave_sum_f64_dpp(double v) {
+  v = dpp_add_f64<0xB1, 0xF>(v);   // quad_perm [1, 0, 3, 2]
+  v = dpp_add_f64<0x4E, 0xF>(v);   // quad_perm [2, 3, 0, 1]
+  v = dpp_add_f64<0x141, 0xF>(v);  // row_half_mirror
+  v = dpp_add_f64<0x140, 0xF>(v);  // row_mirror
+  v = dpp_add_f64<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+  v = dpp_add_f64<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
+  const int lo = __builtin_amdgcn_readlane(__double2loint(v), 63);
+  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), 63);
+  return __hiloint2double(hi, lo);
+}
+
+// Logit sums of expert e for each token by one wavefront, token after token,
+// with every load of a pass issued before any is used: lanes take 8-input
+// chunks k = 8*lane + 512*i, up to four chunks (2048 inputs) per pass, so a
+// token with d <= 2048 costs one memory round trip.  Chunks past d are read
+// at a clamped in-bounds address and contribute 0.  Products of bf16 values
+// are exact in fp64 and so, at these magnitudes, is the sum, whatever its
+// order.  store(t, sum) receives each token's sum (the same in every lane).
+template <typename Store>
+__device__ __forceinline__ void wave_router_dot(int tokens, int d, int e,
+                                                const uint16_t* __restrict__ h,
+                                                const uint16_t* __restrict__ wr, Store store) {
+  const int lane = lane_id();
+  const uint16_t* wrow = wr + (int64_t)e * d;
+  for (int t = 0; t < tokens; ++t) {
+    const uint16_t* hrow = h + (int64_t)t * d;
+    double acc = 0.0;
+    for (int base = 0; base < d; base += 512 * 4) {
+      uint4 w[4], x[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int k = base + 512 * i + 8 * lane;
+        const int kc = k < d ? k : d - 8;
+        w[i] = *reinterpret_cast<const uint4*>(wrow + kc);
+        x[i] = *reinterpret_cast<const uint4*>(hrow + kc);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = base + 512 * i + 8 * lane < d;
+        double wv[8], hv[8];
+        bf16x8_to_f64(w[i], wv);
+        bf16x8_to_f64(x[i], hv);
+#pragma unroll
+        for (int r = 0; r < 8; ++r) acc = fma(hv[r], ok ? wv[r] : 0.0, acc);
+      }
+    }
+    store(t, wave_sum_f64_dpp(acc));
+  }
+}
+
 template <int NT, int NE, bool kCo>
 __device__ __forceinline__ void wave_router_logits(int tokens, int n_experts, int d, int t0, int e0,
                                                    const uint16_t* __restrict__ h,
