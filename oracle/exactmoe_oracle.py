@@ -184,17 +184,30 @@ def group_by_expert(ids: np.ndarray, n_experts: int) -> Grouping:
 # --------------------------------------------------------------------------
 # Sec. 3.4: waves of at most C experts
 # --------------------------------------------------------------------------
-def plan_waves(active, resident, capacity: int):
+def plan_waves(active, resident, capacity: int, overlap: bool = False):
     """Partition the active expert set into waves of at most C experts.
 
     The paper fixes only the size bound.  Reading: experts already resident
     at layer entry come first (ascending id), then the others (ascending id),
     cut into consecutive chunks of C.  Returns a list of lists of expert ids.
+
+    overlap (a second reading, for filling slots while the previous wave
+    computes): Sec. 3.3 lets a slot be refilled once its preceding
+    computation has finished, so a wave whose misses all land in slots the
+    previous wave does not use can be filled while that wave computes.  When
+    the active set does not fit in the C slots at once, the chunks then hold
+    at most max(1, C // 2) experts; under the LRU rule of SlotCache the
+    previous wave's slots carry the newest stamps, so with at most C // 2
+    experts per wave every miss takes a slot outside the previous wave.  A set
+    that fits stays one wave of up to C.
     """
     resident = set(int(e) for e in resident)
     act = [int(e) for e in sorted(int(x) for x in active)]
     order = [e for e in act if e in resident] + [e for e in act if e not in resident]
-    return [order[i:i + capacity] for i in range(0, len(order), capacity)]
+    size = capacity
+    if overlap and len(order) > capacity:
+        size = max(1, capacity // 2)
+    return [order[i:i + size] for i in range(0, len(order), size)]
 
 
 # --------------------------------------------------------------------------

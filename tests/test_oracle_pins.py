@@ -248,6 +248,52 @@ def test_waves_partition_active_set():
         assert all(x in res for x in flat[:n_res])        # resident experts first
 
 
+def test_overlap_waves_partition_active_set():
+    """Overlap reading: a set that fits stays one wave; a larger one is cut into
+    the fewest chunks of at most max(1, C // 2), resident experts first."""
+    rng = np.random.default_rng(21)
+    for _ in range(200):
+        e = 64
+        c = int(rng.integers(1, 33))
+        active = np.sort(rng.choice(e, size=int(rng.integers(1, 65)), replace=False))
+        resident = rng.choice(e, size=int(rng.integers(0, c + 1)), replace=False)
+        waves = O.plan_waves(active, resident, c, overlap=True)
+        size = c if len(active) <= c else max(1, c // 2)
+        assert len(waves) == -(-len(active) // size)
+        flat = [x for w in waves for x in w]
+        assert flat == [x for w in O.plan_waves(active, resident, size) for x in w]
+        assert sorted(flat) == active.tolist() and len(flat) == len(set(flat))
+        assert all(1 <= len(w) <= size for w in waves)
+    assert O.plan_waves(range(10), [], 4, overlap=True) == [[0, 1], [2, 3], [4, 5], [6, 7], [8, 9]]
+    assert O.plan_waves(range(4), [], 4, overlap=True) == [[0, 1, 2, 3]]
+
+
+def _previous_wave_slots_refilled(capacity, calls, rng, overlap):
+    """Run random layer calls through a SlotCache; count fills that land in a
+    slot the call's previous wave used (such a fill must wait for that wave)."""
+    e = 64
+    cache = O.SlotCache(e, capacity)
+    clashes = 0
+    for _ in range(calls):
+        active = np.sort(rng.choice(e, size=int(rng.integers(1, e + 1)), replace=False))
+        prev_slots = set()
+        for w in O.plan_waves(active, cache.resident(), capacity, overlap=overlap):
+            sm, fills = cache.map_wave(w)
+            clashes += sum(1 for _, s in fills if s in prev_slots)
+            prev_slots = {sm[x] for x in w}
+    return clashes
+
+
+def test_overlap_waves_never_refill_the_previous_waves_slots():
+    """With overlap waves and C >= 2, no miss of a wave takes a slot that the
+    call's previous wave used, under the unchanged LRU rule; with full-size
+    waves such refills do occur (so the check has teeth)."""
+    rng = np.random.default_rng(22)
+    for c in (2, 3, 5, 8, 16, 32):
+        assert _previous_wave_slots_refilled(c, 60, rng, overlap=True) == 0, c
+    assert _previous_wave_slots_refilled(16, 20, rng, overlap=False) > 0
+
+
 # ---------------------------------------------------------------- LRU
 def _stack_distances(seq):
     """Mattson stack distance of each reference (inf for a first reference)."""
