@@ -461,7 +461,7 @@ def bench_multiwave(args):
     ws = torch.empty(api.workspace_bytes(dm, T), dtype=torch.uint8, device="cuda")
     log(f"multiwave: host bank ready, pinned H2D {h2d_gbs:.1f} GB/s")
 
-    def one_call(z, state, sequential, profiled):
+    def one_call(z, state, sequential, profiled, overlap=False):
         """One call from a fresh cache in `state`: end-to-end seconds (host
         clock, fills included) of an unprofiled call, or the summed kernel
         seconds of a profiled one (dispatch-level events around each launch
@@ -470,6 +470,7 @@ def bench_multiwave(args):
         if state == "warm":
             _, fills = cache.build_slot_map(list(range(C)))
             cache.fill_slots(fills)
+        cache.set_wave_overlap(overlap)
         torch.cuda.synchronize()
         st = api.Stats()
         if profiled:
@@ -488,15 +489,16 @@ def bench_multiwave(args):
         z = torch.from_numpy(spread_logits(T, N_EXPERTS, TOP_K, D, seed=2)).to("cuda")
         for state in ("cold", "warm"):
             row = dict(distinct_experts=D, state=state)
-            for name, seq in (("fused", False), ("sequential", True)):
-                one_call(z, state, seq, False)               # warm-up of this case
+            for name, seq, ov in (("fused", False, False), ("fused_overlap", False, True),
+                                  ("sequential", True, False)):
+                one_call(z, state, seq, False, ov)           # warm-up of this case
                 e2e, kern, k_sum = [], [], None
                 for _ in range(reps):
-                    a, st, yy = one_call(z, state, seq, False)
+                    a, st, yy = one_call(z, state, seq, False, ov)
                     e2e.append(a)
                     k_sum = st
                 for _ in range(reps):
-                    kern.append(one_call(z, state, seq, True)[0])
+                    kern.append(one_call(z, state, seq, True, ov)[0])
                 outs[(D, state, name)] = yy
                 row[name] = dict(e2e_ms=1e3 * float(np.median(e2e)), kernel_ms=1e3 * float(np.median(kern)),
                                  waves=int(k_sum.waves), hits=int(k_sum.hits), misses=int(k_sum.misses),
@@ -505,9 +507,13 @@ def bench_multiwave(args):
             row["speedup_kernels"] = row["sequential"]["kernel_ms"] / row["fused"]["kernel_ms"]
             row["fused_equals_sequential"] = bool(torch.equal(outs[(D, state, "fused")],
                                                               outs[(D, state, "sequential")]))
+            row["overlap_equals_fused"] = bool(torch.equal(outs[(D, state, "fused")],
+                                                           outs[(D, state, "fused_overlap")]))
+            row["overlap_speedup_e2e"] = row["fused"]["e2e_ms"] / row["fused_overlap"]["e2e_ms"]
             cases.append(row)
             log(f"D={D} {state}: fused {row['fused']['e2e_ms']:.2f} ms e2e / "
-                f"{row['fused']['kernel_ms']:.3f} ms kernels, sequential "
+                f"{row['fused']['kernel_ms']:.3f} ms kernels, overlap "
+                f"{row['fused_overlap']['e2e_ms']:.2f} ms e2e, sequential "
                 f"{row['sequential']['e2e_ms']:.2f} / {row['sequential']['kernel_ms']:.3f} ms")
     head = next(c for c in cases if c["distinct_experts"] == 56 and c["state"] == "warm")
     sec = head["fused"]["e2e_ms"] * 1e-3
@@ -565,7 +571,9 @@ def oracle_multiwave(weights, T, head, budget_s=12.0):
 
 
 def bench_stack(args):
-    """16 layers, 16 slots each, Zipf(1.1) routing, 64 tokens per step."""
+    """16 layers, 16 slots each, Zipf(1.1) routing, 64 tokens per step; waves of
+    C (the paper's plan) and waves of C/2 with fills overlapping the previous
+    wave's computation, each from empty caches over the same routing."""
     import torch
     from paper_2608_15383_amd import api
     from paper_2608_15383_amd.inputs import zipf_gumbel_logits
@@ -582,8 +590,6 @@ def bench_stack(args):
     torch.cuda.empty_cache()
     h2d_gbs = pinned_h2d_gbs(torch, host)
     banks = [torch.zeros(C * rec, dtype=torch.uint8, device="cuda") for _ in range(L)]
-    caches = [api.Cache(dm, C, slot_bank=banks[l],
-                        host_bank=host[l * N_EXPERTS * rec:(l + 1) * N_EXPERTS * rec]) for l in range(L)]
     rng = np.random.default_rng(4)
     perms = [rng.permutation(N_EXPERTS) for _ in range(L)]
     n_steps = warmup + steps
@@ -596,53 +602,72 @@ def bench_stack(args):
     ws = torch.empty(api.workspace_bytes(dm, T), dtype=torch.uint8, device="cuda")
     log(f"stack ready: pinned H2D {h2d_gbs:.1f} GB/s")
 
-    def step(s, st):
-        for l in range(L):
-            api.moe_forward(caches[l], hs[(s * L + l) % len(hs)], None, y, ws,
-                            logits_override=z_dev[s, l], stats=st)
-
-    first = api.Stats()
-    step(0, first)
-    torch.cuda.synchronize()
-    for s in range(1, warmup):
-        step(s, api.Stats())
-    torch.cuda.synchronize()
-    st = api.Stats()
-    t0 = time.perf_counter()
-    for s in range(warmup, n_steps):
-        step(s, st)
-    torch.cuda.synchronize()
-    sec = time.perf_counter() - t0
-    api.profile_begin(1 << 16)
-    step(warmup, api.Stats())
-    prof = api.profile_end(1 << 16)
-    kern = {}
-    for name, t in prof:
-        kern.setdefault(name, []).append(t)
-    kern = {n: dict(avg_us=1e3 * float(np.mean(v)), launches=len(v)) for n, v in kern.items()}
-    kernel_ms = sum(v["avg_us"] * v["launches"] for v in kern.values()) * 1e-3
-
     def hit_rate(x):
         tot = x.hits + x.misses
         return x.hits / tot if tot else 0.0
 
-    calls = steps * L
-    h2d_per_call = st.h2d_bytes / calls
-    dom = max(kern, key=lambda n: kern[n]["avg_us"] * kern[n]["launches"])
-    out = dict(metric=METRIC, value=T * steps / sec, unit="tokens/s", n_gpus=1, steps=steps,
-               warmup=warmup, ms_per_step=1e3 * sec / steps, higher_is_better=True, scaling="weak",
+    def run_mode(overlap):
+        caches = [api.Cache(dm, C, slot_bank=banks[l],
+                            host_bank=host[l * N_EXPERTS * rec:(l + 1) * N_EXPERTS * rec])
+                  for l in range(L)]
+        for c in caches:
+            c.set_wave_overlap(overlap)
+
+        def step(s, st):
+            for l in range(L):
+                api.moe_forward(caches[l], hs[(s * L + l) % len(hs)], None, y, ws,
+                                logits_override=z_dev[s, l], stats=st)
+
+        first = api.Stats()
+        step(0, first)
+        torch.cuda.synchronize()
+        for s in range(1, warmup):
+            step(s, api.Stats())
+        torch.cuda.synchronize()
+        st = api.Stats()
+        t0 = time.perf_counter()
+        for s in range(warmup, n_steps):
+            step(s, st)
+        torch.cuda.synchronize()
+        sec = time.perf_counter() - t0
+        y_last = y.clone()
+        api.profile_begin(1 << 16)
+        step(warmup, api.Stats())
+        prof = api.profile_end(1 << 16)
+        for c in caches:
+            c.close()
+        kern = {}
+        for name, t in prof:
+            kern.setdefault(name, []).append(t)
+        kern = {n: dict(avg_us=1e3 * float(np.mean(v)), launches=len(v)) for n, v in kern.items()}
+        kernel_ms = sum(v["avg_us"] * v["launches"] for v in kern.values()) * 1e-3
+        calls = steps * L
+        achieved = st.h2d_bytes / sec / 1e9
+        res = dict(tokens_per_s=T * steps / sec, ms_per_step=1e3 * sec / steps,
+                   hit_rate_steady=hit_rate(st), hit_rate_cold_first_step=hit_rate(first),
+                   h2d_bytes_per_layer_call=st.h2d_bytes / calls, waves_per_layer_call=st.waves / calls,
+                   misses_per_layer_call=st.misses / calls, h2d_gbs_achieved=achieved,
+                   host_link=dict(bound="host link", achieved=achieved, pinned_copy_gbs=h2d_gbs,
+                                  frac=achieved / h2d_gbs),
+                   kernels_ms_per_step=kernel_ms, kernels=kern,
+                   dominant_kernel=max(kern, key=lambda n: kern[n]["avg_us"] * kern[n]["launches"]))
+        log(f"overlap={overlap}: {res['tokens_per_s']:.0f} tokens/s, link {achieved:.1f} GB/s "
+            f"({res['host_link']['frac']:.2f}), hit rate {res['hit_rate_steady']:.3f}, "
+            f"{res['waves_per_layer_call']:.2f} waves per layer call")
+        return res, y_last
+
+    plain, y_plain = run_mode(False)
+    over, y_over = run_mode(True)
+    out = dict(metric=METRIC, value=over["tokens_per_s"], unit="tokens/s", n_gpus=1, steps=steps,
+               warmup=warmup, ms_per_step=over["ms_per_step"], higher_is_better=True, scaling="weak",
                vs_baseline=None, dtype="bf16", data="synthetic",
                config=dict(workload="olmoe_stack16_zipf1.1_16slots", layers=L, tokens=T,
                            d_model=D_MODEL, d_ff=D_FF, n_experts=N_EXPERTS, top_k=TOP_K, slots=C,
-                           group=128, weights="int4 group-128, fp16 scales",
+                           group=128, weights="int4 group-128, fp16 scales", wave_overlap=True,
                            activations="8 pre-drawn N(0,1) token blocks cycled over layers and steps"),
-               hit_rate_steady=hit_rate(st), hit_rate_cold_first_step=hit_rate(first),
-               h2d_bytes_per_layer_call=h2d_per_call, waves_per_layer_call=st.waves / calls,
-               misses_per_layer_call=st.misses / calls,
-               h2d_gbs_achieved=st.h2d_bytes / sec / 1e9,
-               host_link=dict(bound="host link", achieved=st.h2d_bytes / sec / 1e9,
-                              pinned_copy_gbs=h2d_gbs, frac=st.h2d_bytes / sec / 1e9 / h2d_gbs),
-               kernels_ms_per_step=kernel_ms, kernels=kern, dominant_kernel=dom)
+               **{k: v for k, v in over.items() if k not in ("ms_per_step", "tokens_per_s")},
+               no_overlap=plain, overlap_speedup=over["tokens_per_s"] / plain["tokens_per_s"],
+               last_output_equal=bool(torch.equal(y_plain, y_over)))
     print(json.dumps(out), flush=True)
 
 

@@ -198,9 +198,20 @@ int32_t emoe_cache_state(const emoe_cache* cache, int32_t* slot_of_expert,
  * are invalid).  Blocking: reads device memory after the device is idle. */
 int32_t emoe_cache_sync_timeouts(const emoe_cache* cache, int64_t* timeouts);
 
+/* Copy/compute overlap across waves (Sec. 3.3 lets a slot be refilled once
+ * its preceding computation has finished).  enable = 1: when a call's active
+ * set does not fit in the C slots, its waves hold at most max(1, C/2)
+ * experts.  Under the LRU rule the previous wave's slots carry the newest
+ * stamps, so every miss of a wave then takes a slot the previous wave does
+ * not use, and its copy (ordered only by that slot's completion event)
+ * proceeds while the previous wave computes.  Sets that fit stay one wave.
+ * Default 0: waves of up to C.  Results are bit-identical either way. */
+int32_t emoe_cache_set_wave_overlap(emoe_cache* cache, int32_t enable);
+
 /* Sec. 3.4: split the active set into waves of at most C experts.
  * counts: host [E].  Order: experts resident now (ascending id), then the
- * others (ascending id), cut into chunks of C.  Outputs (host):
+ * others (ascending id), cut into chunks of C (of max(1, C/2) under
+ * emoe_cache_set_wave_overlap when they do not fit at once).  Outputs (host):
  * wave_experts[<=E], wave_offsets[<=E+1] (wave w = wave_experts[off[w]..off[w+1])),
  * n_waves.  Does not change the cache. */
 int32_t emoe_plan_waves(const emoe_cache* cache, const int32_t* counts,

@@ -64,6 +64,7 @@ SIGNATURES = {
     "emoe_cache_destroy": (_i32, [_vp]),
     "emoe_cache_preload_all": (_i32, [_vp, _vp]),
     "emoe_cache_state": (_i32, [_vp, _vp, _vp, _vp]),
+    "emoe_cache_set_wave_overlap": (_i32, [_vp, _i32]),
     "emoe_cache_sync_timeouts": (_i32, [_vp, _i64p]),
     "emoe_plan_waves": (_i32, [_vp, _vp, _vp, _vp, _i32p]),
     "emoe_build_slot_map": (_i32, [_vp, _vp, _i32, _vp, _vp, _vp, _i32p, C.POINTER(Stats)]),

@@ -128,6 +128,11 @@ class Cache:
         check(lib().emoe_cache_sync_timeouts(self.handle, C.byref(n)))
         return n.value
 
+    def set_wave_overlap(self, enable: bool) -> None:
+        """emoe_cache_set_wave_overlap: waves of C/2 when the active set does not fit,
+        so each wave's fills proceed while the previous wave computes."""
+        check(lib().emoe_cache_set_wave_overlap(self.handle, int(bool(enable))))
+
     def set_wave_delay(self, microseconds: int) -> None:
         """emoe_test_set_wave_delay: spin before each wave's projections (test hook)."""
         check(lib().emoe_test_set_wave_delay(self.handle, int(microseconds)))

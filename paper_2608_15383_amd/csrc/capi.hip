@@ -114,6 +114,7 @@ struct emoe_cache {
   DecodeSync* sync = nullptr;       // device: hand-over data of the fused decode launches
   DecodeProgress prog;              // host: epoch of the last direct fused launch
   int32_t wave_delay_us = 0;        // test hook: spin before each wave's projections
+  bool overlap = false;             // waves of C/2 so fills overlap the previous wave
   void* scratch = nullptr;          // device address of this device's no-alloc workspace
 };
 
@@ -545,6 +546,13 @@ int32_t emoe_cache_preload_all(emoe_cache* c, hipStream_t stream) {
   return EMOE_OK;
 }
 
+int32_t emoe_cache_set_wave_overlap(emoe_cache* c, int32_t enable) {
+  if (!c) return fail(EMOE_EINVAL, "cache is NULL");
+  if (enable != 0 && enable != 1) return fail(EMOE_EINVAL, "enable=%d is not 0 or 1", enable);
+  c->overlap = enable != 0;
+  return EMOE_OK;
+}
+
 int32_t emoe_cache_state(const emoe_cache* c, int32_t* slot_of_expert, int32_t* expert_of_slot,
                          int64_t* stamp_of_slot) {
   if (!c) return fail(EMOE_EINVAL, "cache is NULL");
@@ -565,8 +573,11 @@ int32_t emoe_plan_waves(const emoe_cache* c, const int32_t* counts, int32_t* wav
       if (counts[e] < 0) return fail(EMOE_EINVAL, "counts[%d] < 0", e);
       if (counts[e] > 0 && ((c->slot_of[e] >= 0) == (pass == 0))) wave_experts[n++] = e;
     }
+  // Overlap plan: a set that does not fit is cut into waves of C/2, whose
+  // misses (under the LRU rule) never take the previous wave's slots.
+  const int size = (c->overlap && n > c->capacity) ? std::max(1, c->capacity / 2) : c->capacity;
   int w = 0;
-  for (int at = 0; at < n; at += c->capacity) wave_offsets[w++] = at;
+  for (int at = 0; at < n; at += size) wave_offsets[w++] = at;
   wave_offsets[w] = n;
   *n_waves = w;
   return EMOE_OK;

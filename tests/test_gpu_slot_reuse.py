@@ -149,3 +149,37 @@ def test_slot_reuse_waits_for_the_wave_reading_it(olmoe16, path, sequential):
         _slot_records_match_host(cache, slots, host)
     finally:
         cache.close()
+
+
+@pytest.mark.parametrize("distinct,path", [(24, api.EMOE_PATH_GEMV), (40, api.EMOE_PATH_GEMV),
+                                           (64, api.EMOE_PATH_GEMV), (64, api.EMOE_PATH_MFMA)])
+def test_overlap_waves_equal_single_wave(olmoe16, distinct, path):
+    """Waves of C/2 (fills overlapping the previous wave's computation, with a
+    200 us spin widening that window): the result equals the resident
+    single-wave call bit for bit, and waves, hits, misses and the cache state
+    follow the oracle's overlap plan."""
+    lay, layer, host = olmoe16
+    z = spread_logits(T, 64, 8, distinct, seed=6)
+    y1 = layer.forward(lay.h, logits=z, path=path)
+    cache, slots = _new_cache(layer, host)
+    ref = O.SlotCache(64, C, api.expert_record_bytes(layer.dm))
+    try:
+        cache.set_wave_overlap(True)
+        cache.set_wave_delay(200)
+        for call in range(2):
+            st = api.Stats()
+            y = layer.forward(lay.h, logits=z, cache=cache, stats=st, path=path)
+            waves = O.plan_waves(_active(z), ref.resident(), C, overlap=True)
+            h0, m0 = ref.hits, ref.misses
+            for w in waves:
+                ref.map_wave(w)
+            assert st.waves == len(waves) and max(len(w) for w in waves) <= C // 2
+            assert (st.hits, st.misses) == (ref.hits - h0, ref.misses - m0)
+            so, eo, stamp = cache.state()
+            assert so.tolist() == ref.slot_of and eo.tolist() == ref.expert_of
+            assert stamp.tolist() == ref.stamp
+            assert np.array_equal(y, y1), call
+        cache.set_wave_delay(0)
+        _slot_records_match_host(cache, slots, host)
+    finally:
+        cache.close()

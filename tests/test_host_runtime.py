@@ -77,11 +77,13 @@ def test_pack_unpack_round_trip_and_oracle_codes():
         api.pack_expert(dm, q["q_gate"], s["s_gate"], q["q_up"], s["s_up"], bad, s["s_down"])
 
 
-def test_plan_waves_and_slot_maps_match_oracle():
+@pytest.mark.parametrize("overlap", [False, True])
+def test_plan_waves_and_slot_maps_match_oracle(overlap):
     rng = np.random.default_rng(1)
-    for e, c, k in [(64, 16, 8), (8, 2, 2), (16, 5, 3), (32, 32, 4)]:
+    for e, c, k in [(64, 16, 8), (8, 2, 2), (16, 5, 3), (32, 32, 4), (16, 1, 1)]:
         dm = api.dims(128, 128, e, k)
         cache = api.Cache(dm, c)
+        cache.set_wave_overlap(overlap)
         ref = O.SlotCache(e, c, record_bytes=api.expert_record_bytes(dm))
         stats = api.Stats()
         for step in range(60):
@@ -89,7 +91,7 @@ def test_plan_waves_and_slot_maps_match_oracle():
             act = rng.choice(e, size=int(rng.integers(1, e + 1)), replace=False)
             counts[act] = rng.integers(1, 5, size=len(act))
             waves = cache.plan_waves(counts)
-            assert waves == O.plan_waves(np.nonzero(counts)[0], ref.resident(), c)
+            assert waves == O.plan_waves(np.nonzero(counts)[0], ref.resident(), c, overlap)
             for w in waves:
                 sm, fills = cache.build_slot_map(w, stats)
                 rsm, rfills = ref.map_wave(w)
