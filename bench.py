@@ -27,6 +27,10 @@ frontier: the stack's capacity and batch frontier: C in {8, 16, 32, 64} slots
           per layer and T in {1, 2, 4, 8} tokens per step (C = 64: every
           expert resident).  Tokens/s, hit rate and H2D bytes per token for
           each point; value = tokens/s at C = 16, T = 1.
+decoder : synthetic OLMoE-shaped decoder (16 layers of attention + this layer,
+          random weights): time to first token for a 128-token prompt and greedy
+          decode tokens/s over 128 generated tokens, at 64 and 16 slots per
+          layer.  value = decode tokens/s at 64 slots.
 copy    : calibration only (not a layer): a plain 1 GiB device-to-device copy of
           known size, so hardware byte counters (FETCH_SIZE, WRITE_SIZE) read on
           the layer kernels can be scaled to bytes.  value = copy GB/s.
@@ -64,7 +68,7 @@ def parse():
     p.add_argument("--steps", type=int, default=None)
     p.add_argument("--warmup", type=int, default=None)
     p.add_argument("--workload", default="decode",
-                   choices=["decode", "prefill", "multiwave", "stack", "frontier", "copy"])
+                   choices=["decode", "prefill", "multiwave", "stack", "frontier", "decoder", "copy"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-prefill", action="store_true",
                    help="decode only: skip the prefill sub-record")
@@ -748,6 +752,97 @@ def bench_frontier(args):
     print(json.dumps(out), flush=True)
 
 
+def bench_decoder(args):
+    """Synthetic OLMoE-shaped decoder (16 layers of attention + the W4A16 layer,
+    random weights) in the structure of the paper's runtime table: time to
+    first token for a prompt and greedy decode tokens/s, at 64 slots per layer
+    (every expert resident) and at 16 slots (pinned host bank of all 1024
+    records).  The next token never leaves the GPU between steps."""
+    import torch
+    from paper_2608_15383_amd import api
+
+    torch.cuda.init()
+    L, H, Dh, V = 16, 16, 128, 50304
+    prompt_len = 128
+    gen_tokens = args.steps or 128
+    reps = 3
+    dm = api.dims(D_MODEL, D_FF, N_EXPERTS, TOP_K)
+    dd = api.decoder_dims(L, H, Dh, V, prompt_len + gen_tokens + 1, dm)
+    rec = api.expert_record_bytes(dm)
+    g = torch.Generator(device="cuda").manual_seed(11)
+    bf = dict(dtype=torch.bfloat16, device="cuda", generator=g)
+    w = dict(embed=torch.randn((V, D_MODEL), **bf), lm_head=torch.randn((V, D_MODEL), **bf) * 0.02,
+             final_norm=1 + torch.randn((D_MODEL,), **bf) * 0.1)
+    w["attn_norm"] = [1 + torch.randn((D_MODEL,), **bf) * 0.1 for _ in range(L)]
+    w["wqkv"] = [torch.randn((3 * D_MODEL, D_MODEL), **bf) * 0.02 for _ in range(L)]
+    w["wo"] = [torch.randn((D_MODEL, D_MODEL), **bf) * 0.02 for _ in range(L)]
+    w["moe_norm"] = [1 + torch.randn((D_MODEL,), **bf) * 0.1 for _ in range(L)]
+    w["w_router"] = [torch.randn((N_EXPERTS, D_MODEL), **bf) * 0.02 for _ in range(L)]
+    log("decoder: quantizing 16 x 64 experts")
+    host, _ = quantized_host_bank(api, dm, torch, [3000 + l for l in range(L)])
+    torch.cuda.empty_cache()
+    prompt = torch.randint(0, V, (prompt_len,), dtype=torch.int32, device="cuda", generator=g)
+    kv = torch.zeros(api.decoder_kv_bytes(dd), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(api.decoder_workspace_bytes(dd, prompt_len), dtype=torch.uint8, device="cuda")
+    logits = torch.empty(V, dtype=torch.float32, device="cuda")
+    toks = torch.empty(gen_tokens + 1, dtype=torch.int32, device="cuda")
+    rows = []
+    for C in (64, 16):
+        banks = [torch.zeros(C * rec, dtype=torch.uint8, device="cuda") for _ in range(L)]
+        caches = []
+        for l in range(L):
+            c = api.Cache(dm, C, slot_bank=banks[l],
+                          host_bank=host[l * N_EXPERTS * rec:(l + 1) * N_EXPERTS * rec])
+            if C == N_EXPERTS:
+                c.preload_all()
+            else:
+                c.set_wave_overlap(True)
+            caches.append(c)
+        dec = api.Decoder(dd, w, caches, kv)
+        ttft, tps, stats = [], [], api.Stats()
+        for rep in range(reps + 1):           # the first repetition warms up
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            dec.forward(prompt, 0, logits, toks[0:1], ws)
+            first = int(toks[0].item())       # the first token reaches the host
+            t1 = time.perf_counter()
+            st = api.Stats()
+            for i in range(gen_tokens):
+                dec.forward(toks[i:i + 1], prompt_len + i, logits, toks[i + 1:i + 2], ws, stats=st)
+            torch.cuda.synchronize()
+            t2 = time.perf_counter()
+            if rep:
+                ttft.append(t1 - t0)
+                tps.append(gen_tokens / (t2 - t1))
+                stats = st
+        tot = stats.hits + stats.misses
+        row = dict(slots=C, ttft_ms=1e3 * float(np.median(ttft)), decode_tokens_per_s=float(np.median(tps)),
+                   ms_per_token=1e3 / float(np.median(tps)), prompt_tokens=prompt_len,
+                   generated_tokens=gen_tokens, repetitions=reps, first_token=first,
+                   hit_rate=(stats.hits / tot) if tot else None,
+                   h2d_gib_per_request=stats.h2d_bytes / 2 ** 30,
+                   slot_bank_gib=L * C * rec / 2 ** 30)
+        rows.append(row)
+        log(f"C={C}: TTFT {row['ttft_ms']:.2f} ms, decode {row['decode_tokens_per_s']:.1f} tokens/s, "
+            f"hit rate {row['hit_rate']}, H2D {row['h2d_gib_per_request']:.2f} GiB per request")
+        dec.close()
+        for c in caches:
+            c.close()
+        del banks, caches
+        torch.cuda.empty_cache()
+    head = rows[0]
+    out = dict(metric=METRIC, value=head["decode_tokens_per_s"], unit="tokens/s", n_gpus=1,
+               steps=gen_tokens, warmup=1, ms_per_step=head["ms_per_token"], higher_is_better=True,
+               scaling="weak", vs_baseline=None, dtype="bf16", data="synthetic",
+               config=dict(workload="olmoe_synthetic_decoder", layers=L, heads=H, head_dim=Dh, vocab=V,
+                           d_model=D_MODEL, d_ff=D_FF, n_experts=N_EXPERTS, top_k=TOP_K,
+                           prompt_tokens=prompt_len, generated_tokens=gen_tokens,
+                           value_at=dict(slots=64),
+                           weights="random; experts int4 group-128 with fp16 scales, the rest bf16"),
+               capacity=rows)
+    print(json.dumps(out), flush=True)
+
+
 def bench_copy(args):
     import torch
 
@@ -787,6 +882,8 @@ def main():
         bench_copy(args)
     elif args.workload == "frontier":
         bench_frontier(args)
+    elif args.workload == "decoder":
+        bench_decoder(args)
     else:
         bench_layer(args)
 

@@ -41,6 +41,19 @@ class WsLayout(C.Structure):
                                           "chunk_counts", "tok_bias", "total")]
 
 
+class DecoderDims(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("n_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("vocab", C.c_int32), ("max_positions", C.c_int32), ("rope_base", C.c_float),
+                ("rms_eps", C.c_float), ("renormalize", C.c_int32), ("moe", Dims)]
+
+
+class DecoderWeights(C.Structure):
+    _fields_ = [("embed", C.c_void_p), ("lm_head", C.c_void_p), ("final_norm", C.c_void_p),
+                ("attn_norm", C.POINTER(C.c_void_p)), ("wqkv", C.POINTER(C.c_void_p)),
+                ("wo", C.POINTER(C.c_void_p)), ("moe_norm", C.POINTER(C.c_void_p)),
+                ("w_router", C.POINTER(C.c_void_p))]
+
+
 _vp = C.c_void_p
 _i32 = C.c_int32
 _i32p = C.POINTER(C.c_int32)
@@ -77,6 +90,13 @@ SIGNATURES = {
                                         C.POINTER(Stats)]),
     "emoe_test_fail_copy_after": (_i32, [C.c_int64]),
     "emoe_test_set_wave_delay": (_i32, [_vp, _i32]),
+    "emoe_decoder_kv_bytes": (C.c_size_t, [C.POINTER(DecoderDims)]),
+    "emoe_decoder_workspace_bytes": (C.c_size_t, [C.POINTER(DecoderDims), _i32]),
+    "emoe_decoder_create": (_i32, [C.POINTER(DecoderDims), C.POINTER(DecoderWeights),
+                                   C.POINTER(_vp), _vp, C.POINTER(_vp)]),
+    "emoe_decoder_destroy": (_i32, [_vp]),
+    "emoe_decoder_forward": (_i32, [_vp, _vp, _i32, _i32, _vp, _vp, _vp, C.c_size_t, _vp,
+                                    C.POINTER(Stats)]),
     "emoe_profile_begin": (_i32, [_i32]),
     "emoe_profile_end": (_i32, [_vp, _vp, _i32, _i32p]),
 }

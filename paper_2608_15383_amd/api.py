@@ -11,8 +11,8 @@ import ctypes as C
 import numpy as np
 
 from . import _lib
-from ._lib import (Dims, Stats, WsLayout, check, lib, EMOE_PATH_AUTO, EMOE_PATH_GEMV,
-                   EMOE_PATH_MFMA, ExactMoEError)
+from ._lib import (DecoderDims, DecoderWeights, Dims, Stats, WsLayout, check, lib,
+                   EMOE_PATH_AUTO, EMOE_PATH_GEMV, EMOE_PATH_MFMA, ExactMoEError)
 
 
 def _ptr(t) -> int | None:
@@ -194,6 +194,67 @@ def test_fail_copy_after(copies: int) -> None:
     check(lib().emoe_test_fail_copy_after(int(copies)))
 
 
+def decoder_dims(n_layers: int, n_heads: int, head_dim: int, vocab: int, max_positions: int,
+                 moe: Dims, rope_base: float = 10000.0, rms_eps: float = 1e-5,
+                 renormalize: bool = True) -> DecoderDims:
+    return DecoderDims(n_layers, n_heads, head_dim, vocab, max_positions, rope_base, rms_eps,
+                       int(bool(renormalize)), moe)
+
+
+def decoder_kv_bytes(dd: DecoderDims) -> int:
+    return int(lib().emoe_decoder_kv_bytes(C.byref(dd)))
+
+
+def decoder_workspace_bytes(dd: DecoderDims, max_tokens: int) -> int:
+    return int(lib().emoe_decoder_workspace_bytes(C.byref(dd), max_tokens))
+
+
+class Decoder:
+    """emoe_decoder_*: the synthetic decoder around one slot cache per layer.
+
+    weights: dict of device bf16 tensors: embed [V][d], lm_head [V][d],
+    final_norm [d], and per-layer lists attn_norm, wqkv [3d][d], wo [d][d],
+    moe_norm, w_router [E][d].  caches: list of Cache (one per layer).
+    kv: device buffer of decoder_kv_bytes(dd) bytes."""
+
+    def __init__(self, dd: DecoderDims, weights: dict, caches, kv):
+        n = dd.n_layers
+        arr = lambda name: (C.c_void_p * n)(*[_ptr(t) for t in weights[name]])
+        self._arrays = {k: arr(k) for k in ("attn_norm", "wqkv", "wo", "moe_norm", "w_router")}
+        cast = lambda a: C.cast(a, C.POINTER(C.c_void_p))
+        w = DecoderWeights(_ptr(weights["embed"]), _ptr(weights["lm_head"]),
+                           _ptr(weights["final_norm"]), cast(self._arrays["attn_norm"]),
+                           cast(self._arrays["wqkv"]), cast(self._arrays["wo"]),
+                           cast(self._arrays["moe_norm"]), cast(self._arrays["w_router"]))
+        handles = (C.c_void_p * n)(*[c.handle.value for c in caches])
+        self.dims = dd
+        self._keep = (weights, caches, kv, handles)
+        h = C.c_void_p()
+        check(lib().emoe_decoder_create(C.byref(dd), C.byref(w), C.cast(handles, C.POINTER(C.c_void_p)),
+                                        _ptr(kv), C.byref(h)))
+        self.handle = h
+
+    def close(self) -> None:
+        if self.handle:
+            lib().emoe_decoder_destroy(self.handle)
+            self.handle = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def forward(self, tokens, pos0: int, logits, next_token, workspace, stream=None,
+                stats: Stats | None = None) -> None:
+        """emoe_decoder_forward: tokens (device int32 [T]) at positions pos0 .. pos0+T-1."""
+        nbytes = workspace.numel() * workspace.element_size()
+        check(lib().emoe_decoder_forward(self.handle, _ptr(tokens), tokens.shape[0], pos0,
+                                         _ptr(logits), _ptr(next_token), _ptr(workspace), nbytes,
+                                         _stream(stream),
+                                         C.byref(stats) if stats is not None else None))
+
+
 def profile_begin(max_kernels: int) -> None:
     """emoe_profile_begin: time each kernel the layer calls launch from this thread."""
     check(lib().emoe_profile_begin(max_kernels))
@@ -212,4 +273,5 @@ def profile_end(max_out: int = 1 << 16) -> list[tuple[str, float]]:
 __all__ = ["Dims", "Stats", "WsLayout", "ExactMoEError", "EMOE_PATH_AUTO", "EMOE_PATH_GEMV",
            "EMOE_PATH_MFMA", "dims", "check_dims", "expert_record_bytes", "workspace_layout",
            "workspace_bytes", "quantize_experts", "unpack_expert", "pack_expert", "route", "Cache",
-           "moe_forward", "moe_forward_noalloc", "moe_forward_sequential", "test_fail_copy_after", "profile_begin", "profile_end", "lib"]
+           "moe_forward", "moe_forward_noalloc", "decoder_dims", "decoder_kv_bytes",
+           "decoder_workspace_bytes", "Decoder", "moe_forward_sequential", "test_fail_copy_after", "profile_begin", "profile_end", "lib"]

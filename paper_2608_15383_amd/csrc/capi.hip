@@ -16,17 +16,27 @@
 
 using namespace emoe;
 
+namespace {
+thread_local char g_last_error[512] = "";
+}  // namespace
+
 namespace emoe {
 namespace {
 thread_local LaunchEvents t_launch_events;
 }
 LaunchEvents& launch_events() { return t_launch_events; }
+
+int32_t report_error(int32_t status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+  va_end(ap);
+  return status;
+}
 }  // namespace emoe
 
 // ------------------------------------------------------------------ errors
 namespace {
-
-thread_local char g_last_error[512] = "";
 
 int32_t fail(int32_t status, const char* fmt, ...) {
   va_list ap;

@@ -246,6 +246,10 @@ inline void launch(Kernel kernel, dim3 grid, dim3 block, hipStream_t stream, Arg
   ev.used = true;
 }
 
+// Record the calling thread's emoe_last_error() message and return status
+// (used by C ABI entry points outside capi.hip).
+int32_t report_error(int32_t status, const char* fmt, ...);
+
 // ---------------------------------------------------------------------------
 // Launchers (return the launch status; arguments are validated by the caller)
 // ---------------------------------------------------------------------------

@@ -1,0 +1,462 @@
+// Synthetic decoder around the routed-expert layer (exactmoe_decoder.h):
+// embedding gather, residual add + RMSNorm, rotary positions with the KV
+// cache append, causal attention and the greedy argmax as gfx950 kernels; the
+// dense bf16 projections (QKV, output, LM head) through rocBLAS; the routed
+// experts through emoe_moe_forward.
+#include <rocblas/rocblas.h>
+
+#include <cmath>
+#include <new>
+#include <vector>
+
+#include "common.h"
+#include "exactmoe_decoder.h"
+
+using namespace emoe;
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxHeadDim = 256;
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// ---------------------------------------------------------------- kernels
+// x[t] = embed[clamp(tokens[t])], one workgroup per token, 16-byte copies.
+__global__ __launch_bounds__(kThreads) void embed_kernel(int V, int d, const int32_t* tokens,
+                                                         const uint16_t* embed, uint16_t* x) {
+  const int t = blockIdx.x;
+  int tok = tokens[t];
+  tok = tok < 0 ? 0 : (tok >= V ? V - 1 : tok);
+  const uint4* src = reinterpret_cast<const uint4*>(embed + (int64_t)tok * d);
+  uint4* dst = reinterpret_cast<uint4*>(x + (int64_t)t * d);
+  for (int i = threadIdx.x; i < d / 8; i += kThreads) dst[i] = src[i];
+}
+
+// Sum over the workgroup in a fixed order (wavefront butterflies, then the
+// four wavefront sums in order); every thread gets the total.
+__device__ __forceinline__ float block_sum(float v, float* red) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+__device__ __forceinline__ float block_max(float v, float* red) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+  const int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+// Per token row: if delta, x = bf16(x + delta) (written back); then
+// out = bf16(x / sqrt(mean(x^2) + eps) * g), in fp32.  d is a multiple of 8
+// and at most 8 * 256 * 4 (four 8-element chunks per thread).
+__global__ __launch_bounds__(kThreads) void add_rmsnorm_kernel(int d, uint16_t* x,
+                                                               const uint16_t* delta,
+                                                               const uint16_t* g, float eps,
+                                                               uint16_t* out) {
+  __shared__ float red[4];
+  const int t = blockIdx.x;
+  uint4* xr = reinterpret_cast<uint4*>(x + (int64_t)t * d);
+  const uint4* dr = delta ? reinterpret_cast<const uint4*>(delta + (int64_t)t * d) : nullptr;
+  const int n8 = d / 8;
+  float v[4][8];
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int i = threadIdx.x + c * kThreads;
+    if (i >= n8) break;
+    uint4 a = xr[i];
+    uint32_t w[4] = {a.x, a.y, a.z, a.w};
+    if (dr) {
+      const uint4 b = dr[i];
+      const uint32_t u[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const float lo = bf16_to_f32(w[p] & 0xffffu) + bf16_to_f32(u[p] & 0xffffu);
+        const float hi = bf16_to_f32(w[p] >> 16) + bf16_to_f32(u[p] >> 16);
+        w[p] = f32_to_bf16_rne(lo) | (f32_to_bf16_rne(hi) << 16);
+      }
+      xr[i] = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      v[c][2 * p] = bf16_to_f32(w[p] & 0xffffu);
+      v[c][2 * p + 1] = bf16_to_f32(w[p] >> 16);
+      ss = fmaf(v[c][2 * p], v[c][2 * p], ss);
+      ss = fmaf(v[c][2 * p + 1], v[c][2 * p + 1], ss);
+    }
+  }
+  const float inv = 1.0f / sqrtf(block_sum(ss, red) / (float)d + eps);
+  const uint4* gr = reinterpret_cast<const uint4*>(g);
+  uint4* orow = reinterpret_cast<uint4*>(out + (int64_t)t * d);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int i = threadIdx.x + c * kThreads;
+    if (i >= n8) break;
+    const uint4 gv = gr[i];
+    const uint32_t gw[4] = {gv.x, gv.y, gv.z, gv.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const float lo = v[c][2 * p] * inv * bf16_to_f32(gw[p] & 0xffffu);
+      const float hi = v[c][2 * p + 1] * inv * bf16_to_f32(gw[p] >> 16);
+      o[p] = f32_to_bf16_rne(lo) | (f32_to_bf16_rne(hi) << 16);
+    }
+    orow[i] = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+// Rotary positions on q (in place in qkv) and k, and the cache append of k
+// and v, for token t at position pos0 + t.  Element i < Dh/2 of a head pairs
+// with i + Dh/2; the angle p * base^(-2i/Dh) and its sine and cosine are
+// taken in fp64, the rotation in fp32.  qkv row: [q (H*Dh) | k | v].
+__global__ __launch_bounds__(kThreads) void rope_kv_kernel(int H, int Dh, int pos0, float base,
+                                                           uint16_t* qkv, uint16_t* k_cache,
+                                                           uint16_t* v_cache) {
+  __shared__ float cs[kMaxHeadDim / 2][2];
+  const int t = blockIdx.x;
+  const int d = H * Dh, half = Dh / 2;
+  const int p = pos0 + t;
+  for (int i = threadIdx.x; i < half; i += kThreads) {
+    const double ang = (double)p * pow((double)base, -2.0 * (double)i / (double)Dh);
+    cs[i][0] = (float)cos(ang);
+    cs[i][1] = (float)sin(ang);
+  }
+  __syncthreads();
+  uint16_t* q = qkv + (int64_t)t * 3 * d;
+  const uint16_t* k = q + d;
+  const uint16_t* v = q + 2 * d;
+  uint16_t* kc = k_cache + (int64_t)p * d;
+  uint16_t* vc = v_cache + (int64_t)p * d;
+  for (int j = threadIdx.x; j < H * half; j += kThreads) {
+    const int h = j / half, i = j % half;
+    const float c = cs[i][0], s = cs[i][1];
+    const int a = h * Dh + i, b = a + half;
+    const float qa = bf16_to_f32(q[a]), qb = bf16_to_f32(q[b]);
+    q[a] = (uint16_t)f32_to_bf16_rne(qa * c - qb * s);
+    q[b] = (uint16_t)f32_to_bf16_rne(qb * c + qa * s);
+    const float ka = bf16_to_f32(k[a]), kb = bf16_to_f32(k[b]);
+    kc[a] = (uint16_t)f32_to_bf16_rne(ka * c - kb * s);
+    kc[b] = (uint16_t)f32_to_bf16_rne(kb * c + ka * s);
+  }
+  const uint4* vs = reinterpret_cast<const uint4*>(v);
+  uint4* vd = reinterpret_cast<uint4*>(vc);
+  for (int i = threadIdx.x; i < d / 8; i += kThreads) vd[i] = vs[i];
+}
+
+// Causal attention of token t (position pos0 + t), head h, over cache
+// positions 0 .. pos0 + t: scores q.k / sqrt(Dh) (bf16 products summed in
+// fp32), softmax in fp32, output bf16.  One workgroup per (head, token).
+__global__ __launch_bounds__(kThreads) void attention_kernel(int H, int Dh, int pos0,
+                                                             const uint16_t* qkv,
+                                                             const uint16_t* k_cache,
+                                                             const uint16_t* v_cache,
+                                                             uint16_t* out) {
+  __shared__ float score[EMOE_DECODER_MAX_POSITIONS];
+  __shared__ uint32_t qs[kMaxHeadDim / 2];
+  __shared__ float part[kThreads];
+  __shared__ float red[4];
+  const int h = blockIdx.x, t = blockIdx.y;
+  const int d = H * Dh;
+  const int n = pos0 + t + 1;
+  const uint16_t* q = qkv + (int64_t)t * 3 * d + h * Dh;
+  for (int i = threadIdx.x; i < Dh / 2; i += kThreads)
+    qs[i] = reinterpret_cast<const uint32_t*>(q)[i];
+  __syncthreads();
+  const float scale = 1.0f / sqrtf((float)Dh);
+  float mx = -INFINITY;
+  for (int j = threadIdx.x; j < n; j += kThreads) {
+    const uint4* kr = reinterpret_cast<const uint4*>(k_cache + (int64_t)j * d + h * Dh);
+    float acc = 0.f;
+    for (int c = 0; c < Dh / 8; ++c) {
+      const uint4 kv = kr[c];
+      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, kv.x),
+                                            __builtin_bit_cast(bf16x2_t, qs[4 * c]), acc, false);
+      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, kv.y),
+                                            __builtin_bit_cast(bf16x2_t, qs[4 * c + 1]), acc, false);
+      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, kv.z),
+                                            __builtin_bit_cast(bf16x2_t, qs[4 * c + 2]), acc, false);
+      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, kv.w),
+                                            __builtin_bit_cast(bf16x2_t, qs[4 * c + 3]), acc, false);
+    }
+    const float s = acc * scale;
+    score[j] = s;
+    mx = fmaxf(mx, s);
+  }
+  mx = block_max(mx, red);
+  float sum = 0.f;
+  for (int j = threadIdx.x; j < n; j += kThreads) {
+    const float e = expf(score[j] - mx);
+    score[j] = e;
+    sum += e;
+  }
+  sum = block_sum(sum, red);  // its barriers also publish score[]
+  // Output: thread -> (dimension, key stripe); stripes summed in order.
+  const int stripes = kThreads / Dh;
+  const int dim = threadIdx.x % Dh, stripe = threadIdx.x / Dh;
+  float acc = 0.f;
+  if (stripe < stripes) {
+    const uint16_t* vcol = v_cache + h * Dh + dim;
+    for (int j = stripe; j < n; j += stripes) acc = fmaf(score[j], bf16_to_f32(vcol[(int64_t)j * d]), acc);
+  }
+  part[threadIdx.x] = acc;
+  __syncthreads();
+  if (threadIdx.x < Dh) {
+    float o = 0.f;
+    for (int s = 0; s < stripes; ++s) o += part[s * Dh + threadIdx.x];
+    out[(int64_t)t * d + h * Dh + threadIdx.x] = (uint16_t)f32_to_bf16_rne(o / sum);
+  }
+}
+
+// Greedy next token: index of the largest logit, ties to the lower index.
+__global__ __launch_bounds__(1024) void argmax_kernel(int V, const float* logits, int32_t* out) {
+  __shared__ float bv[16];
+  __shared__ int bi[16];
+  float best = -INFINITY;
+  int idx = 0x7fffffff;
+  for (int i = threadIdx.x; i < V; i += 1024) {
+    const float v = logits[i];
+    if (v > best) {
+      best = v;
+      idx = i;
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const float ov = __shfl_xor(best, off);
+    const int oi = __shfl_xor(idx, off);
+    if (ov > best || (ov == best && oi < idx)) {
+      best = ov;
+      idx = oi;
+    }
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    bv[w] = best;
+    bi[w] = idx;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int k = 1; k < 16; ++k)
+      if (bv[k] > best || (bv[k] == best && bi[k] < idx)) {
+        best = bv[k];
+        idx = bi[k];
+      }
+    *out = idx < V ? idx : 0;
+  }
+}
+
+size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int32_t check_decoder_dims(const emoe_decoder_dims* dd) {
+  if (!dd) return report_error(EMOE_EINVAL, "dims is NULL");
+  const int32_t st = emoe_check_dims(&dd->moe);
+  if (st) return st;
+  const int d = dd->moe.d_model;
+  if (dd->n_layers < 1 || dd->n_heads < 1 || dd->head_dim < 8 || dd->head_dim % 8 ||
+      dd->head_dim > kMaxHeadDim || dd->n_heads * dd->head_dim != d)
+    return report_error(EMOE_ESHAPE,
+                        "need n_layers >= 1 and n_heads * head_dim == d_model with head_dim a "
+                        "multiple of 8 up to %d (got %d x %d for d_model %d)",
+                        kMaxHeadDim, dd->n_heads, dd->head_dim, d);
+  if (d > 8 * kThreads * 4) return report_error(EMOE_ESHAPE, "d_model %d above %d", d, 8 * kThreads * 4);
+  if (dd->vocab < 1) return report_error(EMOE_ESHAPE, "vocab %d < 1", dd->vocab);
+  if (dd->max_positions < 1 || dd->max_positions > EMOE_DECODER_MAX_POSITIONS)
+    return report_error(EMOE_ESHAPE, "max_positions %d outside [1, %d]", dd->max_positions,
+                        EMOE_DECODER_MAX_POSITIONS);
+  if (!(dd->rope_base > 1.0f) || !(dd->rms_eps >= 0.0f))
+    return report_error(EMOE_EINVAL, "rope_base must exceed 1 and rms_eps be >= 0");
+  return EMOE_OK;
+}
+
+struct WsLayout {
+  size_t x0, x1, n, qkv, attn, moe_y, moe_ws, moe_ws_bytes, total;
+};
+
+WsLayout decoder_ws_layout(const emoe_decoder_dims& dd, int T) {
+  WsLayout L{};
+  const size_t d = dd.moe.d_model;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align_up(bytes);
+    return at;
+  };
+  L.x0 = take((size_t)T * d * 2);
+  L.x1 = take((size_t)T * d * 2);
+  L.n = take((size_t)T * d * 2);
+  L.qkv = take((size_t)T * 3 * d * 2);
+  L.attn = take((size_t)T * d * 2);
+  L.moe_y = take((size_t)T * d * 2);
+  L.moe_ws_bytes = emoe_workspace_bytes(&dd.moe, T);
+  L.moe_ws = take(L.moe_ws_bytes);
+  L.total = off;
+  return L;
+}
+
+const char* rocblas_name(rocblas_status s) { return rocblas_status_to_string(s); }
+
+}  // namespace
+
+struct emoe_decoder {
+  emoe_decoder_dims dims;
+  const uint16_t* embed = nullptr;
+  const uint16_t* lm_head = nullptr;
+  const uint16_t* final_norm = nullptr;
+  std::vector<const uint16_t*> attn_norm, wqkv, wo, moe_norm, w_router;
+  std::vector<emoe_cache*> caches;
+  uint16_t* kv = nullptr;
+  rocblas_handle blas = nullptr;
+};
+
+namespace {
+
+// Y[T][N] (+ C) = X[T][K] W[N][K]^T with bf16 inputs, fp32 accumulation.
+// out_f32 selects an fp32 output (C unused); otherwise bf16 out with
+// Y = X W^T + C when C is given.
+int32_t dense(emoe_decoder* dec, int T, int N, int K, const uint16_t* X, const uint16_t* W,
+              const uint16_t* C, void* Y, bool out_f32) {
+  const float alpha = 1.0f, beta = (C && !out_f32) ? 1.0f : 0.0f;
+  const rocblas_datatype io = out_f32 ? rocblas_datatype_f32_r : rocblas_datatype_bf16_r;
+  const void* c = (C && !out_f32) ? static_cast<const void*>(C) : static_cast<const void*>(Y);
+  const rocblas_status st = rocblas_gemm_ex(
+      dec->blas, rocblas_operation_transpose, rocblas_operation_none, N, T, K, &alpha, W,
+      rocblas_datatype_bf16_r, K, X, rocblas_datatype_bf16_r, K, &beta, c, io, N, Y, io, N,
+      rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+  if (st != rocblas_status_success)
+    return report_error(EMOE_EHIP, "rocblas_gemm_ex (%d x %d x %d): %s", N, T, K, rocblas_name(st));
+  return EMOE_OK;
+}
+
+#define DEC_LAUNCH(...)                                                                 \
+  do {                                                                                  \
+    hipLaunchKernelGGL(__VA_ARGS__);                                                    \
+    const hipError_t e_ = hipGetLastError();                                            \
+    if (e_ != hipSuccess) return report_error(EMOE_EHIP, "decoder kernel launch: %s",   \
+                                              hipGetErrorString(e_));                   \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+size_t emoe_decoder_kv_bytes(const emoe_decoder_dims* dims) {
+  if (check_decoder_dims(dims) != EMOE_OK) return 0;
+  return (size_t)dims->n_layers * 2 * dims->max_positions * dims->moe.d_model * 2;
+}
+
+size_t emoe_decoder_workspace_bytes(const emoe_decoder_dims* dims, int32_t max_tokens) {
+  if (check_decoder_dims(dims) != EMOE_OK || max_tokens < 1) return 0;
+  return decoder_ws_layout(*dims, max_tokens).total;
+}
+
+int32_t emoe_decoder_create(const emoe_decoder_dims* dims, const emoe_decoder_weights* w,
+                            emoe_cache* const* caches, void* kv_cache, emoe_decoder** out) {
+  int32_t st = check_decoder_dims(dims);
+  if (st) return st;
+  if (!w || !caches || !kv_cache || !out) return report_error(EMOE_EINVAL, "NULL argument");
+  *out = nullptr;
+  const int L = dims->n_layers;
+  if (!w->embed || !w->lm_head || !w->final_norm || !w->attn_norm || !w->wqkv || !w->wo ||
+      !w->moe_norm || !w->w_router)
+    return report_error(EMOE_EINVAL, "NULL weight pointer");
+  for (int l = 0; l < L; ++l) {
+    if (!w->attn_norm[l] || !w->wqkv[l] || !w->wo[l] || !w->moe_norm[l] || !w->w_router[l] ||
+        !caches[l])
+      return report_error(EMOE_EINVAL, "NULL weight or cache of layer %d", l);
+  }
+  emoe_decoder* dec = new (std::nothrow) emoe_decoder();
+  if (!dec) return report_error(EMOE_EINVAL, "out of host memory");
+  dec->dims = *dims;
+  dec->embed = w->embed;
+  dec->lm_head = w->lm_head;
+  dec->final_norm = w->final_norm;
+  dec->attn_norm.assign(w->attn_norm, w->attn_norm + L);
+  dec->wqkv.assign(w->wqkv, w->wqkv + L);
+  dec->wo.assign(w->wo, w->wo + L);
+  dec->moe_norm.assign(w->moe_norm, w->moe_norm + L);
+  dec->w_router.assign(w->w_router, w->w_router + L);
+  dec->caches.assign(caches, caches + L);
+  dec->kv = static_cast<uint16_t*>(kv_cache);
+  const rocblas_status rs = rocblas_create_handle(&dec->blas);
+  if (rs != rocblas_status_success) {
+    delete dec;
+    return report_error(EMOE_EHIP, "rocblas_create_handle: %s", rocblas_name(rs));
+  }
+  *out = dec;
+  return EMOE_OK;
+}
+
+int32_t emoe_decoder_destroy(emoe_decoder* dec) {
+  if (!dec) return EMOE_OK;
+  if (dec->blas) (void)rocblas_destroy_handle(dec->blas);
+  delete dec;
+  return EMOE_OK;
+}
+
+int32_t emoe_decoder_forward(emoe_decoder* dec, const int32_t* tokens, int32_t T, int32_t pos0,
+                             float* logits, int32_t* next_token, void* workspace, size_t ws_bytes,
+                             hipStream_t stream, emoe_stats* stats) {
+  if (!dec) return report_error(EMOE_EINVAL, "decoder is NULL");
+  const emoe_decoder_dims& D = dec->dims;
+  if (T < 1 || pos0 < 0 || (int64_t)pos0 + T > D.max_positions)
+    return report_error(EMOE_EINVAL, "tokens %d at position %d exceed the cache of %d positions",
+                        T, pos0, D.max_positions);
+  if (!tokens || !logits || !next_token || !workspace)
+    return report_error(EMOE_EINVAL, "NULL tokens, logits, next_token or workspace");
+  const WsLayout L = decoder_ws_layout(D, T);
+  if (ws_bytes < L.total)
+    return report_error(EMOE_EINVAL, "workspace of %zu bytes < %zu needed", ws_bytes, L.total);
+  const int d = D.moe.d_model, H = D.n_heads, Dh = D.head_dim;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  uint16_t* xa = reinterpret_cast<uint16_t*>(ws + L.x0);
+  uint16_t* xb = reinterpret_cast<uint16_t*>(ws + L.x1);
+  uint16_t* n = reinterpret_cast<uint16_t*>(ws + L.n);
+  uint16_t* qkv = reinterpret_cast<uint16_t*>(ws + L.qkv);
+  uint16_t* attn = reinterpret_cast<uint16_t*>(ws + L.attn);
+  uint16_t* moe_y = reinterpret_cast<uint16_t*>(ws + L.moe_y);
+  void* moe_ws = ws + L.moe_ws;
+  const rocblas_status rs = rocblas_set_stream(dec->blas, stream);
+  if (rs != rocblas_status_success)
+    return report_error(EMOE_EHIP, "rocblas_set_stream: %s", rocblas_name(rs));
+
+  DEC_LAUNCH(embed_kernel, dim3(T), dim3(kThreads), 0, stream, D.vocab, d, tokens, dec->embed, xa);
+  const uint16_t* delta = nullptr;
+  const size_t kv_layer = (size_t)2 * D.max_positions * d;
+  int32_t st;
+  for (int l = 0; l < D.n_layers; ++l) {
+    uint16_t* kc = dec->kv + (size_t)l * kv_layer;
+    uint16_t* vc = kc + (size_t)D.max_positions * d;
+    DEC_LAUNCH(add_rmsnorm_kernel, dim3(T), dim3(kThreads), 0, stream, d, xa, delta,
+               dec->attn_norm[l], D.rms_eps, n);
+    if ((st = dense(dec, T, 3 * d, d, n, dec->wqkv[l], nullptr, qkv, false))) return st;
+    DEC_LAUNCH(rope_kv_kernel, dim3(T), dim3(kThreads), 0, stream, H, Dh, pos0, D.rope_base, qkv,
+               kc, vc);
+    DEC_LAUNCH(attention_kernel, dim3(H, T), dim3(kThreads), 0, stream, H, Dh, pos0, qkv, kc, vc,
+               attn);
+    if ((st = dense(dec, T, d, d, attn, dec->wo[l], xa, xb, false))) return st;  // x += attn Wo^T
+    std::swap(xa, xb);
+    DEC_LAUNCH(add_rmsnorm_kernel, dim3(T), dim3(kThreads), 0, stream, d, xa, nullptr,
+               dec->moe_norm[l], D.rms_eps, n);
+    if ((st = emoe_moe_forward(dec->caches[l], T, n, dec->w_router[l], nullptr, D.renormalize,
+                               EMOE_PATH_AUTO, moe_y, moe_ws, L.moe_ws_bytes, stream, stats)))
+      return st;
+    delta = moe_y;
+  }
+  DEC_LAUNCH(add_rmsnorm_kernel, dim3(T), dim3(kThreads), 0, stream, d, xa, delta, dec->final_norm,
+             D.rms_eps, n);
+  if ((st = dense(dec, 1, D.vocab, d, n + (size_t)(T - 1) * d, dec->lm_head, nullptr, logits, true)))
+    return st;
+  DEC_LAUNCH(argmax_kernel, dim3(1), dim3(1024), 0, stream, D.vocab, logits, next_token);
+  return EMOE_OK;
+}
+
+}  // extern "C"
