@@ -38,7 +38,7 @@ extern "C" {
 typedef struct emoe_decoder_dims {
   int32_t n_layers;       /* L sparse decoder layers */
   int32_t n_heads;        /* H attention heads; moe.d_model = H * head_dim */
-  int32_t head_dim;       /* Dh, even, at most 256 */
+  int32_t head_dim;       /* Dh: 64, 128 or 256 */
   int32_t vocab;          /* V */
   int32_t max_positions;  /* KV-cache length, <= EMOE_DECODER_MAX_POSITIONS */
   float rope_base;        /* rotary base (e.g. 10000) */

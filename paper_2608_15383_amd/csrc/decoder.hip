@@ -155,39 +155,45 @@ __global__ __launch_bounds__(kThreads) void rope_kv_kernel(int H, int Dh, int po
 // Causal attention of token t (position pos0 + t), head h, over cache
 // positions 0 .. pos0 + t: scores q.k / sqrt(Dh) (bf16 products summed in
 // fp32), softmax in fp32, output bf16.  One workgroup per (head, token).
-__global__ __launch_bounds__(kThreads) void attention_kernel(int H, int Dh, int pos0,
-                                                             const uint16_t* qkv,
+// Scores: a thread per key, the key row's 16-byte chunks all loaded before
+// use.  Output: a thread per (8-dimension chunk, key stripe), 16-byte value
+// loads, the stripes' partial sums added in stripe order.
+template <int kDh>
+__global__ __launch_bounds__(kThreads) void attention_kernel(int H, int pos0, const uint16_t* qkv,
                                                              const uint16_t* k_cache,
                                                              const uint16_t* v_cache,
                                                              uint16_t* out) {
+  constexpr int kChunks = kDh / 8;
+  constexpr int kStripes = kThreads / kChunks;
   __shared__ float score[EMOE_DECODER_MAX_POSITIONS];
-  __shared__ uint32_t qs[kMaxHeadDim / 2];
-  __shared__ float part[kThreads];
+  __shared__ uint32_t qs[kDh / 2];
+  __shared__ float part[kStripes][kDh];
   __shared__ float red[4];
   const int h = blockIdx.x, t = blockIdx.y;
-  const int d = H * Dh;
+  const int d = H * kDh;
   const int n = pos0 + t + 1;
-  const uint16_t* q = qkv + (int64_t)t * 3 * d + h * Dh;
-  for (int i = threadIdx.x; i < Dh / 2; i += kThreads)
+  const uint16_t* q = qkv + (int64_t)t * 3 * d + h * kDh;
+  for (int i = threadIdx.x; i < kDh / 2; i += kThreads)
     qs[i] = reinterpret_cast<const uint32_t*>(q)[i];
   __syncthreads();
-  const float scale = 1.0f / sqrtf((float)Dh);
+  const float scale = 1.0f / sqrtf((float)kDh);
   float mx = -INFINITY;
   for (int j = threadIdx.x; j < n; j += kThreads) {
-    const uint4* kr = reinterpret_cast<const uint4*>(k_cache + (int64_t)j * d + h * Dh);
-    float acc = 0.f;
-    for (int c = 0; c < Dh / 8; ++c) {
-      const uint4 kv = kr[c];
-      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, kv.x),
-                                            __builtin_bit_cast(bf16x2_t, qs[4 * c]), acc, false);
-      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, kv.y),
-                                            __builtin_bit_cast(bf16x2_t, qs[4 * c + 1]), acc, false);
-      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, kv.z),
-                                            __builtin_bit_cast(bf16x2_t, qs[4 * c + 2]), acc, false);
-      acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, kv.w),
-                                            __builtin_bit_cast(bf16x2_t, qs[4 * c + 3]), acc, false);
+    const uint4* kr = reinterpret_cast<const uint4*>(k_cache + (int64_t)j * d + h * kDh);
+    uint4 kv[kChunks];
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) kv[c] = kr[c];
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      const uint32_t kw[4] = {kv[c].x, kv[c].y, kv[c].z, kv[c].w};
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+        acc[p] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, kw[p]),
+                                                 __builtin_bit_cast(bf16x2_t, qs[4 * c + p]),
+                                                 acc[p], false);
     }
-    const float s = acc * scale;
+    const float s = ((acc[0] + acc[1]) + (acc[2] + acc[3])) * scale;
     score[j] = s;
     mx = fmaxf(mx, s);
   }
@@ -199,20 +205,40 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(int H, int Dh, int 
     sum += e;
   }
   sum = block_sum(sum, red);  // its barriers also publish score[]
-  // Output: thread -> (dimension, key stripe); stripes summed in order.
-  const int stripes = kThreads / Dh;
-  const int dim = threadIdx.x % Dh, stripe = threadIdx.x / Dh;
-  float acc = 0.f;
-  if (stripe < stripes) {
-    const uint16_t* vcol = v_cache + h * Dh + dim;
-    for (int j = stripe; j < n; j += stripes) acc = fmaf(score[j], bf16_to_f32(vcol[(int64_t)j * d]), acc);
+  const int chunk = threadIdx.x % kChunks, stripe = threadIdx.x / kChunks;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const uint16_t* vcol = v_cache + h * kDh + chunk * 8;
+  int j = stripe;
+  for (; j + kStripes < n; j += 2 * kStripes) {  // two keys' loads in flight
+    const uint4 a = *reinterpret_cast<const uint4*>(vcol + (int64_t)j * d);
+    const uint4 b = *reinterpret_cast<const uint4*>(vcol + (int64_t)(j + kStripes) * d);
+    const float pa = score[j], pb = score[j + kStripes];
+    const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      acc[2 * p] = fmaf(pa, bf16_to_f32(aw[p] & 0xffffu), acc[2 * p]);
+      acc[2 * p + 1] = fmaf(pa, bf16_to_f32(aw[p] >> 16), acc[2 * p + 1]);
+      acc[2 * p] = fmaf(pb, bf16_to_f32(bw[p] & 0xffffu), acc[2 * p]);
+      acc[2 * p + 1] = fmaf(pb, bf16_to_f32(bw[p] >> 16), acc[2 * p + 1]);
+    }
   }
-  part[threadIdx.x] = acc;
+  if (j < n) {
+    const uint4 a = *reinterpret_cast<const uint4*>(vcol + (int64_t)j * d);
+    const float pa = score[j];
+    const uint32_t aw[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      acc[2 * p] = fmaf(pa, bf16_to_f32(aw[p] & 0xffffu), acc[2 * p]);
+      acc[2 * p + 1] = fmaf(pa, bf16_to_f32(aw[p] >> 16), acc[2 * p + 1]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) part[stripe][chunk * 8 + e] = acc[e];
   __syncthreads();
-  if (threadIdx.x < Dh) {
+  for (int i = threadIdx.x; i < kDh; i += kThreads) {
     float o = 0.f;
-    for (int s = 0; s < stripes; ++s) o += part[s * Dh + threadIdx.x];
-    out[(int64_t)t * d + h * Dh + threadIdx.x] = (uint16_t)f32_to_bf16_rne(o / sum);
+    for (int st = 0; st < kStripes; ++st) o += part[st][i];
+    out[(int64_t)t * d + h * kDh + i] = (uint16_t)f32_to_bf16_rne(o / sum);
   }
 }
 
@@ -261,12 +287,12 @@ int32_t check_decoder_dims(const emoe_decoder_dims* dd) {
   const int32_t st = emoe_check_dims(&dd->moe);
   if (st) return st;
   const int d = dd->moe.d_model;
-  if (dd->n_layers < 1 || dd->n_heads < 1 || dd->head_dim < 8 || dd->head_dim % 8 ||
-      dd->head_dim > kMaxHeadDim || dd->n_heads * dd->head_dim != d)
+  const int dh = dd->head_dim;
+  if (dd->n_layers < 1 || dd->n_heads < 1 || (dh != 64 && dh != 128 && dh != 256) ||
+      dd->n_heads * dh != d)
     return report_error(EMOE_ESHAPE,
-                        "need n_layers >= 1 and n_heads * head_dim == d_model with head_dim a "
-                        "multiple of 8 up to %d (got %d x %d for d_model %d)",
-                        kMaxHeadDim, dd->n_heads, dd->head_dim, d);
+                        "need n_layers >= 1 and n_heads * head_dim == d_model with head_dim "
+                        "64, 128 or 256 (got %d x %d for d_model %d)", dd->n_heads, dh, d);
   if (d > 8 * kThreads * 4) return report_error(EMOE_ESHAPE, "d_model %d above %d", d, 8 * kThreads * 4);
   if (dd->vocab < 1) return report_error(EMOE_ESHAPE, "vocab %d < 1", dd->vocab);
   if (dd->max_positions < 1 || dd->max_positions > EMOE_DECODER_MAX_POSITIONS)
@@ -440,8 +466,15 @@ int32_t emoe_decoder_forward(emoe_decoder* dec, const int32_t* tokens, int32_t T
     if ((st = dense(dec, T, 3 * d, d, n, dec->wqkv[l], nullptr, qkv, false))) return st;
     DEC_LAUNCH(rope_kv_kernel, dim3(T), dim3(kThreads), 0, stream, H, Dh, pos0, D.rope_base, qkv,
                kc, vc);
-    DEC_LAUNCH(attention_kernel, dim3(H, T), dim3(kThreads), 0, stream, H, Dh, pos0, qkv, kc, vc,
-               attn);
+    if (Dh == 64)
+      DEC_LAUNCH(attention_kernel<64>, dim3(H, T), dim3(kThreads), 0, stream, H, pos0, qkv, kc, vc,
+                 attn);
+    else if (Dh == 128)
+      DEC_LAUNCH(attention_kernel<128>, dim3(H, T), dim3(kThreads), 0, stream, H, pos0, qkv, kc,
+                 vc, attn);
+    else
+      DEC_LAUNCH(attention_kernel<256>, dim3(H, T), dim3(kThreads), 0, stream, H, pos0, qkv, kc,
+                 vc, attn);
     if ((st = dense(dec, T, d, d, attn, dec->wo[l], xa, xb, false))) return st;  // x += attn Wo^T
     std::swap(xa, xb);
     DEC_LAUNCH(add_rmsnorm_kernel, dim3(T), dim3(kThreads), 0, stream, d, xa, nullptr,
