@@ -68,7 +68,8 @@ def parse():
     p.add_argument("--steps", type=int, default=None)
     p.add_argument("--warmup", type=int, default=None)
     p.add_argument("--workload", default="decode",
-                   choices=["decode", "prefill", "multiwave", "stack", "frontier", "decoder", "copy"])
+                   choices=["decode", "decode_t4", "prefill", "multiwave", "stack", "frontier",
+                            "decoder", "copy"])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-prefill", action="store_true",
                    help="decode only: skip the prefill sub-record")
@@ -190,17 +191,22 @@ def single_thread_rate(call, budget_s):
         return timed_calls(call, budget_s)
 
 
-def measure_resident(api, torch, dm, T, steps, warmup, n_banks, keep_first_weights=False):
+def measure_resident(api, torch, dm, T, steps, warmup, n_banks, keep_first_weights=False,
+                     prebuilt=None):
     """Time T-token layer calls over n_banks fully resident expert banks
     (rotated call by call) and the dominant kernel of a separate profiled
-    pass.  Returns a dict (and bank-0 weights when asked, for the oracle)."""
+    pass.  Returns a dict (and bank-0 weights when asked, for the oracle).
+    prebuilt: (banks, caches) of an earlier call, reused instead of new banks."""
     gen = torch.Generator(device="cuda").manual_seed(7)
     wr = (torch.randn((N_EXPERTS, D_MODEL), dtype=torch.bfloat16, device="cuda", generator=gen) * 0.02)
     h = torch.randn((T, D_MODEL), dtype=torch.bfloat16, device="cuda", generator=gen)
     y = torch.empty_like(h)
     ws = torch.empty(api.workspace_bytes(dm, T), dtype=torch.uint8, device="cuda")
     banks, caches, keep_weights = [], [], None
-    for b in range(n_banks):
+    if prebuilt is not None:
+        banks, caches = prebuilt
+        n_banks = len(caches)
+    for b in range(n_banks if prebuilt is None else 0):
         bank, cache, weights = make_bank(api, dm, torch, 1000 + b)
         banks.append(bank)
         caches.append(cache)
@@ -255,10 +261,12 @@ def measure_resident(api, torch, dm, T, steps, warmup, n_banks, keep_first_weigh
         k_flops = P * 2 * D_FF * D_MODEL
     else:
         k_bytes, k_flops = alg_bytes, flops
+    # the fused decode kernel's counters are recorded per token count
+    tkey = f"{dominant}_t{T}" if dominant == "decode_fused" and T != 1 else dominant
     if T <= 4 or "gemv" in dominant:
         ach = k_bytes / dur_s / 1e9
         roof = dict(bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s", frac=ach / HBM_PEAK_GBS,
-                    traffic=measured_traffic(dominant), kernel=dominant,
+                    traffic=measured_traffic(tkey), kernel=dominant,
                     alg_bytes_per_launch=k_bytes)
     else:
         ach = k_flops / dur_s / 1e12
@@ -281,8 +289,8 @@ def bench_layer(args):
 
     torch.cuda.init()
     dm = api.dims(D_MODEL, D_FF, N_EXPERTS, TOP_K)
-    decode = args.workload == "decode"
-    T = 1 if decode else 2048
+    decode = args.workload in ("decode", "decode_t4")
+    T = 4 if args.workload == "decode_t4" else 1 if decode else 2048
     steps = args.steps or (400 if decode else 50)
     warmup = args.warmup if args.warmup is not None else (40 if decode else 5)
     n_banks = 16 if decode else 2
@@ -318,6 +326,8 @@ def bench_layer(args):
         out["graph_replay"] = dict(us_per_call=us, gbs=alg_bytes / (us * 1e-6) / 1e9,
                                    calls_per_graph=n_banks, equals_eager=same)
         log(f"graph replay: {us:.2f} us per call, equal to eager: {same}")
+        if T == 1:
+            out["decode_t4"] = decode_t4_record(api, torch, dm, m["banks"], caches)
     # Every bounded wait of the fused decode launch must have been met: a
     # timeout would mean some call's output is invalid (it is written as NaN).
     out["sync_timeouts"] = timeouts_of(caches)
@@ -341,12 +351,26 @@ def bench_layer(args):
             cpu["sample"] += "; 8 tokens of the 2048-token batch"
         out["cpu_baseline"] = cpu
     del m, caches
-    if decode and not args.no_prefill:
+    if T == 1 and not args.no_prefill:
         out["prefill"] = prefill_record(api, torch, dm)
     if out["sync_timeouts"]:
         print(json.dumps(out), file=sys.stderr, flush=True)
         sys.exit(f"{out['sync_timeouts']} bounded device waits gave up: results invalid")
     print(json.dumps(out), flush=True)
+
+
+def decode_t4_record(api, torch, dm, banks, caches, steps=200, warmup=20):
+    """Decode with four tokens per call (every expert resident, the same
+    rotated banks): per-call time, tokens/s and the fused kernel's roofline."""
+    m = measure_resident(api, torch, dm, 4, steps, warmup, len(caches), prebuilt=(banks, caches))
+    sec = m["ms"] * 1e-3
+    rec = dict(workload="olmoe_decode_t4", tokens=4, steps=steps, warmup=warmup,
+               us_per_call=m["ms"] * 1e3, distinct_experts=m["n_distinct"],
+               alg_bytes_per_call=m["alg_bytes"], gbs=m["alg_bytes"] / sec / 1e9,
+               tokens_per_s=4 / sec, roofline=m["roofline"], kernels=m["kern"])
+    log(f"decode T=4: {rec['us_per_call']:.2f} us per call, {rec['gbs']:.0f} GB/s")
+    del m
+    return rec
 
 
 def prefill_record(api, torch, dm, steps=20, warmup=3):

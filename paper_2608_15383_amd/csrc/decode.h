@@ -61,8 +61,11 @@ struct DecodeArgs {
   float* pair_out;
   uint16_t* y;
   DecodeSync* sync;
-  // Filled by decode_fused_plan / launch_decode_fused.
-  int n_router, n_gate, n_down;
+  // Filled by decode_fused_plan / launch_decode_fused.  Workgroup
+  // n_router + j runs gate/up item j (j < n_gate) and then down unit
+  // j - down0 (0 <= j - down0 < n_down); n_work such workers follow the
+  // router workgroups.
+  int n_router, n_gate, n_down, down0, n_work;
   int pairs_per_item;             // gate/up row-block pairs per gate item
   uint32_t epoch;                 // this launch's tag; 0: read it from DecodeSync
 };

@@ -7,15 +7,23 @@
 // layer's 26 MB of packed weights.  The six-kernel sequence is therefore
 // replaced by one grid whose workgroups play three roles by index:
 //   [0, nR)        router items: logits of 4 experts for every token;
-//   [nR, nR+nG)    gate/up items (one token-expert pair, row-block pairs);
-//   [nR+nG, ...)   down items (output row-block rb of every token).
-// Every gate/up and down workgroup waits for the router items, reads the
-// logits and runs the top-k itself (cheap, and it saves the round trips of
-// publishing the selection); gate/up items stage the token rows in LDS while
-// they wait.  Down items prefetch their down tiles while the gate/up items
-// stream theirs, pick up each activation row as it is produced, and add the
-// k expert outputs of each token in rank order.  Down item 0 finally writes
-// the routing and grouping arrays to the workspace, as the unfused path does.
+//   [nR, nR+nW)    workers: worker j runs gate/up item j (one token-expert
+//                  pair, some row-block pairs; items in token-major order),
+//                  if j < nG, and then down unit j - D0 (output row block rb
+//                  of one token t), if that is in [0, T * d/16).
+// D0 places every down unit of token t after the last gate/up item of t, so
+// a workgroup only ever waits for workgroups of lower index.  With one token
+// the two ranges are disjoint (D0 = nG); with more tokens the later gate/up
+// workers take a down unit of an earlier token afterwards, which spreads the
+// down work over many more workgroups than the d/16 row blocks.
+// Every worker waits for the router items, reads the logits and runs the
+// top-k itself (cheap, and it saves the round trips of publishing the
+// selection); gate/up items stage the token rows in LDS while they wait.
+// Down-only workers prefetch their down tiles while the gate/up items stream
+// theirs; every down unit picks up each activation row of its token as it is
+// produced and adds the token's k expert outputs in rank order.  Down unit 0
+// finally writes the routing and grouping arrays to the workspace, as the
+// unfused path does.
 //
 // Data crossing workgroups (logits, activation rows) travels as 64-bit words
 // tagged with the launch's epoch, written and read device-coherently: the
@@ -229,7 +237,10 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   // Gate/up workgroups stage the token rows of h in LDS (s_act, which only
   // down workgroups use otherwise) while the router runs: 256-byte chunks
   // round-robin over the wavefronts.
-  const bool is_gate = blk < a.n_router + a.n_gate;
+  const int wk = blk - a.n_router;  // worker index
+  const bool is_gate = wk < a.n_gate;
+  const int unit = wk - a.down0;    // down unit (valid when is_down)
+  const bool is_down = unit >= 0 && unit < a.n_down;
   const uint16_t* h_lds = reinterpret_cast<const uint16_t*>(s_act);
   if (is_gate) {
     const uint32_t bytes = (uint32_t)a.tokens * (uint32_t)a.d * 2u;
@@ -280,11 +291,17 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   const uint32_t ep = kDevEpoch ? __builtin_amdgcn_readfirstlane(epoch) : a.epoch;
   if (kDevEpoch && !is_gate && tid == 0) arrive(sy, ep, blk);
 
+  // The mixture weights are needed only by the combine.  A worker that also
+  // runs a gate/up item computes them first (so the selection need not stay
+  // in registers through it); a down-only worker while its tiles stream in.
+  if (is_gate && is_down && wi < a.tokens)
+    wave_topk_weights<false>(st, a.n_experts, a.top_k, a.renormalize, s_w + wi * a.top_k);
+
   if (is_gate) {
     // ---------------------------------------------------------------- gate/up
     // Item = (pair pi, row-block pairs b0 ..): one token row of one expert.
     // The activation goes to act row pi (pair order).
-    const int item = blk - a.n_router;
+    const int item = wk;
     const int pairs_of_f = a.f / kTileRows;
     const int chunks = (pairs_of_f + a.pairs_per_item - 1) / a.pairs_per_item;
     const int pi = item / chunks;
@@ -305,22 +322,26 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                   });
     if (kDevEpoch && tid == 0) arrive(sy, ep, blk);
-    return;
+    if (!is_down) return;
+    __syncthreads();  // the staged token rows are no longer read: s_act is free
   }
 
   // ------------------------------------------------------------------ down + combine
-  const int rb = blk - a.n_router - a.n_gate;
+  // Unit = (token tu, output row block rb): the token's k pairs p0 .. p1-1.
+  const int n_rb = a.d / kTileRows;
+  const int tu = unit / n_rb;
+  const int rb = unit - tu * n_rb;
+  const int p0 = tu * a.top_k, p1 = p0 + a.top_k;
   const int G = a.f / kGroup;
-  // Wavefront wi owns pairs wi, wi+4, ...; the first two are prefetched.
+  // Wavefront wi owns pairs p0+wi, p0+wi+4, ...; the first two are prefetched
+  // (by a down-only worker while the gate/up items stream).
   DownBatch pre0, pre1;
-  if (wi < P)
-    down_load_batch(a.slot_bank + (int64_t)s_ids[wi] * a.record_bytes, a.d, a.f, rb, 0, pre0);
-  if (wi + kGemvWaves < P)
-    down_load_batch(a.slot_bank + (int64_t)s_ids[wi + kGemvWaves] * a.record_bytes, a.d, a.f, rb,
-                    0, pre1);
-  // The mixture weights are needed only by the combine: compute them while
-  // the tiles stream in.
-  if (wi < a.tokens)
+  if (p0 + wi < p1)
+    down_load_batch(a.slot_bank + (int64_t)s_ids[p0 + wi] * a.record_bytes, a.d, a.f, rb, 0, pre0);
+  if (p0 + wi + kGemvWaves < p1)
+    down_load_batch(a.slot_bank + (int64_t)s_ids[p0 + wi + kGemvWaves] * a.record_bytes, a.d, a.f,
+                    rb, 0, pre1);
+  if (!is_gate && wi < a.tokens)
     wave_topk_weights<false>(st, a.n_experts, a.top_k, a.renormalize, s_w + wi * a.top_k);
 
   // Each wavefront stages the activation row of the pair it is computing in
@@ -370,31 +391,30 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     act_late |= wave_stage_act_row(sy, a, ep, pi, act_lds32);
     xs_sums(pi, 0, G);
   };
-  if (wi < P) {
-    stage(wi);
-    pair_output(wi, pre0, true);
+  if (p0 + wi < p1) {
+    stage(p0 + wi);
+    pair_output(p0 + wi, pre0, true);
   }
-  if (wi + kGemvWaves < P) {
-    stage(wi + kGemvWaves);
-    pair_output(wi + kGemvWaves, pre1, true);
+  if (p0 + wi + kGemvWaves < p1) {
+    stage(p0 + wi + kGemvWaves);
+    pair_output(p0 + wi + kGemvWaves, pre1, true);
   }
-  for (int pi = wi + 2 * kGemvWaves; pi < P; pi += kGemvWaves) {
+  for (int pi = p0 + wi + 2 * kGemvWaves; pi < p1; pi += kGemvWaves) {
     stage(pi);
     pair_output(pi, pre0, false);
   }
   if (lane == 0) s_late[1][wi] = act_late;
   __syncthreads();
-  if (tid < 16 * a.tokens) {
-    const int t = tid >> 4, n = tid & 15;
+  if (tid < 16) {
+    const int n = tid;
     float acc = 0.f;
-    for (int j = 0; j < a.top_k; ++j)
-      acc = fmaf(s_w[t * a.top_k + j], o_lds[t * a.top_k + j][n], acc);
+    for (int j = 0; j < a.top_k; ++j) acc = fmaf(s_w[p0 + j], o_lds[p0 + j][n], acc);
     const bool late_any =
         route_late | s_late[1][0] | s_late[1][1] | s_late[1][2] | s_late[1][3];
-    a.y[(int64_t)t * a.d + 16 * rb + n] = late_any ? 0x7fc0 : (uint16_t)f32_to_bf16_rne(acc);
+    a.y[(int64_t)tu * a.d + 16 * rb + n] = late_any ? 0x7fc0 : (uint16_t)f32_to_bf16_rne(acc);
   }
 
-  if (rb == 0) {
+  if (unit == 0) {
     // The workspace's routing and grouping arrays, as the unfused path writes them.
     for (int j = tid; j < P; j += 256) {
       a.topk_ids[j] = s_ids[j];
@@ -436,17 +456,26 @@ bool decode_fused_plan(DecodeArgs& a) {
   if ((int64_t)kGemvWaves * a.f * 2 > kFusedActLdsBytes) return false;  // a row per wavefront
   if ((int64_t)a.tokens * a.top_k * (a.f / 2) > kFusedActWords) return false;
   if ((int64_t)a.tokens * a.d * 2 > kFusedActLdsBytes) return false;  // staged token rows
-  const int P = a.tokens * a.top_k;
+  const int T = a.tokens;
   const int pairs_of_f = a.f / kTileRows;
+  const int n_rb = a.d / kTileRows;
   a.n_router = a.logits_override ? 1 : (a.n_experts + 3) / 4;
-  a.n_down = a.d / kTileRows;
-  const int cap = fused_capacity();
+  a.n_down = T * n_rb;
+  const int cap = min(fused_capacity(), kFusedMaxBlocks);
+  // The most gate/up items (fewest row-block pairs each) that fit.  Token t's
+  // items are workers [t*It, (t+1)*It); its down units start at worker
+  // D0 + t*n_rb, which must not come before (t+1)*It.
   for (int ppi = 1; ppi <= pairs_of_f; ppi *= 2) {
     const int chunks = (pairs_of_f + ppi - 1) / ppi;
-    const int n_gate = P * chunks;
-    if (a.n_router + n_gate + a.n_down <= min(cap, kFusedMaxBlocks)) {
+    const int It = a.top_k * chunks;
+    int down0 = It;
+    for (int t = 1; t < T; ++t) down0 = max(down0, (t + 1) * It - t * n_rb);
+    const int n_work = max(T * It, down0 + a.n_down);
+    if (a.n_router + n_work <= cap) {
       a.pairs_per_item = ppi;
-      a.n_gate = n_gate;
+      a.n_gate = T * It;
+      a.down0 = down0;
+      a.n_work = n_work;
       return true;
     }
   }
@@ -462,7 +491,7 @@ hipError_t launch_decode_fused(DecodeArgs& a, DecodeProgress& prog, hipStream_t 
   } else {
     a.epoch = 0u;  // replays number themselves in device memory
   }
-  const dim3 grid(a.n_router + a.n_gate + a.n_down);
+  const dim3 grid(a.n_router + a.n_work);
   if (a.epoch != 0u)
     launch(decode_fused_kernel<false>, grid, dim3(256), stream, a);
   else

@@ -91,43 +91,62 @@ __device__ __forceinline__ double wave_sum_f64_dpp(double v) {
   return __hiloint2double(hi, lo);
 }
 
-// Logit sums of expert e for each token by one wavefront, token after token,
-// with every load of a pass issued before any is used: lanes take 8-input
-// chunks k = 8*lane + 512*i, up to four chunks (2048 inputs) per pass, so a
-// token with d <= 2048 costs one memory round trip.  Chunks past d are read
-// at a clamped in-bounds address and contribute 0.  Products of bf16 values
-// are exact in fp64 and so, at these magnitudes, is the sum, whatever its
-// order.  store(t, sum) receives each token's sum (the same in every lane).
+// Logit sums of expert e for kT consecutive tokens by one wavefront, with
+// every load of a pass issued before any is used: lanes take 8-input chunks
+// k = 8*lane + 512*i, up to four chunks (2048 inputs) per pass and token, so
+// the kT tokens with d <= 2048 cost one memory round trip together.
+// Chunks past d are read at a clamped in-bounds address and contribute 0.
+// Products of bf16 values are exact in fp64 and so, at these magnitudes, is
+// the sum, whatever its order.  store(t, sum) receives each token's sum (the
+// same in every lane).
+template <int kT, typename Store>
+__device__ __forceinline__ void wave_router_dot_tokens(int t0, int d, const uint16_t* __restrict__ wrow,
+                                                       const uint16_t* __restrict__ h, Store store) {
+  const int lane = lane_id();
+  double acc[kT];
+#pragma unroll
+  for (int t = 0; t < kT; ++t) acc[t] = 0.0;
+  for (int base = 0; base < d; base += 512 * 4) {
+    uint4 w[4], x[kT][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int k = base + 512 * i + 8 * lane;
+      const int kc = k < d ? k : d - 8;
+      w[i] = *reinterpret_cast<const uint4*>(wrow + kc);
+#pragma unroll
+      for (int t = 0; t < kT; ++t)
+        x[t][i] = *reinterpret_cast<const uint4*>(h + (int64_t)(t0 + t) * d + kc);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bool ok = base + 512 * i + 8 * lane < d;
+      double wv[8];
+      bf16x8_to_f64(w[i], wv);
+#pragma unroll
+      for (int r = 0; r < 8; ++r) wv[r] = ok ? wv[r] : 0.0;
+#pragma unroll
+      for (int t = 0; t < kT; ++t) {
+        double hv[8];
+        bf16x8_to_f64(x[t][i], hv);
+#pragma unroll
+        for (int r = 0; r < 8; ++r) acc[t] = fma(hv[r], wv[r], acc[t]);
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < kT; ++t) store(t0 + t, wave_sum_f64_dpp(acc[t]));
+}
+
+// Logit sums of expert e for every token: two tokens per pass (four would
+// hold more loaded registers than the fused decode kernel has to spare).
 template <typename Store>
 __device__ __forceinline__ void wave_router_dot(int tokens, int d, int e,
                                                 const uint16_t* __restrict__ h,
                                                 const uint16_t* __restrict__ wr, Store store) {
-  const int lane = lane_id();
   const uint16_t* wrow = wr + (int64_t)e * d;
-  for (int t = 0; t < tokens; ++t) {
-    const uint16_t* hrow = h + (int64_t)t * d;
-    double acc = 0.0;
-    for (int base = 0; base < d; base += 512 * 4) {
-      uint4 w[4], x[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int k = base + 512 * i + 8 * lane;
-        const int kc = k < d ? k : d - 8;
-        w[i] = *reinterpret_cast<const uint4*>(wrow + kc);
-        x[i] = *reinterpret_cast<const uint4*>(hrow + kc);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bool ok = base + 512 * i + 8 * lane < d;
-        double wv[8], hv[8];
-        bf16x8_to_f64(w[i], wv);
-        bf16x8_to_f64(x[i], hv);
-#pragma unroll
-        for (int r = 0; r < 8; ++r) acc = fma(hv[r], ok ? wv[r] : 0.0, acc);
-      }
-    }
-    store(t, wave_sum_f64_dpp(acc));
-  }
+  int t0 = 0;
+  for (; t0 + 2 <= tokens; t0 += 2) wave_router_dot_tokens<2>(t0, d, wrow, h, store);
+  if (t0 < tokens) wave_router_dot_tokens<1>(t0, d, wrow, h, store);
 }
 
 template <int NT, int NE, bool kCo>
