@@ -9,10 +9,11 @@ namespace emoe {
 constexpr int kFusedMaxTokens = 4;   // tokens per fused call (one top-k wavefront each)
 constexpr int kFusedMaxPairs = 32;   // token-expert pairs per fused call
 constexpr int kSyncLanes = 16;       // logit replicas
-constexpr int kFusedActLdsBytes = 32768;  // LDS: the token rows (gate/up) or one activation
-                                          // row per wavefront (down)
+constexpr int kFusedActLdsBytes = 32768;  // LDS: the token rows (gate/up)
 constexpr int kFusedActWords = kFusedMaxPairs * 2048;  // activation words handed over (d_ff <= 4096)
 constexpr int kFusedMaxBlocks = 1024;  // workgroups per fused launch
+constexpr int kFusedMaxD = 4096;       // d_model of a fused launch (DecodeSync::out)
+constexpr int kFusedMaxDownUnits = 8;  // down row blocks per worker
 constexpr uint32_t kDeviceEpoch0 = 0x80000000u;  // first epoch of captured launches
 
 // Data the workgroups of one fused launch hand to each other, in device
@@ -35,6 +36,9 @@ struct DecodeSync {
   // Activation rows in pair order: word w of pair pi holds act[pi][2w .. 2w+1]
   // (bf16, low column in the low 16 bits) at pi * d_ff / 2 + w.
   uint64_t act[kFusedActWords];
+  // Expert outputs in pair order: word pi * d_model + n holds the fp32 bits of
+  // output n of pair pi (written for every pair but the last of each token).
+  uint64_t out[kFusedMaxPairs * kFusedMaxD];
   uint32_t epoch;  // tag of the next captured launch (kDeviceEpoch0 after creation)
   uint32_t pad1[15];
   // Word b: the epoch that workgroup b of the latest launch used.
@@ -62,11 +66,14 @@ struct DecodeArgs {
   uint16_t* y;
   DecodeSync* sync;
   // Filled by decode_fused_plan / launch_decode_fused.  Workgroup
-  // n_router + j runs gate/up item j (j < n_gate) and then down unit
-  // j - down0 (0 <= j - down0 < n_down); n_work such workers follow the
-  // router workgroups.
-  int n_router, n_gate, n_down, down0, n_work;
+  // n_router + j (worker j) runs gate/up item j (j < n_gate: pair j / chunks,
+  // with chunks items per pair) and then down_r output row blocks of the
+  // previous pair; the tail workers (n_gate <= j < n_work) tail_r row blocks
+  // of the last pair each.
+  int n_router, n_gate, n_work;
   int pairs_per_item;             // gate/up row-block pairs per gate item
+  int down_r, tail_r;             // down row blocks per gate/up and per tail worker
+  int gw;                         // down input groups per wavefront (template argument)
   uint32_t epoch;                 // this launch's tag; 0: read it from DecodeSync
 };
 

@@ -5,29 +5,30 @@
 // On MI355X a kernel boundary costs about 2.4 us and a dependent round trip to
 // memory about 1 us under load, against roughly 5 us to stream the decode
 // layer's 26 MB of packed weights.  The six-kernel sequence is therefore
-// replaced by one grid whose workgroups play three roles by index:
+// replaced by one grid whose workgroups play these roles by index:
 //   [0, nR)        router items: logits of 4 experts for every token;
-//   [nR, nR+nW)    workers: worker j runs gate/up item j (one token-expert
-//                  pair, some row-block pairs; items in token-major order),
-//                  if j < nG, and then down unit j - D0 (output row block rb
-//                  of one token t), if that is in [0, T * d/16).
-// D0 places every down unit of token t after the last gate/up item of t, so
-// a workgroup only ever waits for workgroups of lower index.  With one token
-// the two ranges are disjoint (D0 = nG); with more tokens the later gate/up
-// workers take a down unit of an earlier token afterwards, which spreads the
-// down work over many more workgroups than the d/16 row blocks.
+//   [nR, nR+nG)    gate/up workers: worker j runs gate/up item j (pair
+//                  p = j / chunks, some of its row-block pairs; pairs in
+//                  token-major order), then down_r output row blocks of pair
+//                  p - 1;
+//   [nR+nG, ...)   tail workers: tail_r output row blocks of the last pair.
 // Every worker waits for the router items, reads the logits and runs the
 // top-k itself (cheap, and it saves the round trips of publishing the
-// selection); gate/up items stage the token rows in LDS while they wait.
-// Down-only workers prefetch their down tiles while the gate/up items stream
-// theirs; every down unit picks up each activation row of its token as it is
-// produced and adds the token's k expert outputs in rank order.  Down unit 0
-// finally writes the routing and grouping arrays to the workspace, as the
-// unfused path does.
+// selection); gate/up workers stage the token rows in LDS while they wait.
+// Each worker loads the first down tiles of its pair while the gate/up items
+// stream theirs, picks up that pair's activation row once it is complete and
+// splits each row block's input groups over its four wavefronts.  So every
+// pair's down projection starts as soon as its own activation row is done,
+// spread over as many workgroups as gate/up items, and a pair's activations
+// come from workers of lower index than the ones that read them.  The
+// workers holding the last pair of a token then read the token's other k - 1
+// expert outputs (also from workers of lower index) and add the k outputs in
+// rank order.  The first tail worker finally writes the routing and grouping
+// arrays to the workspace, as the unfused path does.
 //
-// Data crossing workgroups (logits, activation rows) travels as 64-bit words
-// tagged with the launch's epoch, written and read device-coherently: the
-// reader polls the data itself, so one store is both the payload and the
+// Data crossing workgroups (logits, activation rows, expert outputs) travels
+// as 64-bit words tagged with the launch's epoch, written and read
+// device-coherently: the reader polls the data itself, so one store is both the payload and the
 // signal, and nothing needs resetting between launches.  The host numbers
 // launches itself; a launch captured into a graph instead takes its epoch
 // from device memory and advances it there, so that every replay has a new
@@ -49,45 +50,6 @@ namespace {
 
 constexpr uint32_t kSpinLimit = 1u << 20;
 constexpr int kPollSleep = 8;  // s_sleep units (64 clocks) between polls
-
-// Stage the activation row of pair pi from the tagged words (DecodeSync::act)
-// in LDS at dst (f bf16), reading it until every word carries this launch's
-// epoch (bounded); one wavefront.
-__device__ __forceinline__ bool wave_stage_act_row(DecodeSync* sy, const DecodeArgs& a,
-                                                   uint32_t epoch, int pi, uint32_t* dst) {
-  constexpr int kWords = 8;  // words per lane per read
-  const int lane = lane_id();
-  const int nw = a.f / 2;  // words per row, a multiple of 64
-  const uint64_t* src = sy->act + (int64_t)pi * nw;
-  bool timed_out = false;
-  for (int w0 = 0; w0 < nw; w0 += 64 * kWords) {
-    uint32_t it = 0;
-    while (true) {
-      uint64_t x[kWords];
-#pragma unroll
-      for (int k = 0; k < kWords; ++k) {
-        const int w = w0 + 64 * k + lane;
-        x[k] = w < nw ? __hip_atomic_load(src + w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                      : ((uint64_t)epoch << 32);
-      }
-      bool ok = true;
-#pragma unroll
-      for (int k = 0; k < kWords; ++k) {
-        const int w = w0 + 64 * k + lane;
-        ok = ok && (uint32_t)(x[k] >> 32) == epoch;
-        if (w < nw) dst[w] = (uint32_t)x[k];
-      }
-      if (__all(ok)) break;
-      if (++it > kSpinLimit) {
-        if (lane == 0) atomicAdd(&sy->timeouts, 1u);
-        timed_out = true;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(kPollSleep);
-    }
-  }
-  return timed_out;
-}
 
 // Token t's logits into st.v: from logits_override, or from the router
 // items' tagged words (replica `replica`), read until every word carries this
@@ -186,17 +148,54 @@ __device__ __forceinline__ void wave_copy_to_lds(const void* src, uint32_t bytes
         (int)voff, (int)off, 0, /*sc1*/ 16);
 }
 
+// Down tiles of one wavefront for up to kUnits row blocks: input groups
+// g = wi + 4j (j < kGW) of each, codes (this lane's 16 bytes of the tile) and
+// raw fp16 scales (converted at use, so no load waits for another).
+template <int kGW>
+struct DownTiles {
+  static constexpr int kUnits = 16 / kGW;  // row blocks per batch (64 code registers)
+  uint4 c[kUnits][kGW];
+  uint16_t s[kUnits][kGW];
+};
+
+// Load this wavefront's tiles of row blocks rb .. rb+nb-1 (nb <= kUnits).
+template <int kGW>
+__device__ __forceinline__ void load_down_tiles(const uint8_t* __restrict__ rec, int d, int f,
+                                                int rb, int nb, DownTiles<kGW>& t) {
+  const int lane = lane_id();
+  const int wi = threadIdx.x >> 6;
+  const int G = f / kGroup;
+  const RecordLayout L = record_layout(d, f);
+  const uint8_t* codes = rec + L.w2_codes + 16 * lane;
+  const uint16_t* sc = reinterpret_cast<const uint16_t*>(rec + L.w2_scales);
+#pragma unroll
+  for (int u = 0; u < DownTiles<kGW>::kUnits; ++u) {
+    if (u < nb) {
+      const int n = 16 * (rb + u) + (lane & 15);
+#pragma unroll
+      for (int j = 0; j < kGW; ++j) {
+        const int g = wi + 4 * j;
+        if (g < G) {
+          t.c[u][j] = *reinterpret_cast<const uint4*>(codes + ((int64_t)(rb + u) * G + g) * kTileBytes);
+          t.s[u][j] = sc[scale_index(n, g, G)];
+        }
+      }
+    }
+  }
+}
+
 // kDevEpoch: the launch is being captured into a graph and reads its epoch
 // from DecodeSync (a.epoch is 0); otherwise a.epoch is the host's number.
-template <bool kDevEpoch>
+// kGW: input groups of the down projection per wavefront (d_ff <= 512 kGW).
+template <bool kDevEpoch, int kGW>
 __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   __shared__ GroupShared<256> gsh;
   __shared__ GateUpShared gush;
-  __shared__ float o_lds[kFusedMaxPairs][16];
   __shared__ int32_t s_ids[kFusedMaxPairs];
   __shared__ float s_w[kFusedMaxPairs];
   __shared__ uint4 s_act[kFusedActLdsBytes / 16];
-  __shared__ float s_xs[kGemvWaves][kFusedActLdsBytes / (2 * kGroup * kGemvWaves) * 4];  // [wave][group][quarter]
+  __shared__ uint32_t s_xw[kGemvWaves][kGW * kGroup / 2];        // staged activations
+  __shared__ float s_part[kGemvWaves][kFusedMaxDownUnits][16];    // per-class down outputs
   __shared__ uint64_t s_topk[kFusedMaxTokens][64];                // top-k scratch per token
   __shared__ int s_rank[kGemvWaves][64];                          // partial ranks (one token)
   __shared__ int s_late[2][kGemvWaves];  // per wavefront: a bounded wait gave up (route, down)
@@ -234,13 +233,22 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     return;
   }
 
-  // Gate/up workgroups stage the token rows of h in LDS (s_act, which only
-  // down workgroups use otherwise) while the router runs: 256-byte chunks
-  // round-robin over the wavefronts.
-  const int wk = blk - a.n_router;  // worker index
+  // Worker wk runs gate/up item wk (pair p = wk / chunks, chunk wk % chunks)
+  // and then the down row blocks [rb0, rb0 + nu) of pair q = p - 1; a tail
+  // worker (wk >= n_gate) only the down row blocks of the last pair.  The
+  // workers that hold the last pair of a token combine that token's outputs.
+  const int wk = blk - a.n_router;
   const bool is_gate = wk < a.n_gate;
-  const int unit = wk - a.down0;    // down unit (valid when is_down)
-  const bool is_down = unit >= 0 && unit < a.n_down;
+  const int n_rb = a.d / kTileRows;
+  const int chunks = (a.f / kTileRows + a.pairs_per_item - 1) / a.pairs_per_item;
+  const int q = is_gate ? wk / chunks - 1 : P - 1;
+  const int rb0 = is_gate ? (wk % chunks) * a.down_r : (wk - a.n_gate) * a.tail_r;
+  const int nu = q < 0 ? 0 : max(0, min(is_gate ? a.down_r : a.tail_r, n_rb - rb0));
+  const bool is_comb = nu > 0 && q % a.top_k == a.top_k - 1;  // combines token q / k
+  const bool writes_routing = wk == a.n_gate;                  // the first tail worker
+
+  // Gate/up workers stage the token rows of h in LDS (s_act) while the router
+  // runs: 256-byte chunks round-robin over the wavefronts.
   const uint16_t* h_lds = reinterpret_cast<const uint16_t*>(s_act);
   if (is_gate) {
     const uint32_t bytes = (uint32_t)a.tokens * (uint32_t)a.d * 2u;
@@ -249,9 +257,9 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
                        reinterpret_cast<uint8_t*>(s_act) + off);
   }
 
-  // Every other workgroup: token t's logits (this launch's epoch in every tag)
-  // and its selection.  One token: wavefront 0 loads the logits and publishes
-  // the rank keys, each wavefront counts, for every expert, the larger keys in
+  // Every worker: token t's logits (this launch's epoch in every tag) and its
+  // selection.  One token: wavefront 0 loads the logits and publishes the
+  // rank keys, each wavefront counts, for every expert, the larger keys in
   // its quarter of them, and wavefront 0 adds the counts.  Several tokens:
   // wavefront t < T ranks token t alone.
   const int replica = blk % kSyncLanes;
@@ -279,6 +287,10 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     wave_topk_select_loaded(a.n_experts, a.top_k, st, s_topk[wi]);
     wave_topk_store_ids<false>(st, a.top_k, s_ids + wi * a.top_k);
   }
+  // The mixture weights, for the combining workers (their token's) and the
+  // one that writes the routing arrays (every token's).
+  if (wi < a.tokens && (writes_routing || (is_comb && wi == q / a.top_k)))
+    wave_topk_weights<false>(st, a.n_experts, a.top_k, a.renormalize, s_w + wi * a.top_k);
   if (is_gate) wait_memory();  // the staged rows
   if (lane == 0) s_late[0][wi] = late;
   __syncthreads();
@@ -286,33 +298,26 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   // outputs become NaN rather than passing as valid results.
   const bool route_late = s_late[0][0] | s_late[0][1] | s_late[0][2] | s_late[0][3];
   // A read epoch has been waited for by now (the logits' tags): from here on
-  // a scalar.  Down workgroups record it before their first tile loads, so
-  // that no later wait covers the store; gate/up workgroups at their end.
+  // a scalar.  Tail workers record it before their first tile loads, so that
+  // no later wait covers the store; gate/up workers after their item.
   const uint32_t ep = kDevEpoch ? __builtin_amdgcn_readfirstlane(epoch) : a.epoch;
   if (kDevEpoch && !is_gate && tid == 0) arrive(sy, ep, blk);
+  const uint64_t tag = (uint64_t)ep << 32;
 
-  // The mixture weights are needed only by the combine.  A worker that also
-  // runs a gate/up item computes them first (so the selection need not stay
-  // in registers through it); a down-only worker while its tiles stream in.
-  if (is_gate && is_down && wi < a.tokens)
-    wave_topk_weights<false>(st, a.n_experts, a.top_k, a.renormalize, s_w + wi * a.top_k);
 
   if (is_gate) {
     // ---------------------------------------------------------------- gate/up
     // Item = (pair pi, row-block pairs b0 ..): one token row of one expert.
     // The activation goes to act row pi (pair order).
-    const int item = wk;
+    const int pi = wk / chunks;
     const int pairs_of_f = a.f / kTileRows;
-    const int chunks = (pairs_of_f + a.pairs_per_item - 1) / a.pairs_per_item;
-    const int pi = item / chunks;
-    const int b0 = (item % chunks) * a.pairs_per_item;
+    const int b0 = (wk % chunks) * a.pairs_per_item;
     const int b1 = min(b0 + a.pairs_per_item, pairs_of_f);
     const int e = s_ids[pi];
     const int top_k = a.top_k;
     // The activation goes out as tagged words (DecodeSync::act), which the
-    // down workgroups poll directly: the store is the signal.
+    // down workers poll directly: the store is the signal.
     const int d = a.d, f = a.f;
-    const uint64_t tag = (uint64_t)ep << 32;
     const uint32_t nan_mask = route_late ? 0x7fc07fc0u : 0u;  // bf16 NaN pair
     uint64_t* act_tag = sy->act;
     for (int b = b0; b < b1; ++b)
@@ -322,99 +327,150 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                   });
     if (kDevEpoch && tid == 0) arrive(sy, ep, blk);
-    if (!is_down) return;
-    __syncthreads();  // the staged token rows are no longer read: s_act is free
   }
 
-  // ------------------------------------------------------------------ down + combine
-  // Unit = (token tu, output row block rb): the token's k pairs p0 .. p1-1.
-  const int n_rb = a.d / kTileRows;
-  const int tu = unit / n_rb;
-  const int rb = unit - tu * n_rb;
-  const int p0 = tu * a.top_k, p1 = p0 + a.top_k;
+  // ------------------------------------------------------------------ down
+  // The down tiles of pair q: wavefront wi takes the input groups g = wi + 4j
+  // (j < kGW) of every row block.  A tail worker reaches this point right
+  // after its top-k, so its first batch streams in while the gate/up items
+  // stream theirs; a gate/up worker after its item (loads issued before the
+  // item's would be waited for with them).
   const int G = a.f / kGroup;
-  // Wavefront wi owns pairs p0+wi, p0+wi+4, ...; the first two are prefetched
-  // (by a down-only worker while the gate/up items stream).
-  DownBatch pre0, pre1;
-  if (p0 + wi < p1)
-    down_load_batch(a.slot_bank + (int64_t)s_ids[p0 + wi] * a.record_bytes, a.d, a.f, rb, 0, pre0);
-  if (p0 + wi + kGemvWaves < p1)
-    down_load_batch(a.slot_bank + (int64_t)s_ids[p0 + wi + kGemvWaves] * a.record_bytes, a.d, a.f,
-                    rb, 0, pre1);
-  if (!is_gate && wi < a.tokens)
-    wave_topk_weights<false>(st, a.n_experts, a.top_k, a.renormalize, s_w + wi * a.top_k);
-
-  // Each wavefront stages the activation row of the pair it is computing in
-  // its own slot of s_act (f bf16), one pair after another.
-  const int slot = __builtin_amdgcn_readfirstlane(wi);  // uniform: scalar slot addresses
-  const uint16_t* act_lds = reinterpret_cast<const uint16_t*>(s_act) + slot * a.f;
-  uint32_t* act_lds32 = reinterpret_cast<uint32_t*>(s_act) + slot * (a.f / 2);
-  float* xs_w = s_xs[slot];
-  // Per-(group, quarter) activation sums of pair pi, groups [g0, g1).
-  auto xs_sums = [&](int pi, int g0, int g1) {
-    for (int i = 4 * g0 + lane; i < 4 * g1; i += 64) {
-      const int g = i >> 2, q = i & 3;
-      uint4 x[4];
-#pragma unroll
-      for (int k = 0; k < 4; ++k)
-        x[k] = *reinterpret_cast<const uint4*>(act_lds + g * kGroup + 8 * q + 32 * k);
-      xs_w[i] = lane_group_xsum(x);
-    }
-  };
-  // Expert output of pair pi for this row block from its staged activation
-  // row; `first` is its first batch of tiles (prefetched when has_first).
-  auto pair_output = [&](int pi, DownBatch first, bool has_first) {
-    const uint8_t* rec = a.slot_bank + (int64_t)s_ids[pi] * a.record_bytes;
-    auto xload = [&](int, int k) {
-      return *reinterpret_cast<const uint4*>(act_lds + k);
-    };
-    auto xsload = [&](int, int g) { return xs_w[g * 4 + (lane >> 4)]; };
-    float acc[kTokChunk] = {0.f, 0.f, 0.f, 0.f};
-    if (!has_first) down_load_batch(rec, a.d, a.f, rb, 0, first);
-    down_apply_batch_xs(first, a.f, 0, xload, xsload, 1, acc);
-    for (int g0 = kDownBatch; g0 < G; g0 += kDownBatch) {
-      DownBatch bt;
-      down_load_batch(rec, a.d, a.f, rb, g0, bt);
-      down_apply_batch_xs(bt, a.f, g0, xload, xsload, 1, acc);
-    }
-    const float o = reduce_quarters(acc[0]);
-    if (lane < 16) {
-      o_lds[pi][lane] = o;
-      a.pair_out[(int64_t)pi * a.d + 16 * rb + lane] = o;
-    }
-  };
-  // Pair by pair as each activation row arrives (its first two pairs'
-  // tiles are prefetched), so computing one pair overlaps the wait for the
-  // next.
   bool act_late = false;
-  auto stage = [&](int pi) {
-    act_late |= wave_stage_act_row(sy, a, ep, pi, act_lds32);
-    xs_sums(pi, 0, G);
-  };
-  if (p0 + wi < p1) {
-    stage(p0 + wi);
-    pair_output(p0 + wi, pre0, true);
-  }
-  if (p0 + wi + kGemvWaves < p1) {
-    stage(p0 + wi + kGemvWaves);
-    pair_output(p0 + wi + kGemvWaves, pre1, true);
-  }
-  for (int pi = p0 + wi + 2 * kGemvWaves; pi < p1; pi += kGemvWaves) {
-    stage(pi);
-    pair_output(pi, pre0, false);
+  if (nu > 0) {
+    const uint8_t* drec = a.slot_bank + (int64_t)s_ids[q] * a.record_bytes;
+    using Tiles = DownTiles<kGW>;
+    Tiles cur;
+    load_down_tiles<kGW>(drec, a.d, a.f, rb0, min(nu, Tiles::kUnits), cur);
+    // This wavefront's groups of activation row q, from the tagged words
+    // (one per lane and group, all read before any is checked; bounded wait)
+    // into its LDS slot.
+    uint32_t* xw = s_xw[wi];
+    const uint64_t* src = sy->act + (int64_t)q * (a.f / 2);
+    uint32_t it = 0;
+    while (wi < G) {  // a wavefront without groups (d_ff < 512) has nothing to read
+      uint64_t x[kGW];
+#pragma unroll
+      for (int j = 0; j < kGW; ++j)  // slots past G read group wi's words again
+        x[j] = __hip_atomic_load(src + (wi + 4 * j < G ? wi + 4 * j : wi) * (kGroup / 2) + lane,
+                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      bool ok = true;
+#pragma unroll
+      for (int j = 0; j < kGW; ++j) {
+        ok &= (uint32_t)(x[j] >> 32) == ep;
+        xw[j * (kGroup / 2) + lane] = (uint32_t)x[j];
+      }
+      if (__all(ok)) break;
+      if (++it > kSpinLimit) {
+        if (lane == 0) atomicAdd(&sy->timeouts, 1u);
+        act_late = true;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(kPollSleep);
+    }
+    __builtin_amdgcn_wave_barrier();
+    const uint16_t* xh = reinterpret_cast<const uint16_t*>(xw);
+    const int quarter = lane >> 4;
+    // The lane's 32 activations of group slot j (4 x uint4).
+    auto xload = [&](int j, uint4* x) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        x[i] = *reinterpret_cast<const uint4*>(xh + j * kGroup + 8 * quarter + 32 * i);
+    };
+    float xs[kGW];
+#pragma unroll
+    for (int j = 0; j < kGW; ++j) {
+      uint4 x[4];
+      xload(j, x);
+      xs[j] = lane_group_xsum(x);
+    }
+    // Batches of Tiles::kUnits row blocks (one batch unless d_ff is large).
+    // Per row block the wavefront's groups are added in order into one
+    // accumulator: its class (groups g with g % 4 == wi) of the output
+    // (device_gemv.h, down_class_total).
+    for (int u0 = 0; u0 < nu; u0 += Tiles::kUnits) {
+      const int nb = min(Tiles::kUnits, nu - u0);
+      if (u0 > 0) load_down_tiles<kGW>(drec, a.d, a.f, rb0 + u0, nb, cur);
+      float acc[Tiles::kUnits];
+#pragma unroll
+      for (int u = 0; u < Tiles::kUnits; ++u) acc[u] = 0.f;
+#pragma unroll
+      for (int j = 0; j < kGW; ++j) {
+        if (wi + 4 * j >= G) break;
+        uint4 x[4];
+        xload(j, x);
+#pragma unroll
+        for (int u = 0; u < Tiles::kUnits; ++u) {
+          if (u < nb) {
+            float unused = 0.f;
+            const float pr = lane_group_dot(cur.c[u][j], x, unused, false);
+            acc[u] = fmaf(half_bits_to_f32(at_use(cur.s[u][j])), fmaf(-136.f, xs[j], pr), acc[u]);
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < Tiles::kUnits; ++u) {
+        if (u < nb) {
+          const float v = reduce_quarters(acc[u]);
+          if (lane < 16) s_part[wi][u0 + u][lane] = v;
+        }
+      }
+    }
   }
   if (lane == 0) s_late[1][wi] = act_late;
   __syncthreads();
-  if (tid < 16) {
-    const int n = tid;
-    float acc = 0.f;
-    for (int j = 0; j < a.top_k; ++j) acc = fmaf(s_w[p0 + j], o_lds[p0 + j][n], acc);
-    const bool late_any =
-        route_late | s_late[1][0] | s_late[1][1] | s_late[1][2] | s_late[1][3];
-    a.y[(int64_t)tu * a.d + 16 * rb + n] = late_any ? 0x7fc0 : (uint16_t)f32_to_bf16_rne(acc);
+  if (nu > 0 && tid < 16 * nu) {
+    // Output of pair q, rows 16 (rb0 + u) + n: the four classes in the fixed
+    // order, handed on as a tagged word (NaN when a wait of this workgroup
+    // gave up).
+    const int u = tid >> 4, n = tid & 15;
+    const int row = 16 * (rb0 + u) + n;
+    const bool bad = route_late | s_late[1][0] | s_late[1][1] | s_late[1][2] | s_late[1][3];
+    const float o = bad ? __uint_as_float(0x7fc00000u)
+                        : (s_part[0][u][n] + s_part[1][u][n]) + (s_part[2][u][n] + s_part[3][u][n]);
+    a.pair_out[(int64_t)q * a.d + row] = o;
+    if (!is_comb) {
+      __hip_atomic_store(sy->out + (int64_t)q * a.d + row, tag | __float_as_uint(o),
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      // The token's other k - 1 outputs of this row (bounded wait), then the
+      // weighted sum in rank order.
+      const int t = q / a.top_k;
+      const int p0 = t * a.top_k;
+      // Eight words at a time, all read before any is checked (bounded
+      // wait); a word with this launch's tag holds its final value.
+      const uint64_t* ow = sy->out + (int64_t)p0 * a.d + row;
+      const int nk = a.top_k - 1;
+      bool comb_late = false;
+      float acc = 0.f;
+      for (int j0 = 0; j0 < nk; j0 += 8) {
+        uint64_t x[8];
+        for (uint32_t it = 0;; ++it) {
+#pragma unroll
+          for (int i = 0; i < 8; ++i)  // past the k - 1 words: read the last again
+            x[i] = __hip_atomic_load(ow + (int64_t)min(j0 + i, nk - 1) * a.d, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+          bool ok = true;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) ok &= (uint32_t)(x[i] >> 32) == ep;
+          if (ok) break;
+          if (it > kSpinLimit) {
+            atomicAdd(&sy->timeouts, 1u);
+            comb_late = true;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(kPollSleep);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (j0 + i < nk) acc = fmaf(s_w[p0 + j0 + i], __uint_as_float((uint32_t)x[i]), acc);
+      }
+      acc = fmaf(s_w[p0 + nk], o, acc);
+      a.y[(int64_t)t * a.d + row] = bad | comb_late ? 0x7fc0 : (uint16_t)f32_to_bf16_rne(acc);
+    }
   }
 
-  if (unit == 0) {
+  if (writes_routing) {
     // The workspace's routing and grouping arrays, as the unfused path writes them.
     for (int j = tid; j < P; j += 256) {
       a.topk_ids[j] = s_ids[j];
@@ -434,16 +490,20 @@ int fused_capacity() {
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
   std::lock_guard<std::mutex> lk(mu);
   if (cap[dev] == 0) {
-    int per_cu = 0, per_cu_dev = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_fused_kernel<false>, 256,
-                                                     0) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu_dev, decode_fused_kernel<true>, 256,
-                                                     0) != hipSuccess ||
+    int per_cu[4] = {}, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu[0], decode_fused_kernel<false, 2>,
+                                                     256, 0) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu[1], decode_fused_kernel<true, 2>,
+                                                     256, 0) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu[2], decode_fused_kernel<false, 4>,
+                                                     256, 0) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu[3], decode_fused_kernel<true, 4>,
+                                                     256, 0) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
       (void)hipGetLastError();
       return 0;
     }
-    cap[dev] = min(per_cu, per_cu_dev) * cus;
+    cap[dev] = min(min(per_cu[0], per_cu[1]), min(per_cu[2], per_cu[3])) * cus;
   }
   return cap[dev];
 }
@@ -453,31 +513,33 @@ int fused_capacity() {
 bool decode_fused_plan(DecodeArgs& a) {
   if (a.tokens < 1 || a.tokens > kFusedMaxTokens || a.tokens * a.top_k > kFusedMaxPairs)
     return false;
-  if ((int64_t)kGemvWaves * a.f * 2 > kFusedActLdsBytes) return false;  // a row per wavefront
+  if (a.d > kFusedMaxD || a.f > 4 * 4 * kGroup) return false;  // sync words; kGW <= 4
   if ((int64_t)a.tokens * a.top_k * (a.f / 2) > kFusedActWords) return false;
   if ((int64_t)a.tokens * a.d * 2 > kFusedActLdsBytes) return false;  // staged token rows
-  const int T = a.tokens;
+  const int P = a.tokens * a.top_k;
   const int pairs_of_f = a.f / kTileRows;
   const int n_rb = a.d / kTileRows;
+  a.gw = a.f <= 8 * kGroup ? 2 : 4;
   a.n_router = a.logits_override ? 1 : (a.n_experts + 3) / 4;
-  a.n_down = T * n_rb;
   const int cap = min(fused_capacity(), kFusedMaxBlocks);
-  // The most gate/up items (fewest row-block pairs each) that fit.  Token t's
-  // items are workers [t*It, (t+1)*It); its down units start at worker
-  // D0 + t*n_rb, which must not come before (t+1)*It.
+  // The most gate/up items (fewest row-block pairs each) that fit, with the
+  // down row blocks of each pair spread over the next pair's items and the
+  // last pair's over as many tail workers as the remaining room allows.
   for (int ppi = 1; ppi <= pairs_of_f; ppi *= 2) {
     const int chunks = (pairs_of_f + ppi - 1) / ppi;
-    const int It = a.top_k * chunks;
-    int down0 = It;
-    for (int t = 1; t < T; ++t) down0 = max(down0, (t + 1) * It - t * n_rb);
-    const int n_work = max(T * It, down0 + a.n_down);
-    if (a.n_router + n_work <= cap) {
-      a.pairs_per_item = ppi;
-      a.n_gate = T * It;
-      a.down0 = down0;
-      a.n_work = n_work;
-      return true;
-    }
+    const int down_r = (n_rb + chunks - 1) / chunks;
+    if (down_r > kFusedMaxDownUnits) break;  // fewer items only raise it
+    const int n_gate = P * chunks;
+    const int room = min(cap - a.n_router - n_gate, n_rb);
+    if (room < 1) continue;
+    const int tail_r = (n_rb + room - 1) / room;
+    if (tail_r > kFusedMaxDownUnits) continue;
+    a.pairs_per_item = ppi;
+    a.n_gate = n_gate;
+    a.down_r = down_r;
+    a.tail_r = tail_r;
+    a.n_work = n_gate + (n_rb + tail_r - 1) / tail_r;
+    return true;
   }
   return false;
 }
@@ -492,12 +554,20 @@ hipError_t launch_decode_fused(DecodeArgs& a, DecodeProgress& prog, hipStream_t 
     a.epoch = 0u;  // replays number themselves in device memory
   }
   const dim3 grid(a.n_router + a.n_work);
-  if (a.epoch != 0u)
-    launch(decode_fused_kernel<false>, grid, dim3(256), stream, a);
-  else
-    launch(decode_fused_kernel<true>, grid, dim3(256), stream, a);
+  const bool dev_epoch = a.epoch == 0u;
+  if (a.gw == 2) {
+    if (dev_epoch)
+      launch(decode_fused_kernel<true, 2>, grid, dim3(256), stream, a);
+    else
+      launch(decode_fused_kernel<false, 2>, grid, dim3(256), stream, a);
+  } else {
+    if (dev_epoch)
+      launch(decode_fused_kernel<true, 4>, grid, dim3(256), stream, a);
+    else
+      launch(decode_fused_kernel<false, 4>, grid, dim3(256), stream, a);
+  }
   e = hipGetLastError();
-  if (e == hipSuccess && a.epoch != 0u) prog.epoch = a.epoch;
+  if (e == hipSuccess && !dev_epoch) prog.epoch = a.epoch;
   return e;
 }
 

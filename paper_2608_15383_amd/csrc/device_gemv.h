@@ -239,13 +239,32 @@ __device__ __forceinline__ void load_x_group(XLoad xload, int m, int g, uint4* x
   for (int i = 0; i < 4; ++i) x[i] = xload(m, g * kGroup + 8 * quarter + 32 * i);
 }
 
-// acc[m] += contribution of the loaded batch to activation rows m < mc;
-// xload(m, k) returns the 8 bf16 activations k .. k+7 of row m.  Row by row,
-// groups in order; the next group's activations are read while this one's
-// are used.
+// Sum a lane's partials over the four lanes of its row: afterwards lanes
+// 0..15 hold the outputs of rows 16*rb + lane.
+__device__ __forceinline__ float reduce_quarters(float v) {
+  v += __shfl_xor(v, 16);
+  v += __shfl_xor(v, 32);
+  return v;
+}
+
+// The down projection accumulates each output in four classes of input
+// groups, class c holding the groups g with g % 4 == c in ascending order
+// (so four wavefronts can split the groups of a row between them, as the
+// fused decode launch does, with the same result).  The output is the sum of
+// the classes in a fixed order, each first summed over the lanes of its row.
+__device__ __forceinline__ float down_class_total(const float* acc) {
+  return (reduce_quarters(acc[0]) + reduce_quarters(acc[1])) +
+         (reduce_quarters(acc[2]) + reduce_quarters(acc[3]));
+}
+
+// acc[m][g % 4] += contribution of group g of the loaded batch to activation
+// row m < mc; xload(m, k) returns the 8 bf16 activations k .. k+7 of row m.
+// Row by row, groups in order; the next group's activations are read while
+// this one's are used.
 template <typename XLoad>
 __device__ __forceinline__ void down_apply_batch(const DownBatch& bt, int f, int g0, XLoad xload,
-                                                 int mc, float* acc) {
+                                                 int mc, float (*acc)[4]) {
+  static_assert(kDownBatch % 4 == 0, "batches start at a group of class 0");
   const int G = f / kGroup;
   if (g0 >= G) return;
 #pragma unroll
@@ -262,7 +281,7 @@ __device__ __forceinline__ void down_apply_batch(const DownBatch& bt, int f, int
       if (more) load_x_group(xload, m, g + 1, xn);
       float xs = 0.f;
       const float p = lane_group_dot(bt.c[j], xc, xs, true);
-      acc[m] = fmaf(half_bits_to_f32(at_use(bt.s[j])), fmaf(-136.f, xs, p), acc[m]);
+      acc[m][j & 3] = fmaf(half_bits_to_f32(at_use(bt.s[j])), fmaf(-136.f, xs, p), acc[m][j & 3]);
       if (more) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) xc[i] = xn[i];
@@ -282,53 +301,6 @@ __device__ __forceinline__ float lane_group_xsum(const uint4* x) {
     for (int p = 0; p < 4; ++p) xsum[i & 1] = dot2(kOnesBf16x2, xv[p], xsum[i & 1]);
   }
   return 0.f + (xsum[0] + xsum[1]);
-}
-
-// down_apply_batch with the activation sums precomputed: xsload(m, g) is
-// lane_group_xsum of this lane's inputs of group g of row m.
-template <typename XLoad, typename XsLoad>
-__device__ __forceinline__ void down_apply_batch_xs(const DownBatch& bt, int f, int g0,
-                                                    XLoad xload, XsLoad xsload, int mc,
-                                                    float* acc) {
-  const int G = f / kGroup;
-  if (g0 >= G) return;
-#pragma unroll
-  for (int m = 0; m < kTokChunk; ++m) {
-    if (m >= mc) break;
-    uint4 xc[4];
-    load_x_group(xload, m, g0, xc);
-#pragma unroll
-    for (int j = 0; j < kDownBatch; ++j) {
-      const int g = g0 + j;
-      if (g >= G) break;
-      // The first half of the next group's activations is read before this
-      // group's arithmetic, the second half after (register budget).
-      const bool more = j + 1 < kDownBatch && g + 1 < G;
-      const int quarter = lane_id() >> 4;
-      uint4 xn[2];
-      if (more) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) xn[i] = xload(m, (g + 1) * kGroup + 8 * quarter + 32 * i);
-      }
-      float unused = 0.f;
-      const float p = lane_group_dot(bt.c[j], xc, unused, false);
-      acc[m] = fmaf(half_bits_to_f32(at_use(bt.s[j])), fmaf(-136.f, xsload(m, g), p), acc[m]);
-      if (more) {
-        xc[0] = xn[0];
-        xc[1] = xn[1];
-#pragma unroll
-        for (int i = 2; i < 4; ++i) xc[i] = xload(m, (g + 1) * kGroup + 8 * quarter + 32 * i);
-      }
-    }
-  }
-}
-
-// Sum a lane's partials over the four lanes of its row: afterwards lanes
-// 0..15 hold the outputs of rows 16*rb + lane.
-__device__ __forceinline__ float reduce_quarters(float v) {
-  v += __shfl_xor(v, 16);
-  v += __shfl_xor(v, 32);
-  return v;
 }
 
 }  // namespace emoe

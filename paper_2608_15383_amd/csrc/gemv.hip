@@ -50,9 +50,11 @@ __global__ __launch_bounds__(256) void down_gemv_kernel(int d, int f, int top_k,
     auto xload = [&](int m, int k) {
       return *reinterpret_cast<const uint4*>(act + (int64_t)(m0 + m) * f + k);
     };
-    float acc[kTokChunk];
+    float acc[kTokChunk][4];
 #pragma unroll
-    for (int m = 0; m < kTokChunk; ++m) acc[m] = 0.f;
+    for (int m = 0; m < kTokChunk; ++m)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[m][c] = 0.f;
     for (int g0 = 0; g0 < G; g0 += kDownBatch) {
       DownBatch bt;
       down_load_batch(rec, d, f, rb, g0, bt);
@@ -60,10 +62,10 @@ __global__ __launch_bounds__(256) void down_gemv_kernel(int d, int f, int top_k,
     }
 #pragma unroll
     for (int m = 0; m < kTokChunk; ++m) {
-      acc[m] = reduce_quarters(acc[m]);
+      const float o = down_class_total(acc[m]);
       if (lane < 16 && m < mc) {
         const int pi = gv.sorted_pairs[m0 + m];
-        pair_out[(int64_t)pi * d + 16 * rb + lane] = acc[m];
+        pair_out[(int64_t)pi * d + 16 * rb + lane] = o;
       }
     }
   }
