@@ -49,7 +49,7 @@ namespace emoe {
 namespace {
 
 constexpr uint32_t kSpinLimit = 1u << 20;
-constexpr int kPollSleep = 8;  // s_sleep units (64 clocks) between polls
+constexpr int kPollSleep = 1;  // s_sleep units (64 clocks) between polls
 
 // Token t's logits into st.v: from logits_override, or from the router
 // items' tagged words (replica `replica`), read until every word carries this
