@@ -48,15 +48,27 @@ enum emoe_status {
 /* Largest supported expert count per layer. */
 #define EMOE_MAX_EXPERTS 256
 
-/* Execution path of the expert projections.  AUTO takes the MFMA grouped GEMM
- * when the call averages at least EMOE_MFMA_MIN_PAIRS_PER_EXPERT token-expert
- * pairs per expert, else the VALU weight-streaming GEMV.  The choice is made
- * once per call from (tokens, top_k, n_experts), so every wave of a call uses
- * the same arithmetic.  The MFMA path needs tokens*d_model*2 and
+/* Execution path of the expert projections (every path computes Eq. 2-3 on
+ * the same packed records; they differ in summation order and in the
+ * precision of the stored pair outputs):
+ *   GEMV:  VALU weight-streaming kernels for every expert (with full
+ *          residency and few tokens, the fused decode launch);
+ *   MFMA:  grouped bf16 MFMA GEMM for every expert, pair outputs rounded to bf16;
+ *   MIXED: per expert, by its own row count in the call: experts with at
+ *          least EMOE_MIXED_MFMA_ROWS token rows on the MFMA kernels, the
+ *          others on the GEMV kernels, pair outputs fp32.
+ * AUTO takes GEMV for at most EMOE_GEMV_MAX_TOKENS tokens and MFMA above (on
+ * MI355X the MFMA kernels are faster from 5 tokens on, also with one or two
+ * rows per expert).  What decides the arithmetic of a pair depends only on
+ * the call's (tokens, top_k, n_experts) and on its own expert's row count,
+ * never on the cache or the wave partition, so every wave of a call uses the
+ * same arithmetic.  The MFMA kernels need tokens*d_model*2 and
  * tokens*top_k*d_ff*2 below 2^31 bytes and d_model, d_ff <= 8192 (AUTO takes
- * the GEMV otherwise; an explicit MFMA request fails with EMOE_ESHAPE). */
-enum emoe_path { EMOE_PATH_AUTO = 0, EMOE_PATH_GEMV = 1, EMOE_PATH_MFMA = 2 };
-#define EMOE_MFMA_MIN_PAIRS_PER_EXPERT 32
+ * the GEMV otherwise; an explicit MFMA or MIXED request fails with
+ * EMOE_ESHAPE). */
+enum emoe_path { EMOE_PATH_AUTO = 0, EMOE_PATH_GEMV = 1, EMOE_PATH_MFMA = 2, EMOE_PATH_MIXED = 3 };
+#define EMOE_GEMV_MAX_TOKENS 4
+#define EMOE_MIXED_MFMA_ROWS 16
 
 typedef struct emoe_dims {
   int32_t d_model;    /* hidden size d; multiple of 128 */
@@ -89,17 +101,17 @@ typedef struct emoe_ws_layout {
   size_t sorted_pairs;  /* i32   [T*k]    pair ids pi = t*k+j grouped by expert */
   size_t active;        /* i32   [E]      active experts, ascending */
   size_t n_active;      /* i32   [1]      number of active experts */
-  size_t tile_offsets;  /* i32   [E+1]    MFMA row-tile prefix sum */
+  size_t tile_offsets;  /* i32   [E+1]    MFMA row-tile prefix sum (experts on the MFMA kernels) */
   size_t pair_pos;      /* i32   [T*k]    grouped position of each pair id */
   size_t act;           /* bf16  [T*k][d_ff]    phi(g)*u per pair, grouped order */
-  size_t pair_out;      /* expert output per pair id, [T*k][d_model]: f32 on the GEMV
-                           path, bf16 (in the first half of the field) on the MFMA path */
+  size_t pair_out;      /* expert output per pair id, [T*k][d_model]: f32 on the GEMV and
+                           mixed paths, bf16 (in the first half of the field) on the MFMA path */
   size_t act_bias;      /* f32   [d_ff/128][T*k]    -136 * group sums of act, by grouped
-                                                      position (MFMA path) */
+                                                      position (MFMA kernels) */
   size_t chunk_counts;  /* i32   [ceil(T*k/64)][E]  pairs per expert in each 64-pair chunk
                                                       (grouping of large calls) */
   size_t tok_bias;      /* f32   [T][d_model/128]   -136 * group sums of each token row of h
-                                                      (MFMA path) */
+                                                      (MFMA kernels) */
   size_t total;         /* bytes needed */
 } emoe_ws_layout;
 

@@ -15,8 +15,9 @@ EMOE_OK, EMOE_EINVAL, EMOE_ESHAPE, EMOE_ERANGE, EMOE_ECAPACITY, EMOE_EHIP, EMOE_
     0, -1, -2, -3, -4, -5, -6
 EMOE_GROUP = 128
 EMOE_MAX_EXPERTS = 256
-EMOE_PATH_AUTO, EMOE_PATH_GEMV, EMOE_PATH_MFMA = 0, 1, 2
-EMOE_MFMA_MIN_PAIRS_PER_EXPERT = 32
+EMOE_PATH_AUTO, EMOE_PATH_GEMV, EMOE_PATH_MFMA, EMOE_PATH_MIXED = 0, 1, 2, 3
+EMOE_MIXED_MFMA_ROWS = 16
+EMOE_GEMV_MAX_TOKENS = 4
 EMOE_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 

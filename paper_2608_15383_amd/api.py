@@ -12,7 +12,8 @@ import numpy as np
 
 from . import _lib
 from ._lib import (DecoderDims, DecoderWeights, Dims, Stats, WsLayout, check, lib,
-                   EMOE_PATH_AUTO, EMOE_PATH_GEMV, EMOE_PATH_MFMA, ExactMoEError)
+                   EMOE_PATH_AUTO, EMOE_PATH_GEMV, EMOE_PATH_MFMA, EMOE_PATH_MIXED,
+                   EMOE_MIXED_MFMA_ROWS, ExactMoEError)
 
 
 def _ptr(t) -> int | None:
@@ -271,7 +272,7 @@ def profile_end(max_out: int = 1 << 16) -> list[tuple[str, float]]:
 
 
 __all__ = ["Dims", "Stats", "WsLayout", "ExactMoEError", "EMOE_PATH_AUTO", "EMOE_PATH_GEMV",
-           "EMOE_PATH_MFMA", "dims", "check_dims", "expert_record_bytes", "workspace_layout",
+           "EMOE_PATH_MFMA", "EMOE_PATH_MIXED", "EMOE_MIXED_MFMA_ROWS", "dims", "check_dims", "expert_record_bytes", "workspace_layout",
            "workspace_bytes", "quantize_experts", "unpack_expert", "pack_expert", "route", "Cache",
            "moe_forward", "moe_forward_noalloc", "decoder_dims", "decoder_kv_bytes",
            "decoder_workspace_bytes", "Decoder", "moe_forward_sequential", "test_fail_copy_after", "profile_begin", "profile_end", "lib"]

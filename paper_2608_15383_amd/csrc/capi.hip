@@ -451,7 +451,7 @@ int32_t emoe_route(const emoe_dims* dims, int32_t T, const uint16_t* h, const ui
     EMOE_LAUNCH(EMOE_K_TOPK, stream, launch_topk(T, E, k, renormalize, z, topk_ids, topk_w, stream));
   EMOE_LAUNCH(EMOE_K_GROUP, stream,
               launch_group(T * k, E, topk_ids, counts, offsets, sorted_pairs, active, n_active,
-                           nullptr, nullptr, stream));
+                           nullptr, nullptr, 1, stream));
   return EMOE_OK;
 }
 
@@ -699,11 +699,13 @@ int32_t emoe_fill_slots(emoe_cache* c, const int32_t* fill_expert, const int32_t
 namespace {
 
 // GEMV row chunks of a wave from the experts' row counts.
-void set_wave_chunks(WaveArg& wa, const int32_t* counts) {
+// GEMV row chunks of the wave's experts (those with fewer than mfma_rows rows).
+void set_wave_chunks(WaveArg& wa, const int32_t* counts, int mfma_rows) {
   int32_t acc = 0;
   for (int i = 0; i < wa.n; ++i) {
     wa.chunk0[i] = acc;
-    acc += (counts[wa.expert[i]] + kGemvRows - 1) / kGemvRows;
+    const int rows = counts[wa.expert[i]];
+    acc += rows < mfma_rows ? (rows + kGemvRows - 1) / kGemvRows : 0;
   }
   wa.chunk0[wa.n] = acc;
 }
@@ -750,7 +752,7 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
     return fail(EMOE_ESTATE, "cache is neither fully resident nor backed by a host bank");
   const emoe_dims& D = c->dims;
   if (T < 0) return fail(EMOE_EINVAL, "tokens=%d < 0", T);
-  if (path < EMOE_PATH_AUTO || path > EMOE_PATH_MFMA) return fail(EMOE_EINVAL, "bad path %d", path);
+  if (path < EMOE_PATH_AUTO || path > EMOE_PATH_MIXED) return fail(EMOE_EINVAL, "bad path %d", path);
   emoe_stats ds{};
   ds.layer_calls = 1;
   if (T == 0) {
@@ -769,10 +771,14 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
                          d / EMOE_GROUP <= kMfmaMaxGroups && f / EMOE_GROUP <= kMfmaMaxGroups &&
                          c->record_bytes <= INT32_MAX;
   if (path == EMOE_PATH_AUTO)
-    path = (P >= EMOE_MFMA_MIN_PAIRS_PER_EXPERT * E && mfma_fits) ? EMOE_PATH_MFMA : EMOE_PATH_GEMV;
-  if (path == EMOE_PATH_MFMA && !mfma_fits)
-    return fail(EMOE_ESHAPE, "MFMA path: %d tokens exceed its 2 GiB activation addressing, or "
-                             "d_model / d_ff exceed %d groups", T, kMfmaMaxGroups);
+    path = (T > EMOE_GEMV_MAX_TOKENS && mfma_fits) ? EMOE_PATH_MFMA : EMOE_PATH_GEMV;
+  if (path != EMOE_PATH_GEMV && !mfma_fits)
+    return fail(EMOE_ESHAPE, "MFMA kernels: %d tokens exceed their 2 GiB activation addressing, "
+                             "or d_model / d_ff exceed %d groups", T, kMfmaMaxGroups);
+  // Experts with at least mfma_rows rows run on the MFMA kernels.
+  const int mfma_rows = path == EMOE_PATH_MFMA    ? 1
+                        : path == EMOE_PATH_MIXED ? EMOE_MIXED_MFMA_ROWS
+                                                  : INT32_MAX;
 
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   float* logits = reinterpret_cast<float*>(ws + L.logits);
@@ -832,7 +838,8 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
   // below.
   const float* z = logits_override ? logits_override : logits;
   float* tok_bias = reinterpret_cast<float*>(ws + L.tok_bias);
-  const bool fused_bias = path == EMOE_PATH_MFMA && !logits_override && d % 512 == 0;
+  const bool uses_mfma = path != EMOE_PATH_GEMV;
+  const bool fused_bias = uses_mfma && !logits_override && d % 512 == 0;
   if (!logits_override) {
     EMOE_LAUNCH(EMOE_K_ROUTER, stream,
                 launch_router_logits(T, E, d, h, w_router, logits, stream,
@@ -845,36 +852,49 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
     EMOE_LAUNCH(EMOE_K_GROUP_COUNT, stream, launch_group_count(P, E, ids, chunk_counts, stream));
     EMOE_LAUNCH(EMOE_K_GROUP, stream,
                 launch_group_place(P, E, ids, chunk_counts, counts, offsets, sorted, active,
-                                   n_active, tiles, pair_pos, stream));
+                                   n_active, tiles, pair_pos, mfma_rows, stream));
     ds.kernel_launches += 3;
   } else {
     EMOE_LAUNCH(EMOE_K_GROUP, stream,
                 launch_group(P, E, ids, counts, offsets, sorted, active, n_active, tiles, pair_pos,
-                             stream));
+                             mfma_rows, stream));
     ds.kernel_launches += 2;
   }
-  const GroupView gv{sorted, offsets, active, n_active, tiles};
-  if (path == EMOE_PATH_MFMA && !fused_bias) {
+  const GroupView gv{sorted, offsets, active, n_active, tiles, mfma_rows};
+  if (uses_mfma && !fused_bias) {
     // Accumulator start of the gate/up MFMA chains, once per call.
     EMOE_LAUNCH(EMOE_K_ROW_BIAS, stream, launch_row_bias(T, d, h, tok_bias, stream));
     ds.kernel_launches += 1;
   }
 
+  // One wave's projections: the GEMV kernels for the experts below mfma_rows
+  // rows, the MFMA kernels for the others (on the mixed path both, gate/up
+  // before down; fp32 pair outputs unless every expert is on MFMA).
   auto run_wave = [&](const WaveArg& wa) -> int32_t {
-    if (path == EMOE_PATH_MFMA) {
+    const bool gemv = path != EMOE_PATH_MFMA;
+    if (gemv) {
+      EMOE_LAUNCH(EMOE_K_GATEUP_GEMV, stream,
+                  launch_gateup_gemv(d, f, k, P, E, h, gv, wa, c->slot_bank, c->record_bytes, act, stream));
+      ds.kernel_launches += 1;
+    }
+    if (uses_mfma) {
       EMOE_LAUNCH(EMOE_K_GATEUP_MFMA, stream,
                   launch_gateup_mfma(T, d, f, k, E, h, tok_bias, gv, wa, c->slot_bank, c->record_bytes,
                                      act, act_bias, stream));
-      EMOE_LAUNCH(EMOE_K_DOWN_MFMA, stream,
-                  launch_down_mfma(T, d, f, k, E, act, act_bias, gv, wa, c->slot_bank, c->record_bytes,
-                                   reinterpret_cast<uint16_t*>(pair_out), stream));
-    } else {
-      EMOE_LAUNCH(EMOE_K_GATEUP_GEMV, stream,
-                  launch_gateup_gemv(d, f, k, P, E, h, gv, wa, c->slot_bank, c->record_bytes, act, stream));
+      ds.kernel_launches += 1;
+    }
+    if (gemv) {
       EMOE_LAUNCH(EMOE_K_DOWN_GEMV, stream,
                   launch_down_gemv(d, f, k, P, E, act, gv, wa, c->slot_bank, c->record_bytes, pair_out, stream));
+      ds.kernel_launches += 1;
     }
-    ds.kernel_launches += 2;
+    if (uses_mfma) {
+      EMOE_LAUNCH(EMOE_K_DOWN_MFMA, stream,
+                  launch_down_mfma(T, d, f, k, E, act, act_bias, gv, wa, c->slot_bank, c->record_bytes,
+                                   reinterpret_cast<uint16_t*>(pair_out), gemv ? pair_out : nullptr,
+                                   stream));
+      ds.kernel_launches += 1;
+    }
     return EMOE_OK;
   };
 
@@ -921,7 +941,7 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
       wa.n = n;
       for (int e = 0; e < E; ++e) wa.slot_of[e] = (int16_t)smap[e];
       for (int i = 0; i < n; ++i) wa.expert[i] = (int16_t)we[i];
-      set_wave_chunks(wa, c->counts_host);
+      set_wave_chunks(wa, c->counts_host, mfma_rows);
       if (sequential) {
         for (int i = 0; i < n; ++i) {
           WaveArg one;
@@ -929,7 +949,7 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
           one.expert[0] = (int16_t)we[i];
           for (int e = 0; e < E; ++e) one.slot_of[e] = -1;
           one.slot_of[we[i]] = (int16_t)smap[we[i]];
-          set_wave_chunks(one, c->counts_host);
+          set_wave_chunks(one, c->counts_host, mfma_rows);
           if ((st = run_wave(one))) return st;
           ds.seq_expert_calls += 1;
         }

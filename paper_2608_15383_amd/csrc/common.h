@@ -90,7 +90,16 @@ struct GroupView {
   const int32_t* active;        // [E]
   const int32_t* n_active;      // [1]
   const int32_t* tile_offsets;  // [E+1] MFMA row-tile prefix sum (MFMA path)
+  // Experts with at least this many rows in the call run on the MFMA kernels
+  // (their row tiles are in tile_offsets), the others on the GEMV kernels.
+  int32_t mfma_rows;
 };
+
+// MFMA row tiles of an expert with cnt rows when experts with at least
+// mfma_rows rows take the MFMA kernels.
+__host__ __device__ inline int mfma_row_tiles(int cnt, int mfma_rows) {
+  return cnt >= mfma_rows ? (cnt + kMfmaRows - 1) / kMfmaRows : 0;
+}
 
 // ---------------------------------------------------------------------------
 // Device helpers
@@ -194,7 +203,8 @@ __device__ __forceinline__ bool resolve_wave_chunk(const WaveArg& wave, const Gr
       cnt[i] = 0;
       if (w < n) {
         const int e = gv.active[w];
-        cnt[i] = (gv.offsets[e + 1] - gv.offsets[e] + kGemvRows - 1) / kGemvRows;
+        const int rows = gv.offsets[e + 1] - gv.offsets[e];
+        cnt[i] = rows < gv.mfma_rows ? (rows + kGemvRows - 1) / kGemvRows : 0;
       }
       local += cnt[i];
     }
@@ -267,11 +277,12 @@ hipError_t launch_topk(int tokens, int n_experts, int top_k, int renormalize, co
                        int32_t* topk_ids, float* topk_w, hipStream_t stream);
 
 // Grouping by expert (Sec. 3.4 step 1) in one workgroup; pair_pos receives
-// the inverse permutation (grouped position of each pair id).
+// the inverse permutation (grouped position of each pair id), tile_offsets
+// the MFMA row tiles of the experts with at least mfma_rows rows.
 hipError_t launch_group(int pairs, int n_experts, const int32_t* topk_ids, int32_t* counts,
                         int32_t* offsets, int32_t* sorted_pairs, int32_t* active,
                         int32_t* n_active, int32_t* tile_offsets, int32_t* pair_pos,
-                        hipStream_t stream);
+                        int mfma_rows, hipStream_t stream);
 
 // The same grouping over many workgroups, for large calls (pairs > 0): per
 // 64-pair chunk expert counts into chunk_counts [ceil(pairs/64)][E], then the
@@ -281,7 +292,8 @@ hipError_t launch_group_count(int pairs, int n_experts, const int32_t* topk_ids,
 hipError_t launch_group_place(int pairs, int n_experts, const int32_t* topk_ids,
                               const int32_t* chunk_counts, int32_t* counts, int32_t* offsets,
                               int32_t* sorted_pairs, int32_t* active, int32_t* n_active,
-                              int32_t* tile_offsets, int32_t* pair_pos, hipStream_t stream);
+                              int32_t* tile_offsets, int32_t* pair_pos, int mfma_rows,
+                              hipStream_t stream);
 constexpr int kGroupWideMinPairs = 1024;  // smaller calls group in one workgroup
 
 // Number of wave-local expert indices a grouped launch must cover.
@@ -314,11 +326,13 @@ hipError_t launch_gateup_mfma(int tokens, int d, int f, int top_k, int n_experts
                               const uint8_t* slot_bank, int64_t record_bytes, uint16_t* act,
                               float* act_bias, hipStream_t stream);
 
-// The MFMA down projection writes its pair outputs in bf16.
+// The MFMA down projection writes its pair outputs in bf16 (pair_out_f32
+// null) or in fp32 (into pair_out_f32; the per-expert path choice, where the
+// GEMV kernels write the other pairs' outputs in fp32).
 hipError_t launch_down_mfma(int tokens, int d, int f, int top_k, int n_experts, const uint16_t* act,
                             const float* act_bias, const GroupView& gv, const WaveArg& wave,
                             const uint8_t* slot_bank, int64_t record_bytes, uint16_t* pair_out,
-                            hipStream_t stream);
+                            float* pair_out_f32, hipStream_t stream);
 
 // pair_out: fp32 (GEMV paths) or bf16 (pair_out_bf16, MFMA path).
 hipError_t launch_combine(int tokens, int d, int top_k, const float* topk_w, const void* pair_out,

@@ -477,7 +477,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
       a.topk_w[j] = s_w[j];
     }
     block_group<256, false>(gsh, P, a.n_experts, s_ids, a.counts, a.offsets, a.sorted_pairs,
-                            a.active, a.n_active, nullptr, a.pair_pos);
+                            a.active, a.n_active, nullptr, a.pair_pos, 1);
   }
 }
 

@@ -458,7 +458,7 @@ __device__ __forceinline__ void block_group(
     int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
     int32_t* __restrict__ sorted_pairs, int32_t* __restrict__ active,
     int32_t* __restrict__ n_active, int32_t* __restrict__ tile_offsets,
-    int32_t* __restrict__ pair_pos) {
+    int32_t* __restrict__ pair_pos, int mfma_rows) {
   constexpr int kWaves = kThreads / 64;
   const int tid = threadIdx.x;
   const int lane = lane_id();
@@ -511,7 +511,7 @@ __device__ __forceinline__ void block_group(
         for (int w = 0; w < kWaves; ++w) c[q] += sh.wbase[w][e];
       local += c[q];
       nz += c[q] > 0;
-      tl += (c[q] + kMfmaRows - 1) / kMfmaRows;
+      tl += mfma_row_tiles(c[q], mfma_rows);
     }
     int total, nz_total, tl_total;
     int base = wave_exclusive_scan(local, total);
@@ -533,7 +533,7 @@ __device__ __forceinline__ void block_group(
         }
       }
       base += c[q];
-      tl_base += (c[q] + kMfmaRows - 1) / kMfmaRows;
+      tl_base += mfma_row_tiles(c[q], mfma_rows);
     }
     if (lane == 0) {
       st_u32<kCo>(offsets + n_experts, (uint32_t)total);

@@ -133,14 +133,16 @@ __device__ __forceinline__ float silu_fast(float x) {
 // per-token table [tokens][d/128], weights W13, output act (bf16, grouped
 // order) plus the bias table of act for the down projection.  Otherwise:
 // x = act [pairs][f] in grouped order, bias act's table [f/128][pairs] by
-// grouped position, weights W2, output pair_out (bf16, pair-id order).
+// grouped position, weights W2, output pair_out (bf16, pair-id order), or
+// pair_out_f32 (fp32) when that is given.
 // bias holds -136 * the sum of each 128-input group of each input row.
 template <bool kGateUp, typename Sh>
 __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_kernel(
     int d, int f, int top_k, int n_experts, const uint16_t* __restrict__ x, uint32_t x_bytes,
     const float* __restrict__ bias, int pairs, GroupView gv, WaveArg wave,
     const uint8_t* __restrict__ slot_bank, int64_t record_bytes, int n_ctiles,
-    uint16_t* __restrict__ act_out, float* __restrict__ act_bias_out, uint16_t* __restrict__ pair_out) {
+    uint16_t* __restrict__ act_out, float* __restrict__ act_bias_out, uint16_t* __restrict__ pair_out,
+    float* __restrict__ pair_out_f32) {
   constexpr int kWaves = Sh::kWaves;
   constexpr int kStages = Sh::kStages;
   constexpr int kCols = Sh::kCols;
@@ -403,6 +405,22 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
         if ((tid & 15) == 0) act_bias_out[(int64_t)g * pairs + row0 + m] = -kCodeBias * sum;
       }
     }
+  } else if (pair_out_f32) {
+    // fp32 outputs straight from the accumulators: 16 consecutive columns
+    // (64 bytes) of one row per 16 lanes.
+    if (wvalid) {
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int m = 16 * mi + 4 * quarter + j;
+          if (m < rows) {
+            float* out = pair_out_f32 + (int64_t)pair_lds[m] * d + 16 * rb0 + n_local;
+#pragma unroll
+            for (int r = 0; r < kNPW; ++r) out[16 * r] = acc[r][mi][j];
+          }
+        }
+    }
   } else {
     // Rows 0..31 are staged in stage 0, rows 32..63 in stage 1.
     constexpr int kStride = kCols + 8;
@@ -498,14 +516,15 @@ hipError_t launch_gateup_mfma(int tokens, int d, int f, int top_k, int n_experts
   launch(grouped_mfma_kernel<true, MfmaShape>, dim3(mfma_grid(n_ctiles, pairs, n_experts)),
          dim3(MfmaShape::kThreads), stream, d, f, top_k, n_experts, h,
          (uint32_t)((int64_t)tokens * d * 2), h_bias, pairs,
-         gv, wave, slot_bank, record_bytes, n_ctiles, act, act_bias, (uint16_t*)nullptr);
+         gv, wave, slot_bank, record_bytes, n_ctiles, act, act_bias, (uint16_t*)nullptr,
+         (float*)nullptr);
   return hipGetLastError();
 }
 
 hipError_t launch_down_mfma(int tokens, int d, int f, int top_k, int n_experts, const uint16_t* act,
                             const float* act_bias, const GroupView& gv, const WaveArg& wave,
                             const uint8_t* slot_bank, int64_t record_bytes, uint16_t* pair_out,
-                            hipStream_t stream) {
+                            float* pair_out_f32, hipStream_t stream) {
   const int pairs = tokens * top_k;
   if (pairs == 0) return hipSuccess;
   constexpr int kCols = MfmaShape::kCols;
@@ -513,7 +532,8 @@ hipError_t launch_down_mfma(int tokens, int d, int f, int top_k, int n_experts, 
   launch(grouped_mfma_kernel<false, MfmaShape>, dim3(mfma_grid(n_ctiles, pairs, n_experts)),
          dim3(MfmaShape::kThreads), stream, d, f, top_k, n_experts, act,
          (uint32_t)((int64_t)pairs * f * 2), act_bias, pairs,
-         gv, wave, slot_bank, record_bytes, n_ctiles, (uint16_t*)nullptr, (float*)nullptr, pair_out);
+         gv, wave, slot_bank, record_bytes, n_ctiles, (uint16_t*)nullptr, (float*)nullptr, pair_out,
+         pair_out_f32);
   return hipGetLastError();
 }
 

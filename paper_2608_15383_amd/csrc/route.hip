@@ -115,10 +115,10 @@ __global__ __launch_bounds__(kGroupThreads) void group_kernel(
     int pairs, int n_experts, const int32_t* __restrict__ ids, int32_t* __restrict__ counts,
     int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_pairs, int32_t* __restrict__ active,
     int32_t* __restrict__ n_active, int32_t* __restrict__ tile_offsets,
-    int32_t* __restrict__ pair_pos) {
+    int32_t* __restrict__ pair_pos, int mfma_rows) {
   __shared__ GroupShared<kGroupThreads> sh;
   block_group<kGroupThreads, false>(sh, pairs, n_experts, ids, counts, offsets, sorted_pairs,
-                                    active, n_active, tile_offsets, pair_pos);
+                                    active, n_active, tile_offsets, pair_pos, mfma_rows);
 }
 
 // Grouping spread over many workgroups (large calls): 64-pair chunks, one per
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void chunk_place_kernel(
     const int32_t* __restrict__ chunk_counts, int32_t* __restrict__ counts,
     int32_t* __restrict__ offsets, int32_t* __restrict__ sorted_pairs,
     int32_t* __restrict__ active, int32_t* __restrict__ n_active,
-    int32_t* __restrict__ tile_offsets, int32_t* __restrict__ pair_pos) {
+    int32_t* __restrict__ tile_offsets, int32_t* __restrict__ pair_pos, int mfma_rows) {
   __shared__ int part_all[kChunkWaves][EMOE_MAX_EXPERTS];
   __shared__ int part_pre[kChunkWaves][EMOE_MAX_EXPERTS];
   __shared__ int base[kChunkWaves][EMOE_MAX_EXPERTS];
@@ -201,7 +201,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void chunk_place_kernel(
         }
       local += cnt[q];
       nz += cnt[q] > 0;
-      tl += (cnt[q] + kMfmaRows - 1) / kMfmaRows;
+      tl += mfma_row_tiles(cnt[q], mfma_rows);
     }
     int total, nz_total, tl_total;
     int off = wave_exclusive_scan(local, total);
@@ -230,7 +230,7 @@ __global__ __launch_bounds__(64 * kChunkWaves) void chunk_place_kernel(
         }
       }
       off += cnt[q];
-      tl_base += (cnt[q] + kMfmaRows - 1) / kMfmaRows;
+      tl_base += mfma_row_tiles(cnt[q], mfma_rows);
     }
     if (writer && lane == 0) {
       offsets[n_experts] = total;
@@ -269,11 +269,13 @@ hipError_t launch_group_count(int pairs, int n_experts, const int32_t* topk_ids,
 hipError_t launch_group_place(int pairs, int n_experts, const int32_t* topk_ids,
                               const int32_t* chunk_counts, int32_t* counts, int32_t* offsets,
                               int32_t* sorted_pairs, int32_t* active, int32_t* n_active,
-                              int32_t* tile_offsets, int32_t* pair_pos, hipStream_t stream) {
+                              int32_t* tile_offsets, int32_t* pair_pos, int mfma_rows,
+                              hipStream_t stream) {
   const int n_wg = ((pairs + 63) / 64 + kChunkWaves - 1) / kChunkWaves;
   if (n_wg == 0) return hipSuccess;
   launch(chunk_place_kernel, dim3(n_wg), dim3(64 * kChunkWaves), stream, pairs, n_experts, topk_ids,
-         chunk_counts, counts, offsets, sorted_pairs, active, n_active, tile_offsets, pair_pos);
+         chunk_counts, counts, offsets, sorted_pairs, active, n_active, tile_offsets, pair_pos,
+         mfma_rows);
   return hipGetLastError();
 }
 
@@ -299,9 +301,9 @@ hipError_t launch_topk(int tokens, int n_experts, int top_k, int renormalize, co
 hipError_t launch_group(int pairs, int n_experts, const int32_t* topk_ids, int32_t* counts,
                         int32_t* offsets, int32_t* sorted_pairs, int32_t* active,
                         int32_t* n_active, int32_t* tile_offsets, int32_t* pair_pos,
-                        hipStream_t stream) {
+                        int mfma_rows, hipStream_t stream) {
   launch(group_kernel, dim3(1), dim3(kGroupThreads), stream, pairs, n_experts, topk_ids, counts,
-         offsets, sorted_pairs, active, n_active, tile_offsets, pair_pos);
+         offsets, sorted_pairs, active, n_active, tile_offsets, pair_pos, mfma_rows);
   return hipGetLastError();
 }
 

@@ -17,7 +17,7 @@ from tests._gpu import TOL, Layer, LazyExperts, dev, host_bits, quantize, rel_er
 
 pytestmark = pytest.mark.gpu
 
-GEMV, MFMA = api.EMOE_PATH_GEMV, api.EMOE_PATH_MFMA
+GEMV, MFMA, MIXED = api.EMOE_PATH_GEMV, api.EMOE_PATH_MFMA, api.EMOE_PATH_MIXED
 
 
 def dims_of(shape: LayerShape):
@@ -211,7 +211,8 @@ def test_random_shapes_every_path(shape, tokens, capacity):
     dm = layer.dm
     slots = torch.zeros(capacity * api.expert_record_bytes(dm), dtype=torch.uint8, device="cuda:0")
     cache = api.Cache(dm, capacity, slot_bank=slots, host_bank=_host_bank(layer))
-    for path in (GEMV, MFMA):
+    resident[MIXED] = layer.forward(lay.h, path=MIXED)
+    for path in (GEMV, MFMA, MIXED):
         assert np.array_equal(layer.forward(lay.h, path=path, cache=cache), resident[path]), path
     assert np.array_equal(layer.forward(lay.h, path=GEMV, cache=cache, sequential=True),
                           resident[GEMV])
@@ -247,21 +248,26 @@ def test_mfma_past_its_group_limit_is_a_shape_error():
                                           (LayerShape(128, 128, 64, 8), 2048)])
 def test_forward_grouping_of_large_calls_bit_exact(shape, tokens):
     """Calls above 1024 pairs group over many workgroups (per-chunk counts, then
-    a stable placement); the arrays must equal the oracle's grouping."""
+    a stable placement); the arrays must equal the oracle's grouping.  The
+    MFMA row-tile prefix sum counts the experts on the MFMA kernels: all of
+    them on the MFMA path, those with at least EMOE_MIXED_MFMA_ROWS rows on the
+    mixed path, none on the GEMV path."""
     lay = make_layer(shape, tokens, seed=5)
     layer = Layer(dims_of(shape), lay, tokens)
-    layer.forward(lay.h, path=GEMV)
     E, P = shape.n_experts, tokens * shape.top_k
     r = O.route(lay.f32("h"), lay.f32("w_router"), shape.top_k)
     gr = O.group_by_expert(r.ids, E)
-    assert np.array_equal(layer.ws_array("topk_ids", P, np.int32).reshape(tokens, -1), r.ids)
-    assert np.array_equal(layer.ws_array("counts", E, np.int32), gr.counts)
-    assert np.array_equal(layer.ws_array("offsets", E + 1, np.int32), gr.offsets)
-    assert np.array_equal(layer.ws_array("sorted_pairs", P, np.int32), gr.sorted_pairs)
-    assert layer.ws_array("n_active", 1, np.int32)[0] == len(gr.active)
-    assert np.array_equal(layer.ws_array("active", len(gr.active), np.int32), gr.active)
-    tiles = np.concatenate([[0], np.cumsum(-(-gr.counts // 64))])
-    assert np.array_equal(layer.ws_array("tile_offsets", E + 1, np.int32), tiles)
+    for path, min_rows in ((GEMV, P + 1), (MFMA, 1), (MIXED, api.EMOE_MIXED_MFMA_ROWS)):
+        layer.forward(lay.h, path=path)
+        assert np.array_equal(layer.ws_array("topk_ids", P, np.int32).reshape(tokens, -1), r.ids)
+        assert np.array_equal(layer.ws_array("counts", E, np.int32), gr.counts)
+        assert np.array_equal(layer.ws_array("offsets", E + 1, np.int32), gr.offsets)
+        assert np.array_equal(layer.ws_array("sorted_pairs", P, np.int32), gr.sorted_pairs)
+        assert layer.ws_array("n_active", 1, np.int32)[0] == len(gr.active)
+        assert np.array_equal(layer.ws_array("active", len(gr.active), np.int32), gr.active)
+        per = np.where(gr.counts >= min_rows, -(-gr.counts // 64), 0)
+        tiles = np.concatenate([[0], np.cumsum(per)])
+        assert np.array_equal(layer.ws_array("tile_offsets", E + 1, np.int32), tiles), path
 
 
 @pytest.mark.parametrize("path", [GEMV, MFMA])
@@ -405,6 +411,66 @@ def test_mfma_multi_wave_equals_single_wave(olmoe):
     ref, _ = oracle_y(sub, experts, 8, tokens=[0, 255])
     assert_close(y[[0, 255]], ref, "MFMA multi-wave")
     experts.cache.clear()
+
+
+def test_mixed_path_takes_each_expert_by_its_rows(olmoe):
+    """128 tokens under Zipf(1.1) routing: experts with at least
+    EMOE_MIXED_MFMA_ROWS rows run on the MFMA kernels, the rest on the GEMV
+    kernels.  Each pair's fp32 output equals, bit for bit, its own path's:
+    rounded to bf16 it is the all-MFMA call's output for the first kind, and
+    it is the all-GEMV call's output for the second.  A 16-slot cache
+    (several waves) and the sequential path give the same bits; y matches
+    the oracle, and AUTO (the all-MFMA call here) equals the MFMA path."""
+    from paper_2608_15383_amd.inputs import zipf_gumbel_logits
+    lay, layer, experts = olmoe
+    dm = layer.dm
+    T, k, d = 128, 8, 2048
+    sub = _sub(lay, T)
+    rng = np.random.default_rng(12)
+    z = zipf_gumbel_logits(T, 64, 1.1, rng.permutation(64), rng).astype(np.float32)
+    ids = O.topk_experts(z, k)
+    counts = np.bincount(ids.ravel(), minlength=64)
+    big = counts >= api.EMOE_MIXED_MFMA_ROWS
+    assert big.sum() >= 4 and ((counts > 0) & ~big).sum() >= 4   # both kinds present
+    y_gemv = layer.forward(sub.h, logits=z, path=GEMV)
+    po_gemv = layer.pair_out(T * k, mfma=False)
+    y_mfma = layer.forward(sub.h, logits=z, path=MFMA)
+    po_mfma = layer.ws_array("pair_out", T * k * d, np.uint16).reshape(T * k, d)
+    st = api.Stats()
+    y = layer.forward(sub.h, logits=z, path=MIXED, stats=st)
+    # top-k and grouping, the row sums of h, both kinds of both projections, combine
+    assert st.kernel_launches == 2 + 1 + 4 + 1
+    po = layer.pair_out(T * k, mfma=False)
+    on_mfma = big[ids.ravel()]
+    assert np.array_equal(f32_to_bf16_bits(po[on_mfma]), po_mfma[on_mfma])
+    assert np.array_equal(po[~on_mfma], po_gemv[~on_mfma])
+    assert np.array_equal(layer.forward(sub.h, logits=z), y_mfma)     # AUTO
+    host = _host_bank(layer)
+    slots = torch.zeros(16 * api.expert_record_bytes(dm), dtype=torch.uint8, device="cuda:0")
+    cache = api.Cache(dm, 16, slot_bank=slots, host_bank=host)
+    st = api.Stats()
+    assert np.array_equal(layer.forward(sub.h, logits=z, path=MIXED, cache=cache, stats=st), y)
+    assert st.waves >= 3
+    assert np.array_equal(layer.forward(sub.h, logits=z, path=MIXED, cache=cache,
+                                        sequential=True), y)
+    cache.close()
+    rows = [int(np.argmax(on_mfma.reshape(T, k).any(1))), int(np.argmin(on_mfma.reshape(T, k).all(1)))]
+    ref, _ = oracle_y(sub, experts, k, logits=z, tokens=rows)
+    assert_close(y[rows], ref, "mixed path")
+    assert_close(y, y_gemv.astype(np.float64), "mixed vs GEMV path")
+    experts.cache.clear()
+
+
+def test_mixed_path_without_large_experts_is_the_gemv_path():
+    """Below EMOE_MIXED_MFMA_ROWS rows per expert the mixed path runs the GEMV
+    kernels only: the same bits as the GEMV path."""
+    shape = LayerShape(512, 256, 16, 4)
+    lay = make_layer(shape, 12, seed=5)
+    layer = Layer(dims_of(shape), lay, 12)
+    y = layer.forward(lay.h, path=MIXED)
+    assert np.array_equal(y, layer.forward(lay.h, path=GEMV))
+    ref, _ = oracle_y(lay, LazyExperts(lay), 4)
+    assert_close(y, ref, "mixed, small experts")
 
 
 def test_global_to_slot_map_permutation(olmoe):
