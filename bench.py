@@ -57,6 +57,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_olmoe.md")
 # the hardware counters is reported only while these files are unchanged.
 KERNEL_SOURCES = {
     "decode_fused": ["common.h", "decode.h", "decode.hip", "device_gemv.h", "device_route.h"],
+    "decode_fused_t4": ["common.h", "decode.h", "decode.hip", "device_gemv.h", "device_route.h"],
     "gateup_mfma": ["common.h", "gemm.hip"],
     "down_mfma": ["common.h", "gemm.hip"],
 }
@@ -73,6 +74,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-prefill", action="store_true",
                    help="decode only: skip the prefill sub-record")
+    p.add_argument("--no-t4", action="store_true",
+                   help="decode only: skip the 4-token decode sub-record")
     return p.parse_args()
 
 
@@ -326,7 +329,7 @@ def bench_layer(args):
         out["graph_replay"] = dict(us_per_call=us, gbs=alg_bytes / (us * 1e-6) / 1e9,
                                    calls_per_graph=n_banks, equals_eager=same)
         log(f"graph replay: {us:.2f} us per call, equal to eager: {same}")
-        if T == 1:
+        if T == 1 and not args.no_t4:
             out["decode_t4"] = decode_t4_record(api, torch, dm, m["banks"], caches)
     # Every bounded wait of the fused decode launch must have been met: a
     # timeout would mean some call's output is invalid (it is written as NaN).

@@ -48,6 +48,25 @@
 namespace emoe {
 namespace {
 
+// Phase timestamps for measurement builds (compiled with -DEMOE_PHASE_TRACE by
+// phase_trace.py; absent otherwise): word 16 b + i holds the wall clock
+// (100 MHz) at which workgroup b passed phase i.  The stores perturb the
+// timing a little (they count on the same vector-memory counter as the loads).
+#ifdef EMOE_PHASE_TRACE
+__device__ uint64_t g_phase_trace[kFusedMaxBlocks * 16];
+#define EMOE_PHASE(i)                                                                   \
+  do {                                                                                  \
+    if (threadIdx.x == 0) g_phase_trace[blockIdx.x * 16 + (i)] = wall_clock64();        \
+  } while (0)
+#define EMOE_PHASE_WAVE(i)                                                              \
+  do {                                                                                  \
+    if (lane_id() == 0) g_phase_trace[blockIdx.x * 16 + (i)] = wall_clock64();          \
+  } while (0)
+#else
+#define EMOE_PHASE(i) do {} while (0)
+#define EMOE_PHASE_WAVE(i) do {} while (0)
+#endif
+
 constexpr uint32_t kSpinLimit = 1u << 20;
 constexpr int kPollSleep = 1;  // s_sleep units (64 clocks) between polls
 
@@ -207,6 +226,13 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   DecodeSync* sy = a.sync;
   const int P = a.tokens * a.top_k;
   const uint32_t epoch = kDevEpoch ? launch_epoch(sy) : a.epoch;
+  EMOE_PHASE(0);  // start
+#ifdef EMOE_PHASE_TRACE
+  if (blk == 0 && tid == 0) {  // the layout, for reading the trace
+    g_phase_trace[14] = (uint64_t)a.n_router | (uint64_t)a.n_gate << 16 | (uint64_t)a.n_work << 32;
+    g_phase_trace[15] = (uint64_t)a.pairs_per_item | (uint64_t)a.down_r << 16 | (uint64_t)a.tail_r << 32;
+  }
+#endif
 
   if (blk < a.n_router) {
     // ---------------------------------------------------------------- router
@@ -226,6 +252,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
         });
       }
     }
+    EMOE_PHASE(1);  // router: logits stored
     if (kDevEpoch) {
       if (tid == 0) arrive(sy, epoch, blk);
       if (blk == 0 && wi == 0) advance_epoch(sy, epoch, (int)gridDim.x);
@@ -270,6 +297,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     uint64_t* keys = s_topk[1];
     if (wi == 0) {
       late = load_logits(sy, a, epoch, replica, 0, st);
+      EMOE_PHASE_WAVE(1);  // worker: logits seen
       keys[lane] = topk_lane_key(st, a.n_experts);
     }
     __syncthreads();
@@ -297,6 +325,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   // Logits that never arrived leave this workgroup's selection invalid: its
   // outputs become NaN rather than passing as valid results.
   const bool route_late = s_late[0][0] | s_late[0][1] | s_late[0][2] | s_late[0][3];
+  EMOE_PHASE(2);  // top-k done
   // A read epoch has been waited for by now (the logits' tags): from here on
   // a scalar.  Tail workers record it before their first tile loads, so that
   // no later wait covers the store; gate/up workers after their item.
@@ -326,6 +355,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
                     __hip_atomic_store(act_tag + ((s * f + n) >> 1), tag | v | nan_mask,
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                   });
+    EMOE_PHASE(4);  // gate/up item done
     if (kDevEpoch && tid == 0) arrive(sy, ep, blk);
   }
 
@@ -336,6 +366,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   // stream theirs; a gate/up worker after its item (loads issued before the
   // item's would be waited for with them).
   const int G = a.f / kGroup;
+  EMOE_PHASE(3);  // down part reached
   bool act_late = false;
   if (nu > 0) {
     const uint8_t* drec = a.slot_bank + (int64_t)s_ids[q] * a.record_bytes;
@@ -369,6 +400,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
       __builtin_amdgcn_s_sleep(kPollSleep);
     }
     __builtin_amdgcn_wave_barrier();
+    EMOE_PHASE(5);  // activation row staged (wavefront 0)
     const uint16_t* xh = reinterpret_cast<const uint16_t*>(xw);
     const int quarter = lane >> 4;
     // The lane's 32 activations of group slot j (4 x uint4).
@@ -417,6 +449,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
       }
     }
   }
+  EMOE_PHASE(6);  // down tiles computed (wavefront 0)
   if (lane == 0) s_late[1][wi] = act_late;
   __syncthreads();
   if (nu > 0 && tid < 16 * nu) {
@@ -465,11 +498,13 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
         for (int i = 0; i < 8; ++i)
           if (j0 + i < nk) acc = fmaf(s_w[p0 + j0 + i], __uint_as_float((uint32_t)x[i]), acc);
       }
+      EMOE_PHASE(7);  // combining worker: the token's other outputs seen
       acc = fmaf(s_w[p0 + nk], o, acc);
-      a.y[(int64_t)t * a.d + row] = bad | comb_late ? 0x7fc0 : (uint16_t)f32_to_bf16_rne(acc);
+      a.y[(int64_t)t * a.d + row] = (bad | comb_late) ? 0x7fc0 : (uint16_t)f32_to_bf16_rne(acc);
     }
   }
 
+  EMOE_PHASE(9);  // end (before the routing arrays)
   if (writes_routing) {
     // The workspace's routing and grouping arrays, as the unfused path writes them.
     for (int j = tid; j < P; j += 256) {
@@ -572,3 +607,15 @@ hipError_t launch_decode_fused(DecodeArgs& a, DecodeProgress& prog, hipStream_t 
 }
 
 }  // namespace emoe
+
+#ifdef EMOE_PHASE_TRACE
+// Measurement builds only: copy the phase timestamps of the first n_blocks
+// workgroups of the latest fused launch to host memory (16 words each).
+extern "C" int32_t emoe_debug_phase_trace(uint64_t* host_out, int32_t n_blocks) {
+  if (!host_out || n_blocks < 0 || n_blocks > emoe::kFusedMaxBlocks) return EMOE_EINVAL;
+  return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(emoe::g_phase_trace), (size_t)n_blocks * 16 * 8,
+                             0, hipMemcpyDeviceToHost) == hipSuccess
+             ? EMOE_OK
+             : EMOE_EHIP;
+}
+#endif
