@@ -272,8 +272,9 @@ int32_t emoe_fill_slots(emoe_cache* cache, const int32_t* fill_expert, const int
  * refills what it needs and computes on correct records.  Waves enqueued
  * before the failing one still complete on `stream`.
  * With full residency, the GEMV path, at most 4 tokens (and 32 pairs),
- * d_ff <= 4096 and tokens*d_model <= 16384 the whole layer runs as one fused
- * kernel launch with the same arithmetic (and bit-identical results).  Calls
+ * d_ff <= 2048, d_model <= 4096 and tokens*d_model <= 16384 the whole layer
+ * runs as one fused kernel launch with the same arithmetic (and
+ * bit-identical results).  Calls
  * on one cache must not overlap in time (use one stream, or order the
  * streams): the cache holds the words that launch's workgroups hand over.
  * With full residency the call may be captured into a HIP graph: a captured

@@ -205,7 +205,7 @@ def test_random_shapes_every_path(shape, tokens, capacity):
         resident[path] = layer.forward(lay.h, path=path, stats=st)
         assert_close(resident[path], ref, f"{shape} T={tokens} path={path}")
     k, f, d = shape.top_k, shape.d_ff, shape.d_model
-    fused = (tokens <= 4 and tokens * k <= 32 and 4 * f * 2 <= 32768
+    fused = (tokens <= 4 and tokens * k <= 32 and f <= 2048 and d <= 4096
              and tokens * d * 2 <= 32768 and tokens * k * f // 2 <= 32 * 2048)
     assert (st.kernel_launches == 1) == fused
     dm = layer.dm
@@ -553,9 +553,9 @@ def test_fused_decode_matches_unfused_bitwise(shape, tokens):
     layer = Layer(dims_of(shape), lay, tokens)
     st = api.Stats()
     y_f = layer.forward(lay.h, stats=st)
-    # Fused when it fits: one activation row per down wavefront and the token
-    # rows in 32 KB of LDS, the handed-over activation words in the cache.
-    fits = (4 * shape.d_ff * 2 <= 32768 and tokens * shape.d_model * 2 <= 32768
+    # Fused when it fits: the token rows in 32 KB of LDS, at most four down
+    # input groups per wavefront, the handed-over words in the cache.
+    fits = (shape.d_ff <= 2048 and shape.d_model <= 4096 and tokens * shape.d_model * 2 <= 32768
             and tokens * shape.top_k * shape.d_ff // 2 <= 32 * 2048)
     assert (st.kernel_launches == 1) == fits
     po_f = layer.ws_array("pair_out", tokens * shape.top_k * shape.d_model, np.float32)
