@@ -349,12 +349,19 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     const int d = a.d, f = a.f;
     const uint32_t nan_mask = route_late ? 0x7fc07fc0u : 0u;  // bf16 NaN pair
     uint64_t* act_tag = sy->act;
-    for (int b = b0; b < b1; ++b)
-      gateup_rows(gush, a.d, a.f, [=](int s) { return h_lds + (s / top_k) * d; }, pi, pi + 1,
-                  a.slot_bank + (int64_t)e * a.record_bytes, b, [=](int s, int n, uint32_t v) {
-                    __hip_atomic_store(act_tag + ((s * f + n) >> 1), tag | v | nan_mask,
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                  });
+    auto store_act = [=](int s, int n, uint32_t v) {
+      __hip_atomic_store(act_tag + ((s * f + n) >> 1), tag | v | nan_mask, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    };
+    const uint8_t* rec = a.slot_bank + (int64_t)e * a.record_bytes;
+    if (b1 - b0 > 1 && d <= kGemvWaves * kGateBatch * kGroup) {
+      // The next row-block pair's tiles load while this one is computed.
+      gateup_row_blocks(gush, d, f, h_lds + (pi / top_k) * d, pi, rec, b0, b1, store_act);
+    } else {
+      for (int b = b0; b < b1; ++b)
+        gateup_rows(gush, d, f, [=](int s) { return h_lds + (s / top_k) * d; }, pi, pi + 1, rec,
+                    b, store_act);
+    }
     EMOE_PHASE(4);  // gate/up item done
     if (kDevEpoch && tid == 0) arrive(sy, ep, blk);
   }
