@@ -6,7 +6,9 @@
 // memory about 1 us under load, against roughly 5 us to stream the decode
 // layer's 26 MB of packed weights.  The six-kernel sequence is therefore
 // replaced by one grid whose workgroups play these roles by index:
-//   [0, nR)        router items: logits of 4 experts for every token;
+//   [0, nR)        router items: logits of 4 experts for one or two
+//                  tokens (a pair of tokens per router wavefront and pass,
+//                  so with more than two tokens the items split them);
 //   [nR, nR+nG)    gate/up workers: worker j runs gate/up item j (pair
 //                  p = j / chunks, some of its row-block pairs; pairs in
 //                  token-major order), then down_r output row blocks of pair
@@ -69,6 +71,10 @@ __device__ uint64_t g_phase_trace[kFusedMaxBlocks * 16];
 
 constexpr uint32_t kSpinLimit = 1u << 20;
 constexpr int kPollSleep = 1;  // s_sleep units (64 clocks) between polls
+// Between polls of the logits with several tokens: then every wavefront of a
+// worker that has a token polls, while the router items still stream their
+// weights (one token: wavefront 0 alone, kPollSleep).
+constexpr int kLogitPollSleep = 4;
 
 // Token t's logits into st.v: from logits_override, or from the router
 // items' tagged words (replica `replica`), read until every word carries this
@@ -105,7 +111,10 @@ __device__ __forceinline__ bool load_logits(DecodeSync* sy, const DecodeArgs& a,
       if (lane == 0) atomicAdd(&sy->timeouts, 1u);
       return true;
     }
-    __builtin_amdgcn_s_sleep(kPollSleep);
+    if (a.tokens > 1)
+      __builtin_amdgcn_s_sleep(kLogitPollSleep);
+    else
+      __builtin_amdgcn_s_sleep(kPollSleep);
   }
 }
 
@@ -240,9 +249,14 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     // kSyncLanes replicas, so the hundreds of readers below spread over as
     // many memory locations.
     if (!a.logits_override) {
-      const int e0 = 4 * blk + wi;
+      // With router_shift 1, items 2i and 2i + 1 take expert quad i for
+      // tokens 0, 1 and 2, 3; with 0, item i takes quad i for every token.
+      static_assert(kFusedMaxTokens <= 4, "two router items per expert quad at most");
+      const int e0 = 4 * (blk >> a.router_shift) + wi;
+      const int t0 = 2 * (blk & a.router_shift);
+      const int t1 = min(a.tokens, t0 + 2);
       if (e0 < a.n_experts) {
-        wave_router_dot(a.tokens, a.d, e0, a.h, a.w_router, [&](int t, double sum) {
+        wave_router_dot(t0, t1, a.d, e0, a.h, a.w_router, [&](int t, double sum) {
           const uint32_t v = __float_as_uint((float)sum);
           const int at = t * a.n_experts + e0;
           if (lane < kSyncLanes)
@@ -562,7 +576,9 @@ bool decode_fused_plan(DecodeArgs& a) {
   const int pairs_of_f = a.f / kTileRows;
   const int n_rb = a.d / kTileRows;
   a.gw = a.f <= 8 * kGroup ? 2 : 4;
-  a.n_router = a.logits_override ? 1 : (a.n_experts + 3) / 4;
+  // Router items: 4 experts by (at most) two tokens, one pass each.
+  a.router_shift = a.tokens > 2 ? 1 : 0;
+  a.n_router = a.logits_override ? 1 : ((a.n_experts + 3) / 4) << a.router_shift;
   const int cap = min(fused_capacity(), kFusedMaxBlocks);
   // The most gate/up items (fewest row-block pairs each) that fit, with the
   // down row blocks of each pair spread over the next pair's items and the

@@ -137,16 +137,15 @@ __device__ __forceinline__ void wave_router_dot_tokens(int t0, int d, const uint
   for (int t = 0; t < kT; ++t) store(t0 + t, wave_sum_f64_dpp(acc[t]));
 }
 
-// Logit sums of expert e for every token: two tokens per pass (four would
+// Logit sums of expert e for tokens [t0, t1): two tokens per pass (four would
 // hold more loaded registers than the fused decode kernel has to spare).
 template <typename Store>
-__device__ __forceinline__ void wave_router_dot(int tokens, int d, int e,
+__device__ __forceinline__ void wave_router_dot(int t0, int t1, int d, int e,
                                                 const uint16_t* __restrict__ h,
                                                 const uint16_t* __restrict__ wr, Store store) {
   const uint16_t* wrow = wr + (int64_t)e * d;
-  int t0 = 0;
-  for (; t0 + 2 <= tokens; t0 += 2) wave_router_dot_tokens<2>(t0, d, wrow, h, store);
-  if (t0 < tokens) wave_router_dot_tokens<1>(t0, d, wrow, h, store);
+  for (; t0 + 2 <= t1; t0 += 2) wave_router_dot_tokens<2>(t0, d, wrow, h, store);
+  if (t0 < t1) wave_router_dot_tokens<1>(t0, d, wrow, h, store);
 }
 
 template <int NT, int NE, bool kCo>
