@@ -212,6 +212,37 @@ __device__ __forceinline__ void load_down_tiles(const uint8_t* __restrict__ rec,
   }
 }
 
+// Row blocks rb .. rb+kN-1 into units 0 .. kN-1, every load issued so that
+// the waits for loads issued before these stay exact: a unit past nb reads
+// unit nb-1 again, a row block past the last reads the last one and a slot
+// past the last group reads the last group (all unused).
+template <int kGW, int kN>
+__device__ __forceinline__ void load_down_tiles_all(const uint8_t* __restrict__ rec, int d, int f,
+                                                    int rb, int nb, DownTiles<kGW>& t) {
+  static_assert(kN <= DownTiles<kGW>::kUnits, "units of one batch");
+  const int lane = lane_id();
+  const int wi = threadIdx.x >> 6;
+  const int G = f / kGroup;
+  const RecordLayout L = record_layout(d, f);
+  const uint8_t* codes = rec + L.w2_codes + 16 * lane;
+  const uint16_t* sc = reinterpret_cast<const uint16_t*>(rec + L.w2_scales);
+#pragma unroll
+  for (int u = 0; u < kN; ++u) {
+    const int r = min(rb + min(u, nb - 1), d / kTileRows - 1);
+    const int n = 16 * r + (lane & 15);
+#pragma unroll
+    for (int j = 0; j < kGW; ++j) {
+      const int g = min(wi + 4 * j, G - 1);
+      t.c[u][j] = *reinterpret_cast<const uint4*>(codes + ((int64_t)r * G + g) * kTileBytes);
+      t.s[u][j] = sc[scale_index(n, g, G)];
+    }
+  }
+}
+
+// Down row blocks a gate/up worker of one row-block pair loads with its
+// gate/up tiles.
+constexpr int kDownEarly = 2;
+
 // kDevEpoch: the launch is being captured into a graph and reads its epoch
 // from DecodeSync (a.epoch is 0); otherwise a.epoch is the host's number.
 // kGW: input groups of the down projection per wavefront (d_ff <= 512 kGW).
@@ -348,6 +379,13 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   const uint64_t tag = (uint64_t)ep << 32;
 
 
+  // The first batch of this worker's down tiles (pair q's record).
+  using Tiles = DownTiles<kGW>;
+  Tiles dn;
+  const uint8_t* drec = a.slot_bank + (int64_t)s_ids[max(q, 0)] * a.record_bytes;
+  const bool early = is_gate && a.pairs_per_item == 1 && a.down_r <= kDownEarly &&
+                     a.d == kGemvWaves * kGateBatch * kGroup;
+
   if (is_gate) {
     // ---------------------------------------------------------------- gate/up
     // Item = (pair pi, row-block pairs b0 ..): one token row of one expert.
@@ -368,7 +406,16 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
                          __HIP_MEMORY_SCOPE_AGENT);
     };
     const uint8_t* rec = a.slot_bank + (int64_t)e * a.record_bytes;
-    if (b1 - b0 > 1 && d <= kGemvWaves * kGateBatch * kGroup) {
+    if (early) {
+      // One row-block pair: its tiles, then this worker's down tiles, are
+      // issued before the pair is computed, so the down tiles stream with
+      // the gate/up weights (a worker of pair 0, which has no down work,
+      // reads pair 0's tiles, unused).
+      GateUpBatch gb;
+      gateup_load_batch(rec, d, f, b0, gb);
+      load_down_tiles_all<kGW, kDownEarly>(drec, d, f, rb0, max(nu, 1), dn);
+      gateup_pair_compute<true>(gush, d, h_lds + (pi / top_k) * d, pi, gb, b0, store_act);
+    } else if (b1 - b0 > 1 && d <= kGemvWaves * kGateBatch * kGroup) {
       // The next row-block pair's tiles load while this one is computed.
       gateup_row_blocks(gush, d, f, h_lds + (pi / top_k) * d, pi, rec, b0, b1, store_act);
     } else {
@@ -390,10 +437,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   EMOE_PHASE(3);  // down part reached
   bool act_late = false;
   if (nu > 0) {
-    const uint8_t* drec = a.slot_bank + (int64_t)s_ids[q] * a.record_bytes;
-    using Tiles = DownTiles<kGW>;
-    Tiles cur;
-    load_down_tiles<kGW>(drec, a.d, a.f, rb0, min(nu, Tiles::kUnits), cur);
+    if (!early) load_down_tiles<kGW>(drec, a.d, a.f, rb0, min(nu, Tiles::kUnits), dn);
     // This wavefront's groups of activation row q, from the tagged words
     // (one per lane and group, all read before any is checked; bounded wait)
     // into its LDS slot.
@@ -443,7 +487,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     // (device_gemv.h, down_class_total).
     for (int u0 = 0; u0 < nu; u0 += Tiles::kUnits) {
       const int nb = min(Tiles::kUnits, nu - u0);
-      if (u0 > 0) load_down_tiles<kGW>(drec, a.d, a.f, rb0 + u0, nb, cur);
+      if (u0 > 0) load_down_tiles<kGW>(drec, a.d, a.f, rb0 + u0, nb, dn);
       float acc[Tiles::kUnits];
 #pragma unroll
       for (int u = 0; u < Tiles::kUnits; ++u) acc[u] = 0.f;
@@ -456,8 +500,8 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
         for (int u = 0; u < Tiles::kUnits; ++u) {
           if (u < nb) {
             float unused = 0.f;
-            const float pr = lane_group_dot(cur.c[u][j], x, unused, false);
-            acc[u] = fmaf(half_bits_to_f32(at_use(cur.s[u][j])), fmaf(-136.f, xs[j], pr), acc[u]);
+            const float pr = lane_group_dot(dn.c[u][j], x, unused, false);
+            acc[u] = fmaf(half_bits_to_f32(at_use(dn.s[u][j])), fmaf(-136.f, xs[j], pr), acc[u]);
           }
         }
       }

@@ -126,21 +126,73 @@ __device__ __forceinline__ void gateup_load_batch(const uint8_t* __restrict__ re
   }
 }
 
-// gateup_rows for one activation row x (d <= kGemvWaves * kGateBatch * 128)
-// and the row-block pairs b0 .. b1-1, with the next pair's tiles loaded while
-// the current pair is computed.  Same arithmetic, in the same order, as
-// gateup_rows, so the same bits.
+// Gate/up row-block pair b for one activation row x (row `row`) from its
+// loaded tiles (d <= kGemvWaves * kGateBatch * 128): the same arithmetic, in
+// the same order, as gateup_rows, so the same bits.  Touches no global memory
+// before the store.  kFull: d is exactly kGemvWaves * kGateBatch * 128, so
+// every slot of the batch is a group and the code has no branch on the
+// group count (a branch would let the compiler sink a tile's load into it,
+// behind any loads the caller issued after the batch's, and wait for those).
+template <bool kFull = false, typename Store>
+__device__ __forceinline__ void gateup_pair_compute(GateUpShared& sh, int d, const uint16_t* x,
+                                                    int row, const GateUpBatch& cur, int b,
+                                                    Store store) {
+  const int lane = lane_id();
+  const int wi = threadIdx.x >> 6;
+  const int G = kFull ? kGemvWaves * kGateBatch : d / kGroup;
+  const int n_local = lane & 15;
+  const int quarter = lane >> 4;
+  const uint16_t* xrow = x + 8 * quarter;
+  float accg = 0.f, accu = 0.f;
+  uint4 xc[4];
+  load_x32(xrow + wi * kGroup, xc);
+#pragma unroll
+  for (int j = 0; j < kGateBatch; ++j) {
+    const int g = wi + kGemvWaves * j;
+    if (!kFull && g >= G) break;
+    const bool more = j + 1 < kGateBatch && (kFull || g + kGemvWaves < G);
+    uint4 xn[4];
+    if (more) load_x32(xrow + (g + kGemvWaves) * kGroup, xn);
+    float xs = 0.f;
+    const float pg = lane_group_dot(cur.cg[j], xc, xs, true);
+    const float pu = lane_group_dot(cur.cu[j], xc, xs, false);
+    accg = fmaf(half_bits_to_f32(cur.sgu[j] & 0xffffu), fmaf(-136.f, xs, pg), accg);
+    accu = fmaf(half_bits_to_f32(cur.sgu[j] >> 16), fmaf(-136.f, xs, pu), accu);
+    if (more) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xc[i] = xn[i];
+    }
+  }
+  accg += __shfl_xor(accg, 16);
+  accg += __shfl_xor(accg, 32);
+  accu += __shfl_xor(accu, 16);
+  accu += __shfl_xor(accu, 32);
+  if (quarter == 0) {
+    sh.red[wi][0][0][n_local] = accg;
+    sh.red[wi][0][1][n_local] = accu;
+  }
+  __syncthreads();
+  if (wi == 0) {
+    float gs = 0.f, us = 0.f;
+#pragma unroll
+    for (int w = 0; w < kGemvWaves; ++w) {
+      gs += sh.red[w][0][0][n_local];
+      us += sh.red[w][0][1][n_local];
+    }
+    const uint32_t a16 = f32_to_bf16_rne(silu_mul(gs, us));
+    const uint32_t next = __shfl_down(a16, 1);
+    if (lane < 16 && (n_local & 1) == 0) store(row, 16 * b + n_local, a16 | (next << 16));
+  }
+  __syncthreads();
+}
+
+// gateup_pair_compute over the row-block pairs b0 .. b1-1, with the next
+// pair's tiles loaded while the current pair is computed.
 template <typename Store>
 __device__ __forceinline__ void gateup_row_blocks(GateUpShared& sh, int d, int f,
                                                   const uint16_t* x, int row,
                                                   const uint8_t* __restrict__ rec, int b0, int b1,
                                                   Store store) {
-  const int lane = lane_id();
-  const int wi = threadIdx.x >> 6;
-  const int G = d / kGroup;
-  const int n_local = lane & 15;
-  const int quarter = lane >> 4;
-  const uint16_t* xrow = x + 8 * quarter;
   GateUpBatch cur;
   gateup_load_batch(rec, d, f, b0, cur);
   for (int b = b0; b < b1; ++b) {
@@ -148,47 +200,7 @@ __device__ __forceinline__ void gateup_row_blocks(GateUpShared& sh, int d, int f
     // same loads and the wait for the current pair's tiles stays exact.
     GateUpBatch nxt;
     gateup_load_batch(rec, d, f, min(b + 1, b1 - 1), nxt);
-    float accg = 0.f, accu = 0.f;
-    uint4 xc[4];
-    load_x32(xrow + wi * kGroup, xc);
-#pragma unroll
-    for (int j = 0; j < kGateBatch; ++j) {
-      const int g = wi + kGemvWaves * j;
-      if (g >= G) break;
-      const bool more = j + 1 < kGateBatch && g + kGemvWaves < G;
-      uint4 xn[4];
-      if (more) load_x32(xrow + (g + kGemvWaves) * kGroup, xn);
-      float xs = 0.f;
-      const float pg = lane_group_dot(cur.cg[j], xc, xs, true);
-      const float pu = lane_group_dot(cur.cu[j], xc, xs, false);
-      accg = fmaf(half_bits_to_f32(cur.sgu[j] & 0xffffu), fmaf(-136.f, xs, pg), accg);
-      accu = fmaf(half_bits_to_f32(cur.sgu[j] >> 16), fmaf(-136.f, xs, pu), accu);
-      if (more) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) xc[i] = xn[i];
-      }
-    }
-    accg += __shfl_xor(accg, 16);
-    accg += __shfl_xor(accg, 32);
-    accu += __shfl_xor(accu, 16);
-    accu += __shfl_xor(accu, 32);
-    if (quarter == 0) {
-      sh.red[wi][0][0][n_local] = accg;
-      sh.red[wi][0][1][n_local] = accu;
-    }
-    __syncthreads();
-    if (wi == 0) {
-      float gs = 0.f, us = 0.f;
-#pragma unroll
-      for (int w = 0; w < kGemvWaves; ++w) {
-        gs += sh.red[w][0][0][n_local];
-        us += sh.red[w][0][1][n_local];
-      }
-      const uint32_t a16 = f32_to_bf16_rne(silu_mul(gs, us));
-      const uint32_t next = __shfl_down(a16, 1);
-      if (lane < 16 && (n_local & 1) == 0) store(row, 16 * b + n_local, a16 | (next << 16));
-    }
-    __syncthreads();
+    gateup_pair_compute(sh, d, x, row, cur, b, store);
     cur = nxt;
   }
 }
