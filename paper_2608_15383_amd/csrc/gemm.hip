@@ -16,7 +16,8 @@
 //    XOR-swizzled by the row index, which makes the MFMA A-fragment reads free
 //    of bank conflicts.  The per-row bias of the group is one contiguous
 //    256-byte run and the wavefront's 64 scales one 8-byte load per lane, so a
-//    group costs each wavefront 10 vector memory instructions.
+//    group costs each wavefront 10 vector memory instructions, issued in four
+//    parts spread over the previous group's k-steps.
 //  - Each dword of codes expands in registers to one B operand of
 //    v_mfma_f32_16x16x32_bf16 (record layout in common.h): the codes enter as
 //    bf16 (128 + u), and the chain of four MFMAs of a group starts from the
@@ -45,6 +46,7 @@ constexpr int kRows = kMfmaRows;                          // 64 token rows per t
 constexpr int kChunks = kGroup / 8;                       // 16-byte chunks per row and group
 constexpr float kCodeBias = 136.f;                        // 128 (magic number) + 8 (offset binary)
 constexpr int kXcds = 8;                                  // accelerator complex dies per device
+constexpr bool kIssueFirst = true;  // a group's load part goes out before its k-step's MFMAs
 
 // Shape of a grouped-projection launch: kWaves wavefronts per workgroup, each
 // owning 4 weight row blocks (64 outputs) of a 64-token row tile, and a ring
@@ -240,19 +242,37 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   uint2 sc[kStages];
   uint4 wreg[kStages][kNPW];
 
-  // Issue every load of group g into stage S (same count in every thread):
-  // token rows into LDS, weight codes and scales into registers.
-  auto issue = [&](int g, auto stage) __attribute__((always_inline)) {
+  // The loads of group g into stage S (same count in every thread), in four
+  // parts: 0 and 1 copy half of the token-row chunks each into LDS, 2 and 3
+  // load two weight tiles each into registers (3 also the scales).  The parts
+  // go out one per k-step of the group being computed, so the wavefronts of
+  // a workgroup do not all queue their loads on the CU's address path at the
+  // same moment.
+  auto issue_part = [&](int g, auto stage, auto part) __attribute__((always_inline)) {
+    constexpr int S = decltype(stage)::value;
+    constexpr int P = decltype(part)::value;
     StageT& sm = stage_of(stage);
+    if constexpr (P < 2) {
 #pragma unroll
-    for (int j = 0; j < kDma; ++j)
-      load_lds16(x_rsrc, &sm.a[(kDma * wi + j) * 64 * 8], a_off[j], (uint32_t)g * kGroup * 2);
+      for (int j = P * (kDma / 2); j < (P + 1) * (kDma / 2); ++j)
+        load_lds16(x_rsrc, &sm.a[(kDma * wi + j) * 64 * 8], a_off[j], (uint32_t)g * kGroup * 2);
+    } else {
 #pragma unroll
-    for (int r = 0; r < kNPW; ++r)
-      wreg[decltype(stage)::value][r] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(w_rsrc, (int)(w_off + (uint32_t)(r * G * kTileBytes)),
-                   g * kTileBytes, 0));
-    sc[decltype(stage)::value] = __builtin_bit_cast(
-        uint2, __builtin_amdgcn_raw_buffer_load_b64(w_rsrc, (int)s_off, g * 128, 0));
+      for (int r = 2 * (P - 2); r < 2 * (P - 1); ++r)
+        wreg[S][r] = __builtin_bit_cast(
+            uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                       w_rsrc, (int)(w_off + (uint32_t)(r * G * kTileBytes)), g * kTileBytes, 0));
+      if constexpr (P == 3)
+        sc[S] = __builtin_bit_cast(
+            uint2, __builtin_amdgcn_raw_buffer_load_b64(w_rsrc, (int)s_off, g * 128, 0));
+    }
+  };
+  static_assert(kDma % 2 == 0 && kNPW == 4, "four load parts");
+  auto issue = [&](int g, auto stage) __attribute__((always_inline)) {
+    issue_part(g, stage, std::integral_constant<int, 0>());
+    issue_part(g, stage, std::integral_constant<int, 1>());
+    issue_part(g, stage, std::integral_constant<int, 2>());
+    issue_part(g, stage, std::integral_constant<int, 3>());
   };
 
   // Dequantization constants, hidden from constant folding (the empty asm
@@ -269,9 +289,13 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
 
   // kMB: row blocks holding tile rows (the last tile of an expert may fill
   // fewer than 4; the blocks past its rows are skipped).
-  auto compute = [&](int g, auto stage, auto mb) __attribute__((always_inline)) {
+  // With `more`, k-step i also issues load part i of group g + 1 into the
+  // other stage (before the k-step's MFMAs when kIssueFirst).
+  auto compute = [&](int g, auto stage, auto mb, auto more) __attribute__((always_inline)) {
     constexpr int S = decltype(stage)::value;
     constexpr int kMB = decltype(mb)::value;
+    constexpr bool kMore = decltype(more)::value;
+    using Next = std::integral_constant<int, S ^ 1>;
     const StageT& sm = stage_of(stage);
     f32x4_t c0[4];
 #pragma unroll
@@ -281,8 +305,13 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
 #pragma unroll
     for (int r = 0; r < kNPW; ++r) wc[r] = wreg[S][r];
     f32x4_t tmp[kNPW][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    auto kstep = [&](auto ic) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic)::value;
+      if constexpr (kMore && kIssueFirst) {
+        __builtin_amdgcn_sched_barrier(0);
+        issue_part(g + 1, Next(), ic);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       bf16x8_t a[4];
 #pragma unroll
       for (int mi = 0; mi < kMB; ++mi) {
@@ -297,7 +326,16 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
         for (int mi = 0; mi < kMB; ++mi)
           tmp[r][mi] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[mi], b, i == 0 ? c0[mi] : tmp[r][mi], 0, 0, 0);
       }
-    }
+      if constexpr (kMore && !kIssueFirst) {
+        __builtin_amdgcn_sched_barrier(0);
+        issue_part(g + 1, Next(), ic);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    kstep(std::integral_constant<int, 0>());
+    kstep(std::integral_constant<int, 1>());
+    kstep(std::integral_constant<int, 2>());
+    kstep(std::integral_constant<int, 3>());
 #pragma unroll
     for (int r = 0; r < kNPW; ++r) {
       const uint32_t sw = r < 2 ? sc[S].x : sc[S].y;
@@ -314,8 +352,11 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   // compile time so the wait counts stay exact.
   auto step = [&](int g, auto stage, auto more, auto mb) __attribute__((always_inline)) {
     constexpr int S = decltype(stage)::value;
-    if constexpr (decltype(more)::value) issue(g + 1, std::integral_constant<int, S ^ 1>());
-    if (wvalid) compute(g, stage, mb);
+    if (wvalid) {
+      compute(g, stage, mb, more);
+    } else if constexpr (decltype(more)::value) {
+      issue(g + 1, std::integral_constant<int, S ^ 1>());
+    }
     wait_loads<0>();
     barrier();
   };
