@@ -212,6 +212,32 @@ __device__ __forceinline__ void load_down_tiles(const uint8_t* __restrict__ rec,
   }
 }
 
+// Units kFrom .. nb-1 of a batch (row blocks rb + kFrom ..).
+template <int kGW, int kFrom>
+__device__ __forceinline__ void load_down_tiles_from(const uint8_t* __restrict__ rec, int d, int f,
+                                                     int rb, int nb, DownTiles<kGW>& t) {
+  const int lane = lane_id();
+  const int wi = threadIdx.x >> 6;
+  const int G = f / kGroup;
+  const RecordLayout L = record_layout(d, f);
+  const uint8_t* codes = rec + L.w2_codes + 16 * lane;
+  const uint16_t* sc = reinterpret_cast<const uint16_t*>(rec + L.w2_scales);
+#pragma unroll
+  for (int u = kFrom; u < DownTiles<kGW>::kUnits; ++u) {
+    if (u < nb) {
+      const int n = 16 * (rb + u) + (lane & 15);
+#pragma unroll
+      for (int j = 0; j < kGW; ++j) {
+        const int g = wi + 4 * j;
+        if (g < G) {
+          t.c[u][j] = *reinterpret_cast<const uint4*>(codes + ((int64_t)(rb + u) * G + g) * kTileBytes);
+          t.s[u][j] = sc[scale_index(n, g, G)];
+        }
+      }
+    }
+  }
+}
+
 // Row blocks rb .. rb+kN-1 into units 0 .. kN-1, every load issued so that
 // the waits for loads issued before these stay exact: a unit past nb reads
 // unit nb-1 again, a row block past the last reads the last one and a slot
@@ -239,14 +265,20 @@ __device__ __forceinline__ void load_down_tiles_all(const uint8_t* __restrict__ 
   }
 }
 
-// Down row blocks a gate/up worker of one row-block pair loads with its
-// gate/up tiles.
+// Down row blocks a gate/up worker loads with its gate/up tiles: with those
+// of a one-pair item, and with the last pair's of a several-pair item (the
+// rest of its first batch follows in the down part).
 constexpr int kDownEarly = 2;
+template <int kGW>
+constexpr int kDownEarlyMany = 8 / kGW;  // eight tiles per wavefront
 
 // kDevEpoch: the launch is being captured into a graph and reads its epoch
 // from DecodeSync (a.epoch is 0); otherwise a.epoch is the host's number.
 // kGW: input groups of the down projection per wavefront (d_ff <= 512 kGW).
-template <bool kDevEpoch, int kGW>
+// kMany: gate/up items may hold several row-block pairs (pairs_per_item > 1);
+// without it the launch has one-pair items only and compiles without the
+// several-pair code, which leaves that code's registers to the rest.
+template <bool kDevEpoch, int kGW, bool kMany>
 __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   __shared__ GroupShared<256> gsh;
   __shared__ GateUpShared gush;
@@ -383,17 +415,24 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   using Tiles = DownTiles<kGW>;
   Tiles dn;
   const uint8_t* drec = a.slot_bank + (int64_t)s_ids[max(q, 0)] * a.record_bytes;
-  const bool early = is_gate && a.pairs_per_item == 1 && a.down_r <= kDownEarly &&
-                     a.d == kGemvWaves * kGateBatch * kGroup;
+  // Gate/up item: pair pi, row-block pairs b0 .. b1-1.
+  const int pi = wk / chunks;
+  const int b0 = (wk % chunks) * a.pairs_per_item;
+  const int b1 = min(b0 + a.pairs_per_item, a.f / kTileRows);
+  // Items whose tiles all load in one batch per pair issue this worker's
+  // first batch of down tiles with their last gate/up tiles: a one-pair item
+  // (down_r <= kDownEarly) with the pair's tiles, a several-pair item in
+  // place of the next pair's.
+  const bool one_batch = a.d <= kGemvWaves * kGateBatch * kGroup;
+  const bool early_one = is_gate && b1 - b0 == 1 && a.down_r <= kDownEarly &&
+                         a.d == kGemvWaves * kGateBatch * kGroup;
+  const bool early_many = kMany && is_gate && b1 - b0 > 1 && one_batch;
+  const bool early = early_one || early_many;
 
   if (is_gate) {
     // ---------------------------------------------------------------- gate/up
     // Item = (pair pi, row-block pairs b0 ..): one token row of one expert.
     // The activation goes to act row pi (pair order).
-    const int pi = wk / chunks;
-    const int pairs_of_f = a.f / kTileRows;
-    const int b0 = (wk % chunks) * a.pairs_per_item;
-    const int b1 = min(b0 + a.pairs_per_item, pairs_of_f);
     const int e = s_ids[pi];
     const int top_k = a.top_k;
     // The activation goes out as tagged words (DecodeSync::act), which the
@@ -406,18 +445,24 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
                          __HIP_MEMORY_SCOPE_AGENT);
     };
     const uint8_t* rec = a.slot_bank + (int64_t)e * a.record_bytes;
-    if (early) {
-      // One row-block pair: its tiles, then this worker's down tiles, are
-      // issued before the pair is computed, so the down tiles stream with
-      // the gate/up weights (a worker of pair 0, which has no down work,
-      // reads pair 0's tiles, unused).
+    // (A worker of pair 0, which has no down work, reads pair 0's tiles,
+    // unused.)
+    if (early_one) {
+      // The pair's tiles, then this worker's down tiles, are issued before
+      // the pair is computed, so the down tiles stream with the gate/up
+      // weights.
       GateUpBatch gb;
       gateup_load_batch(rec, d, f, b0, gb);
       load_down_tiles_all<kGW, kDownEarly>(drec, d, f, rb0, max(nu, 1), dn);
       gateup_pair_compute<true>(gush, d, h_lds + (pi / top_k) * d, pi, gb, b0, store_act);
-    } else if (b1 - b0 > 1 && d <= kGemvWaves * kGateBatch * kGroup) {
-      // The next row-block pair's tiles load while this one is computed.
-      gateup_row_blocks(gush, d, f, h_lds + (pi / top_k) * d, pi, rec, b0, b1, store_act);
+    } else if (early_many) {
+      // The next row-block pair's tiles load while this one is computed, and
+      // the down tiles while the last one is.
+      if constexpr (kMany)
+        gateup_row_blocks(gush, d, f, h_lds + (pi / top_k) * d, pi, rec, b0, b1, store_act, [&] {
+          load_down_tiles_all<kGW, kDownEarlyMany<kGW>>(
+              drec, d, f, rb0, max(min(nu, kDownEarlyMany<kGW>), 1), dn);
+        });
     } else {
       for (int b = b0; b < b1; ++b)
         gateup_rows(gush, d, f, [=](int s) { return h_lds + (s / top_k) * d; }, pi, pi + 1, rec,
@@ -437,7 +482,11 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   EMOE_PHASE(3);  // down part reached
   bool act_late = false;
   if (nu > 0) {
-    if (!early) load_down_tiles<kGW>(drec, a.d, a.f, rb0, min(nu, Tiles::kUnits), dn);
+    if (!early)
+      load_down_tiles<kGW>(drec, a.d, a.f, rb0, min(nu, Tiles::kUnits), dn);
+    else if (kMany && early_many)
+      load_down_tiles_from<kGW, kDownEarlyMany<kGW>>(drec, a.d, a.f, rb0, min(nu, Tiles::kUnits),
+                                                     dn);
     // This wavefront's groups of activation row q, from the tagged words
     // (one per lane and group, all read before any is checked; bounded wait)
     // into its LDS slot.
@@ -590,20 +639,31 @@ int fused_capacity() {
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
   std::lock_guard<std::mutex> lk(mu);
   if (cap[dev] == 0) {
-    int per_cu[4] = {}, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu[0], decode_fused_kernel<false, 2>,
-                                                     256, 0) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu[1], decode_fused_kernel<true, 2>,
-                                                     256, 0) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu[2], decode_fused_kernel<false, 4>,
-                                                     256, 0) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu[3], decode_fused_kernel<true, 4>,
-                                                     256, 0) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    // Every instantiation (epoch source, down groups per wavefront, items
+    // of several pairs or not) must fit the same number per CU.
+    const void* kernels[8] = {
+        reinterpret_cast<const void*>(decode_fused_kernel<false, 2, false>),
+        reinterpret_cast<const void*>(decode_fused_kernel<true, 2, false>),
+        reinterpret_cast<const void*>(decode_fused_kernel<false, 4, false>),
+        reinterpret_cast<const void*>(decode_fused_kernel<true, 4, false>),
+        reinterpret_cast<const void*>(decode_fused_kernel<false, 2, true>),
+        reinterpret_cast<const void*>(decode_fused_kernel<true, 2, true>),
+        reinterpret_cast<const void*>(decode_fused_kernel<false, 4, true>),
+        reinterpret_cast<const void*>(decode_fused_kernel<true, 4, true>)};
+    int per_cu = 1 << 30, cus = 0;
+    for (const void* k : kernels) {
+      int n = 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, 256, 0) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+      }
+      per_cu = min(per_cu, n);
+    }
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
       (void)hipGetLastError();
       return 0;
     }
-    cap[dev] = min(min(per_cu[0], per_cu[1]), min(per_cu[2], per_cu[3])) * cus;
+    cap[dev] = per_cu * cus;
   }
   return cap[dev];
 }
@@ -657,16 +717,17 @@ hipError_t launch_decode_fused(DecodeArgs& a, DecodeProgress& prog, hipStream_t 
   }
   const dim3 grid(a.n_router + a.n_work);
   const bool dev_epoch = a.epoch == 0u;
-  if (a.gw == 2) {
-    if (dev_epoch)
-      launch(decode_fused_kernel<true, 2>, grid, dim3(256), stream, a);
-    else
-      launch(decode_fused_kernel<false, 2>, grid, dim3(256), stream, a);
-  } else {
-    if (dev_epoch)
-      launch(decode_fused_kernel<true, 4>, grid, dim3(256), stream, a);
-    else
-      launch(decode_fused_kernel<false, 4>, grid, dim3(256), stream, a);
+  const bool many = a.pairs_per_item > 1;
+  const int form = (dev_epoch ? 1 : 0) | (a.gw == 2 ? 0 : 2) | (many ? 4 : 0);
+  switch (form) {
+    case 0: launch(decode_fused_kernel<false, 2, false>, grid, dim3(256), stream, a); break;
+    case 1: launch(decode_fused_kernel<true, 2, false>, grid, dim3(256), stream, a); break;
+    case 2: launch(decode_fused_kernel<false, 4, false>, grid, dim3(256), stream, a); break;
+    case 3: launch(decode_fused_kernel<true, 4, false>, grid, dim3(256), stream, a); break;
+    case 4: launch(decode_fused_kernel<false, 2, true>, grid, dim3(256), stream, a); break;
+    case 5: launch(decode_fused_kernel<true, 2, true>, grid, dim3(256), stream, a); break;
+    case 6: launch(decode_fused_kernel<false, 4, true>, grid, dim3(256), stream, a); break;
+    default: launch(decode_fused_kernel<true, 4, true>, grid, dim3(256), stream, a); break;
   }
   e = hipGetLastError();
   if (e == hipSuccess && !dev_epoch) prog.epoch = a.epoch;

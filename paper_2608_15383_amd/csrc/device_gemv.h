@@ -133,10 +133,13 @@ __device__ __forceinline__ void gateup_load_batch(const uint8_t* __restrict__ re
 // every slot of the batch is a group and the code has no branch on the
 // group count (a branch would let the compiler sink a tile's load into it,
 // behind any loads the caller issued after the batch's, and wait for those).
-template <bool kFull = false, typename Store>
+// kXs: 0 forms each group's activation sum inline, 1 also keeps it in xsv[j],
+// 2 takes it from xsv[j] (the same value: the row and the groups are the same
+// for every pair of an item).
+template <bool kFull = false, int kXs = 0, typename Store>
 __device__ __forceinline__ void gateup_pair_compute(GateUpShared& sh, int d, const uint16_t* x,
                                                     int row, const GateUpBatch& cur, int b,
-                                                    Store store) {
+                                                    Store store, float* xsv = nullptr) {
   const int lane = lane_id();
   const int wi = threadIdx.x >> 6;
   const int G = kFull ? kGemvWaves * kGateBatch : d / kGroup;
@@ -153,9 +156,10 @@ __device__ __forceinline__ void gateup_pair_compute(GateUpShared& sh, int d, con
     const bool more = j + 1 < kGateBatch && (kFull || g + kGemvWaves < G);
     uint4 xn[4];
     if (more) load_x32(xrow + (g + kGemvWaves) * kGroup, xn);
-    float xs = 0.f;
-    const float pg = lane_group_dot(cur.cg[j], xc, xs, true);
+    float xs = kXs == 2 ? xsv[j] : 0.f;
+    const float pg = lane_group_dot(cur.cg[j], xc, xs, kXs != 2);
     const float pu = lane_group_dot(cur.cu[j], xc, xs, false);
+    if (kXs == 1) xsv[j] = xs;
     accg = fmaf(half_bits_to_f32(cur.sgu[j] & 0xffffu), fmaf(-136.f, xs, pg), accg);
     accu = fmaf(half_bits_to_f32(cur.sgu[j] >> 16), fmaf(-136.f, xs, pu), accu);
     if (more) {
@@ -186,23 +190,34 @@ __device__ __forceinline__ void gateup_pair_compute(GateUpShared& sh, int d, con
   __syncthreads();
 }
 
-// gateup_pair_compute over the row-block pairs b0 .. b1-1, with the next
-// pair's tiles loaded while the current pair is computed.
-template <typename Store>
+// gateup_pair_compute over the row-block pairs b0 .. b1-1 (b1 - b0 >= 2),
+// with the next pair's tiles loaded while the current pair is computed; in
+// place of a next pair, the last pair runs after `last_loads()`, the caller's
+// loads for what follows (all of them issued unconditionally, so the wait
+// for the last pair's tiles stays exact).
+template <typename Store, typename LastLoads>
 __device__ __forceinline__ void gateup_row_blocks(GateUpShared& sh, int d, int f,
                                                   const uint16_t* x, int row,
                                                   const uint8_t* __restrict__ rec, int b0, int b1,
-                                                  Store store) {
+                                                  Store store, LastLoads last_loads) {
   GateUpBatch cur;
   gateup_load_batch(rec, d, f, b0, cur);
-  for (int b = b0; b < b1; ++b) {
-    // The last pair loads itself again (unused), so every pass issues the
-    // same loads and the wait for the current pair's tiles stays exact.
+  // The first pair forms the groups' activation sums, the others reuse them.
+  float xsv[kGateBatch];
+  {
     GateUpBatch nxt;
-    gateup_load_batch(rec, d, f, min(b + 1, b1 - 1), nxt);
-    gateup_pair_compute(sh, d, x, row, cur, b, store);
+    gateup_load_batch(rec, d, f, b0 + 1, nxt);
+    gateup_pair_compute<false, 1>(sh, d, x, row, cur, b0, store, xsv);
     cur = nxt;
   }
+  for (int b = b0 + 1; b < b1 - 1; ++b) {
+    GateUpBatch nxt;
+    gateup_load_batch(rec, d, f, b + 1, nxt);
+    gateup_pair_compute<false, 2>(sh, d, x, row, cur, b, store, xsv);
+    cur = nxt;
+  }
+  last_loads();
+  gateup_pair_compute<false, 2>(sh, d, x, row, cur, b1 - 1, store, xsv);
 }
 
 // The grouped rows [begin, end) of one expert; the token of grouped row s is
