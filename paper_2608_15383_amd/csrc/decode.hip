@@ -52,21 +52,41 @@ namespace {
 
 // Phase timestamps for measurement builds (compiled with -DEMOE_PHASE_TRACE by
 // phase_trace.py; absent otherwise): word 16 b + i holds the wall clock
-// (100 MHz) at which workgroup b passed phase i.  The stores perturb the
-// timing a little (they count on the same vector-memory counter as the loads).
+// (100 MHz) at which workgroup b passed phase i.  Thread 0 keeps them in LDS
+// while the workgroup runs and copies them out as it exits, so the trace adds
+// no stores to the vector-memory counter that the kernel's own waits count.
 #ifdef EMOE_PHASE_TRACE
 __device__ uint64_t g_phase_trace[kFusedMaxBlocks * 16];
+#define EMOE_TRACE_LDS __shared__ uint64_t s_trace[16]
+#define EMOE_TRACE_INIT()                                                               \
+  do {                                                                                  \
+    if (threadIdx.x == 0)                                                               \
+      for (int k_ = 0; k_ < 16; ++k_) s_trace[k_] = 0;                                  \
+  } while (0)
 #define EMOE_PHASE(i)                                                                   \
   do {                                                                                  \
-    if (threadIdx.x == 0) g_phase_trace[blockIdx.x * 16 + (i)] = wall_clock64();        \
+    if (threadIdx.x == 0) s_trace[i] = wall_clock64();                                  \
   } while (0)
 #define EMOE_PHASE_WAVE(i)                                                              \
   do {                                                                                  \
-    if (lane_id() == 0) g_phase_trace[blockIdx.x * 16 + (i)] = wall_clock64();          \
+    if (threadIdx.x == 0) s_trace[i] = wall_clock64();                                  \
+  } while (0)
+#define EMOE_TRACE_SET(i, v)                                                            \
+  do {                                                                                  \
+    if (threadIdx.x == 0) s_trace[i] = (v);                                             \
+  } while (0)
+#define EMOE_TRACE_FLUSH()                                                              \
+  do {                                                                                  \
+    if (threadIdx.x == 0)                                                               \
+      for (int k_ = 0; k_ < 16; ++k_) g_phase_trace[blockIdx.x * 16 + k_] = s_trace[k_]; \
   } while (0)
 #else
+#define EMOE_TRACE_LDS static_assert(true, "")
+#define EMOE_TRACE_INIT() do {} while (0)
 #define EMOE_PHASE(i) do {} while (0)
 #define EMOE_PHASE_WAVE(i) do {} while (0)
+#define EMOE_TRACE_SET(i, v) do {} while (0)
+#define EMOE_TRACE_FLUSH() do {} while (0)
 #endif
 
 constexpr uint32_t kSpinLimit = 1u << 20;
@@ -179,17 +199,17 @@ __device__ __forceinline__ void wave_copy_to_lds(const void* src, uint32_t bytes
 // Down tiles of one wavefront for up to kUnits row blocks: input groups
 // g = wi + 4j (j < kGW) of each, codes (this lane's 16 bytes of the tile) and
 // raw fp16 scales (converted at use, so no load waits for another).
-template <int kGW>
+template <int kGW, int kU = 16 / kGW>
 struct DownTiles {
-  static constexpr int kUnits = 16 / kGW;  // row blocks per batch (64 code registers)
+  static constexpr int kUnits = kU;  // row blocks per batch (at most 64 code registers)
   uint4 c[kUnits][kGW];
   uint16_t s[kUnits][kGW];
 };
 
 // Load this wavefront's tiles of row blocks rb .. rb+nb-1 (nb <= kUnits).
-template <int kGW>
+template <int kGW, int kU>
 __device__ __forceinline__ void load_down_tiles(const uint8_t* __restrict__ rec, int d, int f,
-                                                int rb, int nb, DownTiles<kGW>& t) {
+                                                int rb, int nb, DownTiles<kGW, kU>& t) {
   const int lane = lane_id();
   const int wi = threadIdx.x >> 6;
   const int G = f / kGroup;
@@ -197,7 +217,7 @@ __device__ __forceinline__ void load_down_tiles(const uint8_t* __restrict__ rec,
   const uint8_t* codes = rec + L.w2_codes + 16 * lane;
   const uint16_t* sc = reinterpret_cast<const uint16_t*>(rec + L.w2_scales);
 #pragma unroll
-  for (int u = 0; u < DownTiles<kGW>::kUnits; ++u) {
+  for (int u = 0; u < kU; ++u) {
     if (u < nb) {
       const int n = 16 * (rb + u) + (lane & 15);
 #pragma unroll
@@ -213,9 +233,9 @@ __device__ __forceinline__ void load_down_tiles(const uint8_t* __restrict__ rec,
 }
 
 // Units kFrom .. nb-1 of a batch (row blocks rb + kFrom ..).
-template <int kGW, int kFrom>
+template <int kGW, int kFrom, int kU>
 __device__ __forceinline__ void load_down_tiles_from(const uint8_t* __restrict__ rec, int d, int f,
-                                                     int rb, int nb, DownTiles<kGW>& t) {
+                                                     int rb, int nb, DownTiles<kGW, kU>& t) {
   const int lane = lane_id();
   const int wi = threadIdx.x >> 6;
   const int G = f / kGroup;
@@ -223,7 +243,7 @@ __device__ __forceinline__ void load_down_tiles_from(const uint8_t* __restrict__
   const uint8_t* codes = rec + L.w2_codes + 16 * lane;
   const uint16_t* sc = reinterpret_cast<const uint16_t*>(rec + L.w2_scales);
 #pragma unroll
-  for (int u = kFrom; u < DownTiles<kGW>::kUnits; ++u) {
+  for (int u = kFrom; u < kU; ++u) {
     if (u < nb) {
       const int n = 16 * (rb + u) + (lane & 15);
 #pragma unroll
@@ -242,10 +262,10 @@ __device__ __forceinline__ void load_down_tiles_from(const uint8_t* __restrict__
 // the waits for loads issued before these stay exact: a unit past nb reads
 // unit nb-1 again, a row block past the last reads the last one and a slot
 // past the last group reads the last group (all unused).
-template <int kGW, int kN>
+template <int kGW, int kN, int kU>
 __device__ __forceinline__ void load_down_tiles_all(const uint8_t* __restrict__ rec, int d, int f,
-                                                    int rb, int nb, DownTiles<kGW>& t) {
-  static_assert(kN <= DownTiles<kGW>::kUnits, "units of one batch");
+                                                    int rb, int nb, DownTiles<kGW, kU>& t) {
+  static_assert(kN <= kU, "units of one batch");
   const int lane = lane_id();
   const int wi = threadIdx.x >> 6;
   const int G = f / kGroup;
@@ -298,13 +318,14 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   DecodeSync* sy = a.sync;
   const int P = a.tokens * a.top_k;
   const uint32_t epoch = kDevEpoch ? launch_epoch(sy) : a.epoch;
+  EMOE_TRACE_LDS;
+  EMOE_TRACE_INIT();
   EMOE_PHASE(0);  // start
-#ifdef EMOE_PHASE_TRACE
-  if (blk == 0 && tid == 0) {  // the layout, for reading the trace
-    g_phase_trace[14] = (uint64_t)a.n_router | (uint64_t)a.n_gate << 16 | (uint64_t)a.n_work << 32;
-    g_phase_trace[15] = (uint64_t)a.pairs_per_item | (uint64_t)a.down_r << 16 | (uint64_t)a.tail_r << 32;
+  if (blk == 0) {  // the layout, for reading the trace
+    EMOE_TRACE_SET(14, (uint64_t)a.n_router | (uint64_t)a.n_gate << 16 | (uint64_t)a.n_work << 32);
+    EMOE_TRACE_SET(15, (uint64_t)a.pairs_per_item | (uint64_t)a.down_r << 16 |
+                           (uint64_t)a.tail_r << 32);
   }
-#endif
 
   if (blk < a.n_router) {
     // ---------------------------------------------------------------- router
@@ -334,6 +355,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
       if (tid == 0) arrive(sy, epoch, blk);
       if (blk == 0 && wi == 0) advance_epoch(sy, epoch, (int)gridDim.x);
     }
+    EMOE_TRACE_FLUSH();
     return;
   }
 
@@ -412,7 +434,10 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
 
 
   // The first batch of this worker's down tiles (pair q's record).
-  using Tiles = DownTiles<kGW>;
+  // One-pair launches take their down work in batches of kDownEarly row
+  // blocks (all of it at OLMoE shape), which keeps the unrolled arithmetic,
+  // run by every workgroup at the same moment, short.
+  using Tiles = DownTiles<kGW, kMany ? 16 / kGW : kDownEarly>;
   Tiles dn;
   const uint8_t* drec = a.slot_bank + (int64_t)s_ids[max(q, 0)] * a.record_bytes;
   // Gate/up item: pair pi, row-block pairs b0 .. b1-1.
@@ -628,6 +653,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     block_group<256, false>(gsh, P, a.n_experts, s_ids, a.counts, a.offsets, a.sorted_pairs,
                             a.active, a.n_active, nullptr, a.pair_pos, 1);
   }
+  EMOE_TRACE_FLUSH();
 }
 
 // Co-resident workgroups of the fused kernel (either form) on the current
