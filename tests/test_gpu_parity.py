@@ -546,9 +546,13 @@ def test_prefill_paths_agree(olmoe):
 @pytest.mark.parametrize("shape,tokens", [(TINY, 1), (TINY, 4), (LayerShape(384, 256, 6, 3), 3),
                                           (LayerShape(256, 384, 1, 1), 1),
                                           (LayerShape(128, 128, 200, 8), 4), (OLMOE, 2),
-                                          (OLMOE, 4)])
+                                          (OLMOE, 4), (LayerShape(2048, 2048, 8, 4), 1),
+                                          (LayerShape(2048, 2048, 8, 4), 4),
+                                          (LayerShape(512, 1536, 8, 2), 3)])
 def test_fused_decode_matches_unfused_bitwise(shape, tokens):
-    """The single-launch decode layer equals the per-kernel path bit for bit."""
+    """The single-launch decode layer equals the per-kernel path bit for bit:
+    one- and several-pair items, one and two router items per expert quad, and
+    two and four down input groups per wavefront (d_ff above 1024)."""
     lay = make_layer(shape, tokens, seed=17)
     layer = Layer(dims_of(shape), lay, tokens)
     st = api.Stats()
