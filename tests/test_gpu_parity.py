@@ -589,11 +589,12 @@ def test_fused_decode_repeated_calls_and_override():
 
 
 @pytest.mark.parametrize("tokens,path,launches,override",
-                         [(2, api.EMOE_PATH_AUTO, 1, False), (3, api.EMOE_PATH_AUTO, 1, True),
+                         [(1, api.EMOE_PATH_AUTO, 1, False), (2, api.EMOE_PATH_AUTO, 1, False),
+                          (3, api.EMOE_PATH_AUTO, 1, True),
                           (8, GEMV, None, False), (48, MFMA, None, False)])
 def test_resident_layer_replays_from_a_captured_graph(tokens, path, launches, override):
     """A fully resident layer call captured into a HIP graph replays correctly,
-    replay after replay: the fused decode launch (2 tokens) takes its hand-over
+    replay after replay: the fused decode launch (1-3 tokens) takes its hand-over
     epoch from device memory, not from its launch arguments.  Eager calls run
     between the replays; every replay equals the eager call on the same input
     bit for bit."""
