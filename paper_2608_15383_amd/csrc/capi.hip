@@ -846,15 +846,25 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
                                      fused_bias ? tok_bias : nullptr));
     ds.kernel_launches += 1;
   }
-  EMOE_LAUNCH(EMOE_K_TOPK, stream, launch_topk(T, E, k, renormalize, z, ids, wts, stream));
   if (P > kGroupWideMinPairs) {
+    // Wide grouping: per-chunk counts (with the top-k when top_k divides 64),
+    // then the placement.
     int32_t* chunk_counts = reinterpret_cast<int32_t*>(ws + L.chunk_counts);
-    EMOE_LAUNCH(EMOE_K_GROUP_COUNT, stream, launch_group_count(P, E, ids, chunk_counts, stream));
+    if (topk_count_fits(k)) {
+      EMOE_LAUNCH(EMOE_K_TOPK, stream,
+                  launch_topk_count(T, E, k, renormalize, z, ids, wts, chunk_counts, stream));
+      ds.kernel_launches += 1;
+    } else {
+      EMOE_LAUNCH(EMOE_K_TOPK, stream, launch_topk(T, E, k, renormalize, z, ids, wts, stream));
+      EMOE_LAUNCH(EMOE_K_GROUP_COUNT, stream, launch_group_count(P, E, ids, chunk_counts, stream));
+      ds.kernel_launches += 2;
+    }
     EMOE_LAUNCH(EMOE_K_GROUP, stream,
                 launch_group_place(P, E, ids, chunk_counts, counts, offsets, sorted, active,
                                    n_active, tiles, pair_pos, mfma_rows, stream));
-    ds.kernel_launches += 3;
+    ds.kernel_launches += 1;
   } else {
+    EMOE_LAUNCH(EMOE_K_TOPK, stream, launch_topk(T, E, k, renormalize, z, ids, wts, stream));
     EMOE_LAUNCH(EMOE_K_GROUP, stream,
                 launch_group(P, E, ids, counts, offsets, sorted, active, n_active, tiles, pair_pos,
                              mfma_rows, stream));

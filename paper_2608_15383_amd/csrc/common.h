@@ -289,6 +289,12 @@ hipError_t launch_group(int pairs, int n_experts, const int32_t* topk_ids, int32
 // offsets and a stable placement (identical results to launch_group).
 hipError_t launch_group_count(int pairs, int n_experts, const int32_t* topk_ids,
                               int32_t* chunk_counts, hipStream_t stream);
+// Top-k (as launch_topk) together with launch_group_count's chunk_counts, in
+// one launch; only for top_k dividing 64 with 64 / top_k <= 16.
+constexpr bool topk_count_fits(int top_k) { return top_k >= 4 && 64 % top_k == 0; }
+hipError_t launch_topk_count(int tokens, int n_experts, int top_k, int renormalize,
+                             const float* logits, int32_t* topk_ids, float* topk_w,
+                             int32_t* chunk_counts, hipStream_t stream);
 hipError_t launch_group_place(int pairs, int n_experts, const int32_t* topk_ids,
                               const int32_t* chunk_counts, int32_t* counts, int32_t* offsets,
                               int32_t* sorted_pairs, int32_t* active, int32_t* n_active,

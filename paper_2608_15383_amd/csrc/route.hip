@@ -1,10 +1,13 @@
-// Routing and grouping kernels (Sec. 3.1 Eq. 1, Fig. 1 "tokens are grouped by
-// selected expert", Sec. 3.4).  The arithmetic lives in device_route.h.
+// Routing and grouping kernels (Sec. 3.1 Eq. 1; Fig. 1 and Sec. 3.4, where the
+// token-expert pairs are gathered by the expert they select).  The arithmetic
+// lives in device_route.h.
 //
 //   router_logits_kernel: z[t][e] = fp32(sum_i h[t][i] * W_r[e][i]), fp64 sum
 //                         on fp64 MFMA.
 //   topk_kernel:          k largest logits per token (ties -> lower expert id)
 //                         and their softmax mixture weights in fp64.
+//   topk_count_kernel:    the same for the 64 / k tokens of one 64-pair chunk
+//                         per workgroup, plus that chunk's per-expert counts.
 //   group_kernel:         per-expert counts, exclusive offsets, a stable
 //                         counting sort of pair ids, the ascending active list
 //                         and (optionally) the MFMA row-tile prefix sum.
@@ -107,6 +110,47 @@ __global__ __launch_bounds__(256) void topk_kernel(int tokens, int n_experts, in
   wave_topk<false>(logits + (int64_t)t * n_experts, n_experts, top_k, renormalize,
                    topk_ids + (int64_t)t * top_k, topk_w + (int64_t)t * top_k,
                    s_rank[threadIdx.x >> 6]);
+}
+
+// Top-k of 64 / top_k tokens per workgroup, one wavefront each, when top_k
+// divides 64: the workgroup's pairs are then exactly one 64-pair chunk of the
+// wide grouping (chunk c = blockIdx.x), and after its selections it also
+// writes that chunk's per-expert counts (chunk_count_kernel's row), which
+// saves that launch.  Ids and weights as topk_kernel writes them.
+__global__ __launch_bounds__(1024) void topk_count_kernel(int tokens, int n_experts, int top_k,
+                                                          int renormalize,
+                                                          const float* __restrict__ logits,
+                                                          int32_t* __restrict__ topk_ids,
+                                                          float* __restrict__ topk_w,
+                                                          int32_t* __restrict__ chunk_counts) {
+  __shared__ uint64_t s_rank[16][64];  // per-wavefront top-k scratch
+  __shared__ int s_pair[64];           // the chunk's expert ids, pair order
+  __shared__ int row[EMOE_MAX_EXPERTS];
+  const int lane = lane_id();
+  const int wave = threadIdx.x >> 6;
+  const int c = blockIdx.x;
+  const int t = c * (64 / top_k) + wave;
+  for (int e = threadIdx.x; e < n_experts; e += blockDim.x) row[e] = 0;
+  if (t < tokens) {
+    TopkState st;
+    wave_topk_select<false>(logits + (int64_t)t * n_experts, n_experts, top_k, st, s_rank[wave]);
+    wave_topk_store_ids<false>(st, top_k, topk_ids + (int64_t)t * top_k);
+#pragma unroll
+    for (int r = 0; r < kPerLane; ++r)
+      if (lane + 64 * r < top_k) s_pair[wave * top_k + lane + 64 * r] = st.sel_id[r];
+    wave_topk_weights<false>(st, n_experts, top_k, renormalize, topk_w + (int64_t)t * top_k);
+  }
+  __syncthreads();
+  if (wave == 0) {
+    int bits = 0;
+    while ((1 << bits) < n_experts) ++bits;
+    const bool valid = 64 * c + lane < tokens * top_k;
+    const int e = valid ? s_pair[lane] : 0;
+    const uint64_t m = match_expert(valid, e, bits);
+    const int rank = __popcll(m & ((1ull << lane) - 1ull));
+    if (valid && rank == 0) row[e] = __popcll(m);  // one wavefront: LDS accesses stay in order
+    for (int x = lane; x < n_experts; x += 64) chunk_counts[(int64_t)c * n_experts + x] = row[x];
+  }
 }
 
 constexpr int kGroupThreads = 1024;
@@ -295,6 +339,17 @@ hipError_t launch_topk(int tokens, int n_experts, int top_k, int renormalize, co
   if (tokens == 0) return hipSuccess;
   launch(topk_kernel, dim3((tokens + 3) / 4), dim3(256), stream, tokens, n_experts, top_k,
          renormalize, logits, topk_ids, topk_w);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk_count(int tokens, int n_experts, int top_k, int renormalize,
+                             const float* logits, int32_t* topk_ids, float* topk_w,
+                             int32_t* chunk_counts, hipStream_t stream) {
+  if (tokens == 0) return hipSuccess;
+  if (top_k < 1 || 64 % top_k != 0 || 64 / top_k > 16) return hipErrorInvalidValue;
+  const int per = 64 / top_k;  // tokens (wavefronts) per chunk
+  launch(topk_count_kernel, dim3((tokens + per - 1) / per), dim3(64 * per), stream, tokens,
+         n_experts, top_k, renormalize, logits, topk_ids, topk_w, chunk_counts);
   return hipGetLastError();
 }
 

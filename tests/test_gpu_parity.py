@@ -245,10 +245,15 @@ def test_mfma_past_its_group_limit_is_a_shape_error():
 
 
 @pytest.mark.parametrize("shape,tokens", [(LayerShape(128, 128, 200, 5), 300),
-                                          (LayerShape(128, 128, 64, 8), 2048)])
+                                          (LayerShape(128, 128, 64, 8), 2048),
+                                          (LayerShape(128, 128, 64, 4), 700),
+                                          (LayerShape(128, 128, 96, 16), 101)])
 def test_forward_grouping_of_large_calls_bit_exact(shape, tokens):
     """Calls above 1024 pairs group over many workgroups (per-chunk counts, then
-    a stable placement); the arrays must equal the oracle's grouping.  The
+    a stable placement); the arrays must equal the oracle's grouping.  With
+    top_k dividing 64 the top-k launch also counts the chunks (64 / top_k
+    tokens per workgroup; the last chunk ragged here), otherwise a separate
+    launch does.  The
     MFMA row-tile prefix sum counts the experts on the MFMA kernels: all of
     them on the MFMA path, those with at least EMOE_MIXED_MFMA_ROWS rows on the
     mixed path, none on the GEMV path."""
