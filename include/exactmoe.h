@@ -331,6 +331,14 @@ int32_t emoe_test_fail_copy_after(int64_t copies);
  * exits, so a fill that did not wait for the slot's completion event would
  * overwrite records still being read.  Off by default. */
 int32_t emoe_test_set_wave_delay(emoe_cache* cache, int32_t microseconds);
+/* Failure forcing for tests of the fused decode launch's bounded waits (the
+ * hand-over of logits, activation rows and expert outputs between its
+ * workgroups): a wait gives up after `spin_limit` polls (1 .. 2^20; 2^20 is
+ * the default), and with `unmatched` = 1 the readers wait for a tag that no
+ * writer uses, so every wait gives up.  A workgroup whose wait gave up writes
+ * NaN outputs and counts the timeout (emoe_cache_sync_timeouts); every
+ * workgroup still exits.  (2^20, 0) restores the normal launch. */
+int32_t emoe_test_set_decode_waits(emoe_cache* cache, int32_t spin_limit, int32_t unmatched);
 
 /* ---------------------------------------------------------------- kernel timing */
 /* Kernels launched by the layer calls, as reported by emoe_profile_end. */

@@ -91,6 +91,7 @@ SIGNATURES = {
                                         C.POINTER(Stats)]),
     "emoe_test_fail_copy_after": (_i32, [C.c_int64]),
     "emoe_test_set_wave_delay": (_i32, [_vp, _i32]),
+    "emoe_test_set_decode_waits": (_i32, [_vp, _i32, _i32]),
     "emoe_decoder_kv_bytes": (C.c_size_t, [C.POINTER(DecoderDims)]),
     "emoe_decoder_workspace_bytes": (C.c_size_t, [C.POINTER(DecoderDims), _i32]),
     "emoe_decoder_create": (_i32, [C.POINTER(DecoderDims), C.POINTER(DecoderWeights),

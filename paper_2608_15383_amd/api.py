@@ -138,6 +138,11 @@ class Cache:
         """emoe_test_set_wave_delay: spin before each wave's projections (test hook)."""
         check(lib().emoe_test_set_wave_delay(self.handle, int(microseconds)))
 
+    def set_decode_waits(self, spin_limit: int = 1 << 20, unmatched: bool = False) -> None:
+        """emoe_test_set_decode_waits: the fused decode launch's waits give up after
+        `spin_limit` polls; with `unmatched` they wait for a tag no writer uses (test hook)."""
+        check(lib().emoe_test_set_decode_waits(self.handle, int(spin_limit), int(bool(unmatched))))
+
     def plan_waves(self, counts) -> list[list[int]]:
         e = self.dims.n_experts
         cnt = np.ascontiguousarray(counts, np.int32)

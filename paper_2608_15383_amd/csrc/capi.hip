@@ -124,6 +124,8 @@ struct emoe_cache {
   DecodeSync* sync = nullptr;       // device: hand-over data of the fused decode launches
   DecodeProgress prog;              // host: epoch of the last direct fused launch
   int32_t wave_delay_us = 0;        // test hook: spin before each wave's projections
+  uint32_t decode_spin_limit = 1u << 20;  // test hook: polls before a fused-launch wait gives up
+  uint32_t decode_tag_xor = 0;            // test hook: nonzero, the fused launch's waits never match
   bool overlap = false;             // waves of C/2 so fills overlap the previous wave
   void* scratch = nullptr;          // device address of this device's no-alloc workspace
 };
@@ -821,6 +823,8 @@ int32_t forward_impl(emoe_cache* c, int32_t T, const uint16_t* h, const uint16_t
     a.pair_out = pair_out;
     a.y = y;
     a.sync = c->sync;
+    a.spin_limit = c->decode_spin_limit;
+    a.tag_xor = c->decode_tag_xor;
   }
   if (a.sync && decode_fused_plan(a)) {
     // Few tokens, every expert resident: the whole layer in one launch.
@@ -1028,6 +1032,16 @@ int32_t emoe_test_set_wave_delay(emoe_cache* c, int32_t microseconds) {
   if (microseconds < 0 || microseconds > 1000)
     return fail(EMOE_EINVAL, "wave delay %d us outside [0, 1000]", microseconds);
   c->wave_delay_us = microseconds;
+  return EMOE_OK;
+}
+
+int32_t emoe_test_set_decode_waits(emoe_cache* c, int32_t spin_limit, int32_t unmatched) {
+  if (!c) return fail(EMOE_EINVAL, "cache is NULL");
+  if (spin_limit < 1 || spin_limit > (1 << 20))
+    return fail(EMOE_EINVAL, "spin limit %d outside [1, 2^20]", spin_limit);
+  if (unmatched != 0 && unmatched != 1) return fail(EMOE_EINVAL, "unmatched must be 0 or 1");
+  c->decode_spin_limit = (uint32_t)spin_limit;
+  c->decode_tag_xor = unmatched ? 0x40000000u : 0u;
   return EMOE_OK;
 }
 

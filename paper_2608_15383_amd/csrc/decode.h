@@ -76,6 +76,11 @@ struct DecodeArgs {
   int down_r, tail_r;             // down row blocks per gate/up and per tail worker
   int gw;                         // down input groups per wavefront (template argument)
   uint32_t epoch;                 // this launch's tag; 0: read it from DecodeSync
+  // Bounded waits (tests force them to give up): polls before a wait gives
+  // up, and a mask xor-ed into the tag the readers wait for (0: the launch's
+  // own; anything else: a tag no writer uses, so every wait gives up).
+  uint32_t spin_limit = 1u << 20;
+  uint32_t tag_xor = 0;
 };
 
 // Host side: the epoch of the last direct launch on one cache.

@@ -120,14 +120,14 @@ __device__ __forceinline__ bool load_logits(DecodeSync* sy, const DecodeArgs& a,
       const int e = lane + 64 * c;
       if (e < E) {
         const uint64_t x = __hip_atomic_load(zt + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        ok = ok && (uint32_t)(x >> 32) == epoch;
+        ok = ok && (uint32_t)(x >> 32) == (epoch ^ a.tag_xor);
         st.v[c] = __uint_as_float((uint32_t)x);
       } else {
         st.v[c] = 0.f;
       }
     }
     if (__all(ok)) return false;
-    if (++it > kSpinLimit) {
+    if (++it > a.spin_limit) {
       if (lane == 0) atomicAdd(&sy->timeouts, 1u);
       return true;
     }
@@ -527,11 +527,11 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
       bool ok = true;
 #pragma unroll
       for (int j = 0; j < kGW; ++j) {
-        ok &= (uint32_t)(x[j] >> 32) == ep;
+        ok &= (uint32_t)(x[j] >> 32) == (ep ^ a.tag_xor);
         xw[j * (kGroup / 2) + lane] = (uint32_t)x[j];
       }
       if (__all(ok)) break;
-      if (++it > kSpinLimit) {
+      if (++it > a.spin_limit) {
         if (lane == 0) atomicAdd(&sy->timeouts, 1u);
         act_late = true;
         break;
@@ -624,9 +624,9 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
                                      __HIP_MEMORY_SCOPE_AGENT);
           bool ok = true;
 #pragma unroll
-          for (int i = 0; i < 8; ++i) ok &= (uint32_t)(x[i] >> 32) == ep;
+          for (int i = 0; i < 8; ++i) ok &= (uint32_t)(x[i] >> 32) == (ep ^ a.tag_xor);
           if (ok) break;
-          if (it > kSpinLimit) {
+          if (it > a.spin_limit) {
             atomicAdd(&sy->timeouts, 1u);
             comb_late = true;
             break;

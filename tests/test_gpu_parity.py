@@ -593,6 +593,29 @@ def test_fused_decode_repeated_calls_and_override():
     assert layer.cache.sync_timeouts() == 0
 
 
+@pytest.mark.parametrize("shape,tokens", [(TINY, 1), (OLMOE, 1), (OLMOE, 4)])
+def test_fused_decode_waits_that_give_up(shape, tokens):
+    """Bounded waits of the fused decode launch, forced from the host to give up
+    (emoe_test_set_decode_waits: the readers wait for a tag no writer uses, 8
+    polls each): every workgroup still exits, every output is NaN and the
+    timeouts are counted.  With the normal waits restored, the next calls equal
+    the per-kernel path bit for bit and count no timeout."""
+    lay = make_layer(shape, tokens, seed=31)
+    layer = Layer(dims_of(shape), lay, tokens)
+    y_ref = layer.forward(lay.h, sequential=True)
+    layer.cache.set_decode_waits(8, unmatched=True)
+    st = api.Stats()
+    y_bad = layer.forward(lay.h, stats=st)
+    assert st.kernel_launches == 1
+    assert np.isnan(y_bad).all()
+    gave_up = layer.cache.sync_timeouts()
+    assert gave_up > 0
+    layer.cache.set_decode_waits()
+    for _ in range(3):
+        assert np.array_equal(layer.forward(lay.h), y_ref)
+    assert layer.cache.sync_timeouts() == gave_up
+
+
 @pytest.mark.parametrize("tokens,path,launches,override",
                          [(1, api.EMOE_PATH_AUTO, 1, False), (2, api.EMOE_PATH_AUTO, 1, False),
                           (3, api.EMOE_PATH_AUTO, 1, True),
