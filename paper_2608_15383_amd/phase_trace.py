@@ -4,12 +4,13 @@
     python -m paper_2608_15383_amd.phase_trace [--tokens 1,4]   # run it on the GPU, print tables
 
 The traced library is the product sources compiled with -DEMOE_PHASE_TRACE into
-_build/trace/: every workgroup of a fused launch stores the wall clock (100 MHz) as it passes
-its phases (decode.hip, EMOE_PHASE).  For each token count the run makes 300 warm-up and 400
-timed layer calls on 16 rotating resident OLMoE-shaped banks (d_model 2048, d_ff 1024, 64
-experts, top-8), then reads the timestamps of the last call and prints, per role and phase,
-min / median / p90 / max in microseconds after the earliest workgroup start.  The trace stores
-themselves cost a little time (the per-call figure is printed beside the tables).
+_build/trace/: every workgroup of a fused launch reads the wall clock (100 MHz) as it passes
+its phases, keeps the readings in LDS and copies them out as it exits (decode.hip,
+EMOE_PHASE).  For each token count the run makes 300 warm-up and 400 timed layer calls on 16
+rotating resident OLMoE-shaped banks (d_model 2048, d_ff 1024, 64 experts, top-8), then reads
+the timestamps of the last call and prints, per role and phase, min / median / p90 / max in
+microseconds after the earliest workgroup start.  The clock reads and the copy-out cost a
+little time (the per-call figure is printed beside the tables).
 """
 from __future__ import annotations
 
