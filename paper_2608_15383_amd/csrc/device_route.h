@@ -19,52 +19,12 @@ __device__ __forceinline__ void bf16x8_to_f64(const uint4 v, double* out) {
   }
 }
 
+// Sum of a double over the wavefront (butterfly of lane exchanges), returned in
+// every lane.
 __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
   return v;
-}
-
-// Logits of NT tokens (t0 .. t0+NT-1, those < tokens) for NE experts (e0 ..)
-// computed by one wavefront: lanes split d in 8-element chunks, products and
-// sums in fp64 (bf16 x bf16 products are exact), one rounding to fp32.
-// The fp64 sums are returned in every lane; wave_router_logits stores them.
-template <int NT, int NE>
-__device__ __forceinline__ void wave_router_sums(int tokens, int n_experts, int d, int t0, int e0,
-                                                 const uint16_t* __restrict__ h,
-                                                 const uint16_t* __restrict__ wr,
-                                                 double (&acc)[NT][NE]) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int a = 0; a < NT; ++a)
-#pragma unroll
-    for (int b = 0; b < NE; ++b) acc[a][b] = 0.0;
-  for (int k0 = 8 * lane; k0 < d; k0 += 512) {
-    double wv[NE][8];
-#pragma unroll
-    for (int b = 0; b < NE; ++b) {
-      if (e0 + b < n_experts) {
-        bf16x8_to_f64(*reinterpret_cast<const uint4*>(wr + (int64_t)(e0 + b) * d + k0), wv[b]);
-      } else {
-#pragma unroll
-        for (int r = 0; r < 8; ++r) wv[b][r] = 0.0;
-      }
-    }
-#pragma unroll
-    for (int a = 0; a < NT; ++a) {
-      if (t0 + a >= tokens) break;
-      double hv[8];
-      bf16x8_to_f64(*reinterpret_cast<const uint4*>(h + (int64_t)(t0 + a) * d + k0), hv);
-#pragma unroll
-      for (int b = 0; b < NE; ++b)
-#pragma unroll
-        for (int r = 0; r < 8; ++r) acc[a][b] = fma(hv[r], wv[b][r], acc[a][b]);
-    }
-  }
-#pragma unroll
-  for (int a = 0; a < NT; ++a)
-#pragma unroll
-    for (int b = 0; b < NE; ++b) acc[a][b] = wave_sum_f64(acc[a][b]);
 }
 
 // Sum of a double over the wavefront with DPP lane moves (quad swaps, the
@@ -146,24 +106,6 @@ __device__ __forceinline__ void wave_router_dot(int t0, int t1, int d, int e,
   const uint16_t* wrow = wr + (int64_t)e * d;
   for (; t0 + 2 <= t1; t0 += 2) wave_router_dot_tokens<2>(t0, d, wrow, h, store);
   if (t0 < t1) wave_router_dot_tokens<1>(t0, d, wrow, h, store);
-}
-
-template <int NT, int NE, bool kCo>
-__device__ __forceinline__ void wave_router_logits(int tokens, int n_experts, int d, int t0, int e0,
-                                                   const uint16_t* __restrict__ h,
-                                                   const uint16_t* __restrict__ wr,
-                                                   float* __restrict__ logits) {
-  double s[NT][NE];
-  wave_router_sums<NT, NE>(tokens, n_experts, d, t0, e0, h, wr, s);
-#pragma unroll
-  for (int a = 0; a < NT; ++a) {
-#pragma unroll
-    for (int b = 0; b < NE; ++b) {
-      const int t = t0 + a, e = e0 + b;
-      if (lane_id() == 0 && t < tokens && e < n_experts)
-        st_u32<kCo>(&logits[(int64_t)t * n_experts + e], __float_as_uint((float)s[a][b]));
-    }
-  }
 }
 
 // Wavefront-wide max / min of a 32-bit unsigned value with DPP lane moves
