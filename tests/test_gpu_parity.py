@@ -593,6 +593,22 @@ def test_fused_decode_repeated_calls_and_override():
     assert layer.cache.sync_timeouts() == 0
 
 
+@pytest.mark.parametrize("shape,tokens", [(OLMOE, 1), (OLMOE, 4), (LayerShape(384, 256, 6, 3), 3),
+                                          (TINY, 16)])
+def test_forward_without_renormalization(shape, tokens):
+    """Mixture weights as the softmax over all E logits (renormalize = 0): every
+    path against the oracle, and the default call (the fused decode launch at up
+    to 4 tokens) bit for bit against the per-kernel path."""
+    lay = make_layer(shape, tokens, seed=37)
+    layer = Layer(dims_of(shape), lay, tokens)
+    ref, _ = oracle_y(lay, LazyExperts(lay), shape.top_k, renormalize=False)
+    for path in (GEMV, MFMA, MIXED, api.EMOE_PATH_AUTO):
+        y = layer.forward(lay.h, path=path, renormalize=False)
+        assert_close(y, ref, f"{shape} T={tokens} path={path} without renormalization")
+    y_seq = layer.forward(lay.h, renormalize=False, sequential=True)
+    assert np.array_equal(layer.forward(lay.h, renormalize=False), y_seq)
+
+
 @pytest.mark.parametrize("shape,tokens", [(TINY, 1), (OLMOE, 1), (OLMOE, 4)])
 def test_fused_decode_waits_that_give_up(shape, tokens):
     """Bounded waits of the fused decode launch, forced from the host to give up
