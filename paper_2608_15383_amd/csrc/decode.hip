@@ -89,6 +89,9 @@ __device__ uint64_t g_phase_trace[kFusedMaxBlocks * 16];
 #define EMOE_TRACE_FLUSH() do {} while (0)
 #endif
 
+// Polls before the epoch advance of captured launches gives up; the
+// hand-over waits take theirs from DecodeArgs::spin_limit (the same 2^20
+// unless a test lowers it).
 constexpr uint32_t kSpinLimit = 1u << 20;
 constexpr int kPollSleep = 1;  // s_sleep units (64 clocks) between polls
 // Between polls of the logits with several tokens: then every wavefront of a
