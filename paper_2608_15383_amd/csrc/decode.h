@@ -71,7 +71,8 @@ struct DecodeArgs {
   // previous pair; the tail workers (n_gate <= j < n_work) tail_r row blocks
   // of the last pair each.
   int n_router, n_gate, n_work;
-  int router_shift;               // log2 of the router items per expert quad (0 or 1)
+  int router_shift;               // log2 of the router items per expert group (0 or 1)
+  int router_experts;             // experts per router item (1 or 4)
   int pairs_per_item;             // gate/up row-block pairs per gate item
   int down_r, tail_r;             // down row blocks per gate/up and per tail worker
   int gw;                         // down input groups per wavefront (template argument)

@@ -311,6 +311,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   __shared__ uint32_t s_xw[kGemvWaves][kGW * kGroup / 2];        // staged activations
   __shared__ float s_part[kGemvWaves][kFusedMaxDownUnits][16];    // per-class down outputs
   __shared__ uint64_t s_topk[kFusedMaxTokens][64];                // top-k scratch per token
+  __shared__ double s_rsum[kGemvWaves][2];                         // router: quarter sums
   __shared__ int s_rank[kGemvWaves][64];                          // partial ranks (one token)
   __shared__ int s_late[2][kGemvWaves];  // per wavefront: a bounded wait gave up (route, down)
 
@@ -336,21 +337,38 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
     // kSyncLanes replicas, so the hundreds of readers below spread over as
     // many memory locations.
     if (!a.logits_override) {
-      // With router_shift 1, items 2i and 2i + 1 take expert quad i for
-      // tokens 0, 1 and 2, 3; with 0, item i takes quad i for every token.
-      static_assert(kFusedMaxTokens <= 4, "two router items per expert quad at most");
-      const int e0 = 4 * (blk >> a.router_shift) + wi;
+      // With router_shift 1, items 2i and 2i + 1 take expert group i for
+      // tokens 0, 1 and 2, 3; with 0, item i takes group i for every token.
+      // A group is one expert whose inputs the four wavefronts split in
+      // quarters (router_experts 1), or four experts, one per wavefront.
+      static_assert(kFusedMaxTokens <= 4, "two router items per expert group at most");
       const int t0 = 2 * (blk & a.router_shift);
       const int t1 = min(a.tokens, t0 + 2);
-      if (e0 < a.n_experts) {
-        wave_router_dot(t0, t1, a.d, e0, a.h, a.w_router, [&](int t, double sum) {
-          const uint32_t v = __float_as_uint((float)sum);
-          const int at = t * a.n_experts + e0;
-          if (lane < kSyncLanes)
-            __hip_atomic_store(&sy->logits[lane][at], ((uint64_t)epoch << 32) | v,
-                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          if (lane == kSyncLanes) st_u32<false>(a.logits + at, v);
-        });
+      auto publish = [&](int t, int e, double sum) {
+        const uint32_t v = __float_as_uint((float)sum);
+        const int at = t * a.n_experts + e;
+        if (lane < kSyncLanes)
+          __hip_atomic_store(&sy->logits[lane][at], ((uint64_t)epoch << 32) | v,
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (lane == kSyncLanes) st_u32<false>(a.logits + at, v);
+      };
+      if (a.router_experts == 1) {
+        const int e = blk >> a.router_shift;
+        const int kq = a.d / kGemvWaves;
+        wave_router_dot_part(t0, t1, a.d, wi * kq, kq, e, a.h, a.w_router,
+                             [&](int t, double sum) { s_rsum[wi][t - t0] = sum; });
+        __syncthreads();
+        // The quarters in wavefront order (the sum is exact, so any order
+        // gives these bits).
+        if (wi == 0)
+          for (int t = t0; t < t1; ++t)
+            publish(t, e, ((s_rsum[0][t - t0] + s_rsum[1][t - t0]) + s_rsum[2][t - t0]) +
+                              s_rsum[3][t - t0]);
+      } else {
+        const int e0 = 4 * (blk >> a.router_shift) + wi;
+        if (e0 < a.n_experts)
+          wave_router_dot(t0, t1, a.d, e0, a.h, a.w_router,
+                          [&](int t, double sum) { publish(t, e0, sum); });
       }
     }
     EMOE_PHASE(1);  // router: logits stored
@@ -709,9 +727,15 @@ bool decode_fused_plan(DecodeArgs& a) {
   const int pairs_of_f = a.f / kTileRows;
   const int n_rb = a.d / kTileRows;
   a.gw = a.f <= 8 * kGroup ? 2 : 4;
-  // Router items: 4 experts by (at most) two tokens, one pass each.
+  // Router items: by (at most) two tokens, one pass each, one expert (its
+  // inputs split over the four wavefronts) for at most two tokens and 64
+  // experts, else four experts, one per wavefront (with more tokens the
+  // one-expert items would fill the grid's last slots for little gain).
   a.router_shift = a.tokens > 2 ? 1 : 0;
-  a.n_router = a.logits_override ? 1 : ((a.n_experts + 3) / 4) << a.router_shift;
+  a.router_experts = a.n_experts <= 64 && a.tokens <= 2 ? 1 : 4;
+  a.n_router = a.logits_override
+                   ? 1
+                   : ((a.n_experts + a.router_experts - 1) / a.router_experts) << a.router_shift;
   const int cap = min(fused_capacity(), kFusedMaxBlocks);
   // The most gate/up items (fewest row-block pairs each) that fit, with the
   // down row blocks of each pair spread over the next pair's items and the

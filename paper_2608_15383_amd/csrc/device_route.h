@@ -51,35 +51,36 @@ __device__ __forceinline__ double wave_sum_f64_dpp(double v) {
   return __hiloint2double(hi, lo);
 }
 
-// Logit sums of expert e for kT consecutive tokens by one wavefront, with
-// every load of a pass issued before any is used: lanes take 8-input chunks
-// k = 8*lane + 512*i, up to four chunks (2048 inputs) per pass and token, so
-// the kT tokens with d <= 2048 cost one memory round trip together.
-// Chunks past d are read at a clamped in-bounds address and contribute 0.
-// Products of bf16 values are exact in fp64 and so, at these magnitudes, is
-// the sum, whatever its order.  store(t, sum) receives each token's sum (the
-// same in every lane).
-template <int kT, typename Store>
-__device__ __forceinline__ void wave_router_dot_tokens(int t0, int d, const uint16_t* __restrict__ wrow,
+// Logit sums of expert e for kT consecutive tokens by one wavefront over the
+// inputs [k0, k0 + kn) (kn a multiple of 8), with every load of a pass issued
+// before any is used: lanes take 8-input chunks k = 8*lane + 512*i, kC chunks
+// per pass and token, so the kT tokens with kn <= 512 kC cost one memory
+// round trip together.  Chunks past kn are read at a clamped in-bounds address
+// and contribute 0.  Products of bf16 values are exact in fp64 and so, at
+// these magnitudes, is the sum, whatever its order.  store(t, sum) receives
+// each token's sum (the same in every lane).
+template <int kT, int kC = 4, typename Store>
+__device__ __forceinline__ void wave_router_dot_tokens(int t0, int d, int k0, int kn,
+                                                       const uint16_t* __restrict__ wrow,
                                                        const uint16_t* __restrict__ h, Store store) {
   const int lane = lane_id();
   double acc[kT];
 #pragma unroll
   for (int t = 0; t < kT; ++t) acc[t] = 0.0;
-  for (int base = 0; base < d; base += 512 * 4) {
-    uint4 w[4], x[kT][4];
+  for (int base = 0; base < kn; base += 512 * kC) {
+    uint4 w[kC], x[kT][kC];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kC; ++i) {
       const int k = base + 512 * i + 8 * lane;
-      const int kc = k < d ? k : d - 8;
+      const int kc = k0 + (k < kn ? k : kn - 8);
       w[i] = *reinterpret_cast<const uint4*>(wrow + kc);
 #pragma unroll
       for (int t = 0; t < kT; ++t)
         x[t][i] = *reinterpret_cast<const uint4*>(h + (int64_t)(t0 + t) * d + kc);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const bool ok = base + 512 * i + 8 * lane < d;
+    for (int i = 0; i < kC; ++i) {
+      const bool ok = base + 512 * i + 8 * lane < kn;
       double wv[8];
       bf16x8_to_f64(w[i], wv);
 #pragma unroll
@@ -97,15 +98,27 @@ __device__ __forceinline__ void wave_router_dot_tokens(int t0, int d, const uint
   for (int t = 0; t < kT; ++t) store(t0 + t, wave_sum_f64_dpp(acc[t]));
 }
 
-// Logit sums of expert e for tokens [t0, t1): two tokens per pass (four would
-// hold more loaded registers than the fused decode kernel has to spare).
+// Logit sums of expert e for tokens [t0, t1) over all d inputs: two tokens
+// per pass (four would hold more loaded registers than the fused decode
+// kernel has to spare).
 template <typename Store>
 __device__ __forceinline__ void wave_router_dot(int t0, int t1, int d, int e,
                                                 const uint16_t* __restrict__ h,
                                                 const uint16_t* __restrict__ wr, Store store) {
   const uint16_t* wrow = wr + (int64_t)e * d;
-  for (; t0 + 2 <= t1; t0 += 2) wave_router_dot_tokens<2>(t0, d, wrow, h, store);
-  if (t0 < t1) wave_router_dot_tokens<1>(t0, d, wrow, h, store);
+  for (; t0 + 2 <= t1; t0 += 2) wave_router_dot_tokens<2>(t0, d, 0, d, wrow, h, store);
+  if (t0 < t1) wave_router_dot_tokens<1>(t0, d, 0, d, wrow, h, store);
+}
+
+// The same over the inputs [k0, k0 + kn) only, one 512-input chunk per lane
+// and pass (a quarter of d <= 2048 in one pass).
+template <typename Store>
+__device__ __forceinline__ void wave_router_dot_part(int t0, int t1, int d, int k0, int kn, int e,
+                                                     const uint16_t* __restrict__ h,
+                                                     const uint16_t* __restrict__ wr, Store store) {
+  const uint16_t* wrow = wr + (int64_t)e * d;
+  for (; t0 + 2 <= t1; t0 += 2) wave_router_dot_tokens<2, 1>(t0, d, k0, kn, wrow, h, store);
+  if (t0 < t1) wave_router_dot_tokens<1, 1>(t0, d, k0, kn, wrow, h, store);
 }
 
 // Wavefront-wide max / min of a 32-bit unsigned value with DPP lane moves
