@@ -6,23 +6,28 @@
 // memory about 1 us under load, against roughly 5 us to stream the decode
 // layer's 26 MB of packed weights.  The six-kernel sequence is therefore
 // replaced by one grid whose workgroups play these roles by index:
-//   [0, nR)        router items: logits of 4 experts for one or two
-//                  tokens (a pair of tokens per router wavefront and pass,
-//                  so with more than two tokens the items split them);
+//   [0, nR)        router items: logits of one expert (its inputs split
+//                  over the four wavefronts) or of four experts, for one or
+//                  two tokens (with more than two tokens the items split
+//                  them);
 //   [nR, nR+nG)    gate/up workers: worker j runs gate/up item j (pair
 //                  p = j / chunks, some of its row-block pairs; pairs in
 //                  token-major order), then down_r output row blocks of pair
-//                  p - 1;
-//   [nR+nG, ...)   tail workers: tail_r output row blocks of the last pair.
+//                  p - down_lag;
+//   [nR+nG, ...)   tail workers: tail_r output row blocks of one of the
+//                  last down_lag pairs.
 // Every worker waits for the router items, reads the logits and runs the
 // top-k itself (cheap, and it saves the round trips of publishing the
 // selection); gate/up workers stage the token rows in LDS while they wait.
 // Each worker loads the first down tiles of its pair while the gate/up items
 // stream theirs, picks up that pair's activation row once it is complete and
-// splits each row block's input groups over its four wavefronts.  So every
-// pair's down projection starts as soon as its own activation row is done,
-// spread over as many workgroups as gate/up items, and a pair's activations
-// come from workers of lower index than the ones that read them.  The
+// splits each row block's input groups over its four wavefronts.  Items
+// finish roughly in dispatch order, so with a lag of two pairs a gate/up
+// worker that finishes its item finds its down pair's row already complete,
+// and the rows that complete last go to the tail workers, idle since their
+// top-k.  Every pair's down projection is spread over as many workgroups as
+// gate/up items, and a pair's activations come from workers of lower index
+// than the ones that read them.  The
 // workers holding the last pair of a token then read the token's other k - 1
 // expert outputs (also from workers of lower index) and add the k outputs in
 // rank order.  The first tail worker finally writes the routing and grouping
@@ -328,7 +333,7 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   if (blk == 0) {  // the layout, for reading the trace
     EMOE_TRACE_SET(14, (uint64_t)a.n_router | (uint64_t)a.n_gate << 16 | (uint64_t)a.n_work << 32);
     EMOE_TRACE_SET(15, (uint64_t)a.pairs_per_item | (uint64_t)a.down_r << 16 |
-                           (uint64_t)a.tail_r << 32);
+                           (uint64_t)a.tail_r << 32 | (uint64_t)a.down_lag << 48);
   }
 
   if (blk < a.n_router) {
@@ -381,15 +386,31 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   }
 
   // Worker wk runs gate/up item wk (pair p = wk / chunks, chunk wk % chunks)
-  // and then the down row blocks [rb0, rb0 + nu) of pair q = p - 1; a tail
-  // worker (wk >= n_gate) only the down row blocks of the last pair.  The
-  // workers that hold the last pair of a token combine that token's outputs.
+  // and then the down row blocks [rb0, rb0 + nu) of pair q = p - down_lag,
+  // whose activation row is complete by the time this later-dispatched item
+  // is; the tail workers (wk >= n_gate), idle since their top-k, take the
+  // down row blocks of the last down_lag pairs, whose rows complete last.
+  // Every wait is for lower-indexed workgroups.  The workers that hold the
+  // last pair of a token combine that token's outputs.
   const int wk = blk - a.n_router;
   const bool is_gate = wk < a.n_gate;
   const int n_rb = a.d / kTileRows;
   const int chunks = (a.f / kTileRows + a.pairs_per_item - 1) / a.pairs_per_item;
-  const int q = is_gate ? wk / chunks - 1 : P - 1;
-  const int rb0 = is_gate ? (wk % chunks) * a.down_r : (wk - a.n_gate) * a.tail_r;
+  int q, rb0;
+  if (is_gate) {
+    q = wk / chunks - a.down_lag;
+    rb0 = (wk % chunks) * a.down_r;
+  } else {
+    // Tail worker j: pair P - down_lag + j / per_pair, row-block set j % per_pair.
+    const int per_pair = (n_rb + a.tail_r - 1) / a.tail_r;
+    int j = wk - a.n_gate;
+    q = P - a.down_lag;
+    while (j >= per_pair) {
+      j -= per_pair;
+      ++q;
+    }
+    rb0 = j * a.tail_r;
+  }
   const int nu = q < 0 ? 0 : max(0, min(is_gate ? a.down_r : a.tail_r, n_rb - rb0));
   const bool is_comb = nu > 0 && q % a.top_k == a.top_k - 1;  // combines token q / k
   const bool writes_routing = wk == a.n_gate;                  // the first tail worker
@@ -737,23 +758,31 @@ bool decode_fused_plan(DecodeArgs& a) {
                    ? 1
                    : ((a.n_experts + a.router_experts - 1) / a.router_experts) << a.router_shift;
   const int cap = min(fused_capacity(), kFusedMaxBlocks);
+  // The down projection of pair p runs in the items of pair p + lag, and the
+  // last lag pairs' in the tail workers.
+  const int lag = min(P, kFusedDownLag);
   // The most gate/up items (fewest row-block pairs each) that fit, with the
-  // down row blocks of each pair spread over the next pair's items and the
-  // last pair's over as many tail workers as the remaining room allows.
+  // down row blocks of each pair spread over the items of pair p + lag and
+  // the last lag pairs' over as many tail workers as the remaining room
+  // allows.
   for (int ppi = 1; ppi <= pairs_of_f; ppi *= 2) {
     const int chunks = (pairs_of_f + ppi - 1) / ppi;
     const int down_r = (n_rb + chunks - 1) / chunks;
     if (down_r > kFusedMaxDownUnits) break;  // fewer items only raise it
     const int n_gate = P * chunks;
-    const int room = min(cap - a.n_router - n_gate, n_rb);
-    if (room < 1) continue;
-    const int tail_r = (n_rb + room - 1) / room;
+    const int room = min(cap - a.n_router - n_gate, lag * n_rb);
+    if (room < lag) continue;
+    // Row blocks per tail worker: the fewest for which lag pairs' worth of
+    // workers fit the room.
+    int tail_r = (lag * n_rb + room - 1) / room;
+    while (tail_r <= kFusedMaxDownUnits && lag * ((n_rb + tail_r - 1) / tail_r) > room) ++tail_r;
     if (tail_r > kFusedMaxDownUnits) continue;
     a.pairs_per_item = ppi;
     a.n_gate = n_gate;
     a.down_r = down_r;
     a.tail_r = tail_r;
-    a.n_work = n_gate + (n_rb + tail_r - 1) / tail_r;
+    a.down_lag = lag;
+    a.n_work = n_gate + lag * ((n_rb + tail_r - 1) / tail_r);
     return true;
   }
   return false;

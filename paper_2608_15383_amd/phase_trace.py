@@ -82,6 +82,7 @@ def trace(tokens: int, banks: int = 16):
     w0, w1 = int(tr[0, 14]), int(tr[0, 15])
     n_router, n_gate, n_work = w0 & 0xffff, (w0 >> 16) & 0xffff, (w0 >> 32) & 0xffff
     ppi, down_r, tail_r = w1 & 0xffff, (w1 >> 16) & 0xffff, (w1 >> 32) & 0xffff
+    lag = (w1 >> 48) & 0xffff
     n = n_router + n_work
     tr = tr[:n]
     base = tr[:, 0].min()
@@ -89,14 +90,16 @@ def trace(tokens: int, banks: int = 16):
     j = np.arange(n) - n_router
     gate = (j >= 0) & (j < n_gate)
     tail = j >= n_gate
-    pair = np.where(gate, j // max(chunks, 1), -1)
     k = 8
-    down_gate = gate & (pair >= 1)
-    comb = (down_gate & ((pair - 1) % k == k - 1)) | tail
+    per_pair = -(-(2048 // 16) // tail_r)
+    # The pair whose down row blocks a worker computes.
+    down_pair = np.where(gate, j // max(chunks, 1) - lag, tokens * k - lag + (j - n_gate) // per_pair)
+    down_gate = gate & (down_pair >= 0)
+    comb = (down_gate | tail) & (down_pair % k == k - 1)
     print(f"T={tokens}: {per_call:.2f} us per layer call (traced build); grid {n} workgroups: "
           f"{n_router} router, {n_gate} gate/up workers ({ppi} row-block pair(s) each, then "
-          f"{down_r} down row block(s) of the previous pair), {n_work - n_gate} tail workers "
-          f"({tail_r} row block(s) of the last pair)")
+          f"{down_r} down row block(s) of the pair {lag} before), {n_work - n_gate} tail workers "
+          f"({tail_r} row block(s) each of the last {lag} pair(s))")
     R = tr[:n_router]
     print(" router workgroups")
     _stat("start", R[:, 0], base)
