@@ -15,6 +15,7 @@ constexpr int kFusedMaxBlocks = 1024;  // workgroups per fused launch
 constexpr int kFusedMaxD = 4096;       // d_model of a fused launch (DecodeSync::out)
 constexpr int kFusedMaxDownUnits = 8;  // down row blocks per worker
 constexpr int kFusedDownLag = 2;       // pairs between a gate/up item's pair and its down pair
+constexpr int kFusedTailPairs = 3;     // ... and last pairs whose down the tail workers take (one-pair items)
 constexpr uint32_t kDeviceEpoch0 = 0x80000000u;  // first epoch of captured launches
 
 // Data the workgroups of one fused launch hand to each other, in device
@@ -69,14 +70,16 @@ struct DecodeArgs {
   // Filled by decode_fused_plan / launch_decode_fused.  Workgroup
   // n_router + j (worker j) runs gate/up item j (j < n_gate: pair j / chunks,
   // with chunks items per pair) and then down_r output row blocks of pair
-  // j / chunks - down_lag; the tail workers (n_gate <= j < n_work) take the
-  // last down_lag pairs, tail_r row blocks each, pair by pair.
+  // j / chunks - down_lag (none past pair P - tail_pairs - 1); the tail
+  // workers (n_gate <= j < n_work) take the last tail_pairs pairs, tail_r row
+  // blocks each, pair by pair.
   int n_router, n_gate, n_work;
   int router_shift;               // log2 of the router items per expert group (0 or 1)
   int router_experts;             // experts per router item (1 or 4)
   int pairs_per_item;             // gate/up row-block pairs per gate item
   int down_r, tail_r;             // down row blocks per gate/up and per tail worker
   int down_lag;                   // pairs between a gate/up item's pair and its down pair
+  int tail_pairs;                 // last pairs whose down row blocks the tail workers take
   int gw;                         // down input groups per wavefront (template argument)
   uint32_t epoch;                 // this launch's tag; 0: read it from DecodeSync
   // Bounded waits (tests force them to give up): polls before a wait gives

@@ -15,7 +15,8 @@
 //                  token-major order), then down_r output row blocks of pair
 //                  p - down_lag;
 //   [nR+nG, ...)   tail workers: tail_r output row blocks of one of the
-//                  last down_lag pairs.
+//                  last tail_pairs pairs (the gate/up workers of the last
+//                  tail_pairs - down_lag pairs have no down work).
 // Every worker waits for the router items, reads the logits and runs the
 // top-k itself (cheap, and it saves the round trips of publishing the
 // selection); gate/up workers stage the token rows in LDS while they wait.
@@ -333,7 +334,8 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   if (blk == 0) {  // the layout, for reading the trace
     EMOE_TRACE_SET(14, (uint64_t)a.n_router | (uint64_t)a.n_gate << 16 | (uint64_t)a.n_work << 32);
     EMOE_TRACE_SET(15, (uint64_t)a.pairs_per_item | (uint64_t)a.down_r << 16 |
-                           (uint64_t)a.tail_r << 32 | (uint64_t)a.down_lag << 48);
+                           (uint64_t)a.tail_r << 32 | (uint64_t)a.down_lag << 48 |
+                           (uint64_t)a.tail_pairs << 56);
   }
 
   if (blk < a.n_router) {
@@ -389,9 +391,11 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   // and then the down row blocks [rb0, rb0 + nu) of pair q = p - down_lag,
   // whose activation row is complete by the time this later-dispatched item
   // is; the tail workers (wk >= n_gate), idle since their top-k, take the
-  // down row blocks of the last down_lag pairs, whose rows complete last.
-  // Every wait is for lower-indexed workgroups.  The workers that hold the
-  // last pair of a token combine that token's outputs.
+  // down row blocks of the last tail_pairs pairs (>= down_lag), whose rows
+  // complete last, so the items of the last tail_pairs - down_lag pairs,
+  // which finish last, have no down work.  Every wait is for lower-indexed
+  // workgroups.  The workers that hold the last pair of a token combine that
+  // token's outputs.
   const int wk = blk - a.n_router;
   const bool is_gate = wk < a.n_gate;
   const int n_rb = a.d / kTileRows;
@@ -399,12 +403,13 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   int q, rb0;
   if (is_gate) {
     q = wk / chunks - a.down_lag;
+    if (q >= P - a.tail_pairs) q = -1;  // the tail workers' pairs
     rb0 = (wk % chunks) * a.down_r;
   } else {
-    // Tail worker j: pair P - down_lag + j / per_pair, row-block set j % per_pair.
+    // Tail worker j: pair P - tail_pairs + j / per_pair, row-block set j % per_pair.
     const int per_pair = (n_rb + a.tail_r - 1) / a.tail_r;
     int j = wk - a.n_gate;
-    q = P - a.down_lag;
+    q = P - a.tail_pairs;
     while (j >= per_pair) {
       j -= per_pair;
       ++q;
@@ -758,31 +763,33 @@ bool decode_fused_plan(DecodeArgs& a) {
                    ? 1
                    : ((a.n_experts + a.router_experts - 1) / a.router_experts) << a.router_shift;
   const int cap = min(fused_capacity(), kFusedMaxBlocks);
-  // The down projection of pair p runs in the items of pair p + lag, and the
-  // last lag pairs' in the tail workers.
-  const int lag = min(P, kFusedDownLag);
   // The most gate/up items (fewest row-block pairs each) that fit, with the
   // down row blocks of each pair spread over the items of pair p + lag and
-  // the last lag pairs' over as many tail workers as the remaining room
+  // the last tail pairs' over as many tail workers as the remaining room
   // allows.
   for (int ppi = 1; ppi <= pairs_of_f; ppi *= 2) {
+    // Items of one row-block pair finish with little slack, so there the
+    // last pair's items get no down work (one more tail pair than the lag).
+    const int tail = min(P, ppi == 1 ? kFusedTailPairs : kFusedDownLag);
+    const int lag = min(tail, kFusedDownLag);
     const int chunks = (pairs_of_f + ppi - 1) / ppi;
     const int down_r = (n_rb + chunks - 1) / chunks;
     if (down_r > kFusedMaxDownUnits) break;  // fewer items only raise it
     const int n_gate = P * chunks;
-    const int room = min(cap - a.n_router - n_gate, lag * n_rb);
-    if (room < lag) continue;
-    // Row blocks per tail worker: the fewest for which lag pairs' worth of
-    // workers fit the room.
-    int tail_r = (lag * n_rb + room - 1) / room;
-    while (tail_r <= kFusedMaxDownUnits && lag * ((n_rb + tail_r - 1) / tail_r) > room) ++tail_r;
+    const int room = min(cap - a.n_router - n_gate, tail * n_rb);
+    if (room < tail) continue;
+    // Row blocks per tail worker: the fewest for which the tail pairs' worth
+    // of workers fit the room.
+    int tail_r = (tail * n_rb + room - 1) / room;
+    while (tail_r <= kFusedMaxDownUnits && tail * ((n_rb + tail_r - 1) / tail_r) > room) ++tail_r;
     if (tail_r > kFusedMaxDownUnits) continue;
     a.pairs_per_item = ppi;
     a.n_gate = n_gate;
     a.down_r = down_r;
     a.tail_r = tail_r;
     a.down_lag = lag;
-    a.n_work = n_gate + lag * ((n_rb + tail_r - 1) / tail_r);
+    a.tail_pairs = tail;
+    a.n_work = n_gate + tail * ((n_rb + tail_r - 1) / tail_r);
     return true;
   }
   return false;

@@ -82,7 +82,7 @@ def trace(tokens: int, banks: int = 16):
     w0, w1 = int(tr[0, 14]), int(tr[0, 15])
     n_router, n_gate, n_work = w0 & 0xffff, (w0 >> 16) & 0xffff, (w0 >> 32) & 0xffff
     ppi, down_r, tail_r = w1 & 0xffff, (w1 >> 16) & 0xffff, (w1 >> 32) & 0xffff
-    lag = (w1 >> 48) & 0xffff
+    lag, tail_pairs = (w1 >> 48) & 0xff, (w1 >> 56) & 0xff
     n = n_router + n_work
     tr = tr[:n]
     base = tr[:, 0].min()
@@ -93,13 +93,17 @@ def trace(tokens: int, banks: int = 16):
     k = 8
     per_pair = -(-(2048 // 16) // tail_r)
     # The pair whose down row blocks a worker computes.
-    down_pair = np.where(gate, j // max(chunks, 1) - lag, tokens * k - lag + (j - n_gate) // per_pair)
+    P = tokens * k
+    gate_pair = j // max(chunks, 1) - lag
+    down_pair = np.where(gate, np.where(gate_pair < P - tail_pairs, gate_pair, -1),
+                         P - tail_pairs + (j - n_gate) // per_pair)
     down_gate = gate & (down_pair >= 0)
     comb = (down_gate | tail) & (down_pair % k == k - 1)
     print(f"T={tokens}: {per_call:.2f} us per layer call (traced build); grid {n} workgroups: "
           f"{n_router} router, {n_gate} gate/up workers ({ppi} row-block pair(s) each, then "
-          f"{down_r} down row block(s) of the pair {lag} before), {n_work - n_gate} tail workers "
-          f"({tail_r} row block(s) each of the last {lag} pair(s))")
+          f"{down_r} down row block(s) of the pair {lag} before, none in the last "
+          f"{tail_pairs - lag} pair(s)), {n_work - n_gate} tail workers ({tail_r} row block(s) "
+          f"each of the last {tail_pairs} pair(s))")
     R = tr[:n_router]
     print(" router workgroups")
     _stat("start", R[:, 0], base)
