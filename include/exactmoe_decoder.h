@@ -71,7 +71,9 @@ size_t emoe_decoder_workspace_bytes(const emoe_decoder_dims* dims, int32_t max_t
 /* Create a decoder over caller-owned weights, one slot cache per layer
  * (host array of n_layers emoe_cache*, each created with dims->moe and a slot
  * bank) and a KV cache (device, emoe_decoder_kv_bytes).  Creates a rocBLAS
- * handle for the dense projections.  EMOE_ESHAPE for unsupported sizes. */
+ * handle for the dense projections of prompts (more than 4 tokens; decode
+ * steps use the library's own GEMV kernel).  EMOE_ESHAPE for unsupported
+ * sizes. */
 int32_t emoe_decoder_create(const emoe_decoder_dims* dims, const emoe_decoder_weights* weights,
                             emoe_cache* const* caches, void* kv_cache, emoe_decoder** out);
 int32_t emoe_decoder_destroy(emoe_decoder* dec);

@@ -1,8 +1,9 @@
 // Synthetic decoder around the routed-expert layer (exactmoe_decoder.h):
 // embedding gather, residual add + RMSNorm, rotary positions with the KV
 // cache append, causal attention and the greedy argmax as gfx950 kernels; the
-// dense bf16 projections (QKV, output, LM head) through rocBLAS; the routed
-// experts through emoe_moe_forward.
+// dense bf16 projections (QKV, output, LM head) as weight-streaming GEMV
+// kernels for up to four tokens (decode steps) and through rocBLAS for more
+// (prompts); the routed experts through emoe_moe_forward.
 #include <rocblas/rocblas.h>
 
 #include <cmath>
@@ -22,6 +23,83 @@ constexpr int kMaxHeadDim = 256;
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------- kernels
+// Y[t][n] = sum_k X[t][k] W[n][k] (+ C[t][n]) for kT <= 4 tokens: a
+// weight-streaming GEMV.  Each wavefront owns kR rows of W; lane l reads the
+// 16-byte chunks k = 8l + 512u of every row (and of the token rows), all
+// loads of a 2048-input row block issued before any product, and the fp32
+// dot products (bf16 pairs) are summed over the lanes by butterfly.  Output
+// bf16 (rounded to nearest even after adding C) or fp32.
+constexpr int kDenseMaxTokens = 4;
+constexpr int kDenseUnroll = 4;  // 512-input chunks per lane in flight
+
+__device__ __forceinline__ float dot8_bf16(uint4 a, uint4 b, float c) {
+  c = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.x),
+                                      __builtin_bit_cast(bf16x2_t, b.x), c, false);
+  c = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.y),
+                                      __builtin_bit_cast(bf16x2_t, b.y), c, false);
+  c = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.z),
+                                      __builtin_bit_cast(bf16x2_t, b.z), c, false);
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a.w),
+                                         __builtin_bit_cast(bf16x2_t, b.w), c, false);
+}
+
+template <int kR, int kT>
+__global__ __launch_bounds__(kThreads) void dense_gemv_kernel(int N, int K, const uint16_t* X,
+                                                              const uint16_t* W, const uint16_t* C,
+                                                              void* Y, int out_f32) {
+  const int lane = threadIdx.x & 63;
+  const int n0 = (blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) * kR;
+  if (n0 >= N) return;
+  float acc[kR][kT];
+#pragma unroll
+  for (int r = 0; r < kR; ++r)
+#pragma unroll
+    for (int t = 0; t < kT; ++t) acc[r][t] = 0.f;
+  for (int k0 = 8 * lane; k0 < K; k0 += 512 * kDenseUnroll) {
+    uint4 w[kDenseUnroll][kR], x[kDenseUnroll][kT];
+#pragma unroll
+    for (int u = 0; u < kDenseUnroll; ++u) {
+      const int k = k0 + 512 * u;
+      if (k < K) {
+#pragma unroll
+        for (int r = 0; r < kR; ++r) {
+          const int n = min(n0 + r, N - 1);  // rows past N repeat the last (not stored)
+          w[u][r] = *reinterpret_cast<const uint4*>(W + (int64_t)n * K + k);
+        }
+#pragma unroll
+        for (int t = 0; t < kT; ++t) x[u][t] = *reinterpret_cast<const uint4*>(X + (int64_t)t * K + k);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kDenseUnroll; ++u) {
+      if (k0 + 512 * u < K) {
+#pragma unroll
+        for (int r = 0; r < kR; ++r)
+#pragma unroll
+          for (int t = 0; t < kT; ++t) acc[r][t] = dot8_bf16(w[u][r], x[u][t], acc[r][t]);
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kR; ++r)
+#pragma unroll
+    for (int t = 0; t < kT; ++t) {
+      float v = acc[r][t];
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+      const int n = n0 + r;
+      if (lane == 0 && n < N) {
+        const int64_t at = (int64_t)t * N + n;
+        if (out_f32) {
+          static_cast<float*>(Y)[at] = v;
+        } else {
+          if (C) v += __uint_as_float((uint32_t)C[at] << 16);
+          static_cast<uint16_t*>(Y)[at] = (uint16_t)f32_to_bf16_rne(v);
+        }
+      }
+    }
+}
+
 // x[t] = embed[clamp(tokens[t])], one workgroup per token, 16-byte copies.
 __global__ __launch_bounds__(kThreads) void embed_kernel(int V, int d, const int32_t* tokens,
                                                          const uint16_t* embed, uint16_t* x) {
@@ -349,7 +427,34 @@ namespace {
 // out_f32 selects an fp32 output (C unused); otherwise bf16 out with
 // Y = X W^T + C when C is given.
 int32_t dense(emoe_decoder* dec, int T, int N, int K, const uint16_t* X, const uint16_t* W,
-              const uint16_t* C, void* Y, bool out_f32) {
+              const uint16_t* C, void* Y, bool out_f32, hipStream_t stream) {
+  if (T <= kDenseMaxTokens && K % 8 == 0) {
+    // Decode steps: the weight-streaming GEMV, two rows per wavefront when
+    // that still gives every CU a workgroup or two, else one.
+    const int per_wg_2 = 2 * (kThreads / 64);
+    const bool two = (N + per_wg_2 - 1) / per_wg_2 >= 256;
+    const int per_wg = two ? per_wg_2 : kThreads / 64;
+    const dim3 grid((N + per_wg - 1) / per_wg);
+    const uint16_t* c = out_f32 ? nullptr : C;
+    const int f32 = out_f32 ? 1 : 0;
+#define DENSE_CASE(R, TT)                                                                        \
+  hipLaunchKernelGGL((dense_gemv_kernel<R, TT>), grid, dim3(kThreads), 0, stream, N, K, X, W, c, Y, \
+                     f32)
+    switch ((two ? 8 : 0) + T) {
+      case 1: DENSE_CASE(1, 1); break;
+      case 2: DENSE_CASE(1, 2); break;
+      case 3: DENSE_CASE(1, 3); break;
+      case 4: DENSE_CASE(1, 4); break;
+      case 9: DENSE_CASE(2, 1); break;
+      case 10: DENSE_CASE(2, 2); break;
+      case 11: DENSE_CASE(2, 3); break;
+      default: DENSE_CASE(2, 4); break;
+    }
+#undef DENSE_CASE
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return report_error(EMOE_EHIP, "dense_gemv_kernel launch: %s", hipGetErrorString(e));
+    return EMOE_OK;
+  }
   const float alpha = 1.0f, beta = (C && !out_f32) ? 1.0f : 0.0f;
   const rocblas_datatype io = out_f32 ? rocblas_datatype_f32_r : rocblas_datatype_bf16_r;
   const void* c = (C && !out_f32) ? static_cast<const void*>(C) : static_cast<const void*>(Y);
@@ -463,7 +568,7 @@ int32_t emoe_decoder_forward(emoe_decoder* dec, const int32_t* tokens, int32_t T
     uint16_t* vc = kc + (size_t)D.max_positions * d;
     DEC_LAUNCH(add_rmsnorm_kernel, dim3(T), dim3(kThreads), 0, stream, d, xa, delta,
                dec->attn_norm[l], D.rms_eps, n);
-    if ((st = dense(dec, T, 3 * d, d, n, dec->wqkv[l], nullptr, qkv, false))) return st;
+    if ((st = dense(dec, T, 3 * d, d, n, dec->wqkv[l], nullptr, qkv, false, stream))) return st;
     DEC_LAUNCH(rope_kv_kernel, dim3(T), dim3(kThreads), 0, stream, H, Dh, pos0, D.rope_base, qkv,
                kc, vc);
     if (Dh == 64)
@@ -475,7 +580,7 @@ int32_t emoe_decoder_forward(emoe_decoder* dec, const int32_t* tokens, int32_t T
     else
       DEC_LAUNCH(attention_kernel<256>, dim3(H, T), dim3(kThreads), 0, stream, H, pos0, qkv, kc,
                  vc, attn);
-    if ((st = dense(dec, T, d, d, attn, dec->wo[l], xa, xb, false))) return st;  // x += attn Wo^T
+    if ((st = dense(dec, T, d, d, attn, dec->wo[l], xa, xb, false, stream))) return st;  // x += attn Wo^T
     std::swap(xa, xb);
     DEC_LAUNCH(add_rmsnorm_kernel, dim3(T), dim3(kThreads), 0, stream, d, xa, nullptr,
                dec->moe_norm[l], D.rms_eps, n);
@@ -486,7 +591,8 @@ int32_t emoe_decoder_forward(emoe_decoder* dec, const int32_t* tokens, int32_t T
   }
   DEC_LAUNCH(add_rmsnorm_kernel, dim3(T), dim3(kThreads), 0, stream, d, xa, delta, dec->final_norm,
              D.rms_eps, n);
-  if ((st = dense(dec, 1, D.vocab, d, n + (size_t)(T - 1) * d, dec->lm_head, nullptr, logits, true)))
+  if ((st = dense(dec, 1, D.vocab, d, n + (size_t)(T - 1) * d, dec->lm_head, nullptr, logits, true,
+                  stream)))
     return st;
   DEC_LAUNCH(argmax_kernel, dim3(1), dim3(1024), 0, stream, D.vocab, logits, next_token);
   return EMOE_OK;
