@@ -235,7 +235,7 @@ __global__ __launch_bounds__(kThreads) void rope_kv_kernel(int H, int Dh, int po
 // fp32), softmax in fp32, output bf16.  One workgroup per (head, token).
 // Scores: a thread per key, the key row's 16-byte chunks all loaded before
 // use.  Output: a thread per (8-dimension chunk, key stripe), 16-byte value
-// loads, the stripes' partial sums added in stripe order.
+// loads eight keys at a time, the stripes' partial sums added in stripe order.
 template <int kDh>
 __global__ __launch_bounds__(kThreads) void attention_kernel(int H, int pos0, const uint16_t* qkv,
                                                              const uint16_t* k_cache,
@@ -286,30 +286,28 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(int H, int pos0, co
   const int chunk = threadIdx.x % kChunks, stripe = threadIdx.x / kChunks;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   const uint16_t* vcol = v_cache + h * kDh + chunk * 8;
-  int j = stripe;
-  for (; j + kStripes < n; j += 2 * kStripes) {  // two keys' loads in flight
-    const uint4 a = *reinterpret_cast<const uint4*>(vcol + (int64_t)j * d);
-    const uint4 b = *reinterpret_cast<const uint4*>(vcol + (int64_t)(j + kStripes) * d);
-    const float pa = score[j], pb = score[j + kStripes];
-    const uint32_t aw[4] = {a.x, a.y, a.z, a.w}, bw[4] = {b.x, b.y, b.z, b.w};
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      acc[2 * p] = fmaf(pa, bf16_to_f32(aw[p] & 0xffffu), acc[2 * p]);
-      acc[2 * p + 1] = fmaf(pa, bf16_to_f32(aw[p] >> 16), acc[2 * p + 1]);
-      acc[2 * p] = fmaf(pb, bf16_to_f32(bw[p] & 0xffffu), acc[2 * p]);
-      acc[2 * p + 1] = fmaf(pb, bf16_to_f32(bw[p] >> 16), acc[2 * p + 1]);
-    }
-  }
-  if (j < n) {
-    const uint4 a = *reinterpret_cast<const uint4*>(vcol + (int64_t)j * d);
-    const float pa = score[j];
+  // Eight keys' value loads in flight per stripe (a decode step's few
+  // hundred keys take two rounds), then the rest one at a time.
+  auto add_key = [&](const uint4 a, float pa) {
     const uint32_t aw[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
       acc[2 * p] = fmaf(pa, bf16_to_f32(aw[p] & 0xffffu), acc[2 * p]);
       acc[2 * p + 1] = fmaf(pa, bf16_to_f32(aw[p] >> 16), acc[2 * p + 1]);
     }
+  };
+  constexpr int kVKeys = 8;
+  int j = stripe;
+  for (; j + (kVKeys - 1) * kStripes < n; j += kVKeys * kStripes) {
+    uint4 a[kVKeys];
+#pragma unroll
+    for (int u = 0; u < kVKeys; ++u)
+      a[u] = *reinterpret_cast<const uint4*>(vcol + (int64_t)(j + u * kStripes) * d);
+#pragma unroll
+    for (int u = 0; u < kVKeys; ++u) add_key(a[u], score[j + u * kStripes]);
   }
+  for (; j < n; j += kStripes)
+    add_key(*reinterpret_cast<const uint4*>(vcol + (int64_t)j * d), score[j]);
 #pragma unroll
   for (int e = 0; e < 8; ++e) part[stripe][chunk * 8 + e] = acc[e];
   __syncthreads();
