@@ -339,6 +339,21 @@ int32_t emoe_test_set_wave_delay(emoe_cache* cache, int32_t microseconds);
  * NaN outputs and counts the timeout (emoe_cache_sync_timeouts); every
  * workgroup still exits.  (2^20, 0) restores the normal launch. */
 int32_t emoe_test_set_decode_waits(emoe_cache* cache, int32_t spin_limit, int32_t unmatched);
+/* Host-only inspection of the fused decode launch (no GPU call), for tests of
+ * its work assignment: the plan of a `tokens`-token call with `capacity`
+ * co-resident workgroups into plan[9] = {router workgroups, gate/up workers,
+ * workers, row-block pairs per gate/up item, down row blocks per gate/up
+ * worker, per tail worker, down lag (pairs), tail pairs, down input groups
+ * per wavefront}, and for workers 0 .. min(workers, max_workers) - 1 (worker
+ * w is workgroup routers + w) the down work work[3w .. 3w+2] = {pair, first
+ * row block, row blocks} (pair -1 / 0 row blocks: none).  Gate/up worker w
+ * computes the gate/up item w of pair w / c, with c = ceil(d_ff / 16 / row-block
+ * pairs per item) items per pair; every wait of a worker is for workgroups of
+ * lower index.  EMOE_ESHAPE when
+ * the call does not fit one fused launch, EMOE_EINVAL for NULL pointers or a
+ * capacity below 1. */
+int32_t emoe_debug_fused_plan(const emoe_dims* dims, int32_t tokens, int32_t capacity,
+                              int32_t* plan, int32_t* work, int32_t max_workers);
 
 /* ---------------------------------------------------------------- kernel timing */
 /* Kernels launched by the layer calls, as reported by emoe_profile_end. */

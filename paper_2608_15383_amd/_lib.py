@@ -92,6 +92,7 @@ SIGNATURES = {
     "emoe_test_fail_copy_after": (_i32, [C.c_int64]),
     "emoe_test_set_wave_delay": (_i32, [_vp, _i32]),
     "emoe_test_set_decode_waits": (_i32, [_vp, _i32, _i32]),
+    "emoe_debug_fused_plan": (_i32, [_dimsp, _i32, _i32, _vp, _vp, _i32]),
     "emoe_decoder_kv_bytes": (C.c_size_t, [C.POINTER(DecoderDims)]),
     "emoe_decoder_workspace_bytes": (C.c_size_t, [C.POINTER(DecoderDims), _i32]),
     "emoe_decoder_create": (_i32, [C.POINTER(DecoderDims), C.POINTER(DecoderWeights),

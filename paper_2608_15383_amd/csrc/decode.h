@@ -96,6 +96,15 @@ struct DecodeProgress {
 
 // Size the grid; false if the layer does not fit one co-resident fused launch.
 bool decode_fused_plan(DecodeArgs& a);
+// The same for `cap` co-resident workgroups (no device query).
+bool decode_fused_plan_for(DecodeArgs& a, int cap);
+
+// The output row blocks [rb0, rb0 + nu) of pair q that worker wk (workgroup
+// n_router + wk) of a planned launch computes; nu = 0: none.
+struct FusedDownWork {
+  int q = -1, rb0 = 0, nu = 0;
+};
+__host__ __device__ FusedDownWork fused_down_work(const DecodeArgs& a, int wk);
 // Launch a planned call on `stream` (no host synchronization): a direct
 // launch takes the next epoch from `prog`, a launch being captured into a
 // graph takes its epochs from device memory.

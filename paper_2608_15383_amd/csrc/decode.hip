@@ -301,6 +301,43 @@ constexpr int kDownEarly = 2;
 template <int kGW>
 constexpr int kDownEarlyMany = 8 / kGW;  // eight tiles per wavefront
 
+}  // namespace
+
+// The down row blocks [rb0, rb0 + nu) of pair q that worker wk of a planned
+// launch computes (nu = 0: none): gate/up worker wk (wk < n_gate, pair
+// p = wk / chunks) takes pair p - down_lag unless that is one of the last
+// tail_pairs pairs, which the tail workers take, per_pair workers of tail_r
+// row blocks per pair.  Host and device share it (the kernel and the plan
+// checks).
+__host__ __device__ FusedDownWork fused_down_work(const DecodeArgs& a, int wk) {
+  const int P = a.tokens * a.top_k;
+  const int n_rb = a.d / kTileRows;
+  const int chunks = (a.f / kTileRows + a.pairs_per_item - 1) / a.pairs_per_item;
+  FusedDownWork w;
+  const bool is_gate = wk < a.n_gate;
+  if (is_gate) {
+    w.q = wk / chunks - a.down_lag;
+    if (w.q >= P - a.tail_pairs) w.q = -1;  // the tail workers' pairs
+    w.rb0 = (wk % chunks) * a.down_r;
+  } else {
+    // Tail worker j: pair P - tail_pairs + j / per_pair, row-block set j % per_pair.
+    const int per_pair = (n_rb + a.tail_r - 1) / a.tail_r;
+    int j = wk - a.n_gate;
+    w.q = P - a.tail_pairs;
+    while (j >= per_pair) {
+      j -= per_pair;
+      ++w.q;
+    }
+    w.rb0 = j * a.tail_r;
+  }
+  const int r = is_gate ? a.down_r : a.tail_r;
+  w.nu = w.q < 0 ? 0 : (n_rb - w.rb0 < r ? n_rb - w.rb0 : r);
+  if (w.nu < 0) w.nu = 0;
+  return w;
+}
+
+namespace {
+
 // kDevEpoch: the launch is being captured into a graph and reads its epoch
 // from DecodeSync (a.epoch is 0); otherwise a.epoch is the host's number.
 // kGW: input groups of the down projection per wavefront (d_ff <= 512 kGW).
@@ -398,25 +435,9 @@ __global__ __launch_bounds__(256, 3) void decode_fused_kernel(DecodeArgs a) {
   // token's outputs.
   const int wk = blk - a.n_router;
   const bool is_gate = wk < a.n_gate;
-  const int n_rb = a.d / kTileRows;
   const int chunks = (a.f / kTileRows + a.pairs_per_item - 1) / a.pairs_per_item;
-  int q, rb0;
-  if (is_gate) {
-    q = wk / chunks - a.down_lag;
-    if (q >= P - a.tail_pairs) q = -1;  // the tail workers' pairs
-    rb0 = (wk % chunks) * a.down_r;
-  } else {
-    // Tail worker j: pair P - tail_pairs + j / per_pair, row-block set j % per_pair.
-    const int per_pair = (n_rb + a.tail_r - 1) / a.tail_r;
-    int j = wk - a.n_gate;
-    q = P - a.tail_pairs;
-    while (j >= per_pair) {
-      j -= per_pair;
-      ++q;
-    }
-    rb0 = j * a.tail_r;
-  }
-  const int nu = q < 0 ? 0 : max(0, min(is_gate ? a.down_r : a.tail_r, n_rb - rb0));
+  const FusedDownWork dw = fused_down_work(a, wk);
+  const int q = dw.q, rb0 = dw.rb0, nu = dw.nu;
   const bool is_comb = nu > 0 && q % a.top_k == a.top_k - 1;  // combines token q / k
   const bool writes_routing = wk == a.n_gate;                  // the first tail worker
 
@@ -744,6 +765,10 @@ int fused_capacity() {
 }  // namespace
 
 bool decode_fused_plan(DecodeArgs& a) {
+  return decode_fused_plan_for(a, min(fused_capacity(), kFusedMaxBlocks));
+}
+
+bool decode_fused_plan_for(DecodeArgs& a, int cap) {
   if (a.tokens < 1 || a.tokens > kFusedMaxTokens || a.tokens * a.top_k > kFusedMaxPairs)
     return false;
   if (a.d > kFusedMaxD || a.f > 4 * 4 * kGroup) return false;  // sync words; kGW <= 4
@@ -762,7 +787,7 @@ bool decode_fused_plan(DecodeArgs& a) {
   a.n_router = a.logits_override
                    ? 1
                    : ((a.n_experts + a.router_experts - 1) / a.router_experts) << a.router_shift;
-  const int cap = min(fused_capacity(), kFusedMaxBlocks);
+  cap = min(cap, kFusedMaxBlocks);
   // The most gate/up items (fewest row-block pairs each) that fit, with the
   // down row blocks of each pair spread over the items of pair p + lag and
   // the last tail pairs' over as many tail workers as the remaining room
@@ -824,6 +849,32 @@ hipError_t launch_decode_fused(DecodeArgs& a, DecodeProgress& prog, hipStream_t 
 }
 
 }  // namespace emoe
+
+// Host only: the fused launch's plan for `capacity` co-resident workgroups
+// and every worker's down work (see exactmoe.h).
+extern "C" int32_t emoe_debug_fused_plan(const emoe_dims* dims, int32_t tokens, int32_t capacity,
+                                         int32_t* plan, int32_t* work, int32_t max_workers) {
+  if (!dims || !plan || (max_workers > 0 && !work) || max_workers < 0 || capacity < 1)
+    return EMOE_EINVAL;
+  if (emoe_check_dims(dims) != EMOE_OK) return EMOE_ESHAPE;
+  emoe::DecodeArgs a{};
+  a.tokens = tokens;
+  a.d = dims->d_model;
+  a.f = dims->d_ff;
+  a.n_experts = dims->n_experts;
+  a.top_k = dims->top_k;
+  if (!emoe::decode_fused_plan_for(a, capacity)) return EMOE_ESHAPE;
+  const int32_t v[9] = {a.n_router, a.n_gate,   a.n_work,    a.pairs_per_item, a.down_r,
+                        a.tail_r,   a.down_lag, a.tail_pairs, a.gw};
+  for (int i = 0; i < 9; ++i) plan[i] = v[i];
+  for (int wk = 0; wk < a.n_work && wk < max_workers; ++wk) {
+    const emoe::FusedDownWork w = emoe::fused_down_work(a, wk);
+    work[3 * wk] = w.q;
+    work[3 * wk + 1] = w.rb0;
+    work[3 * wk + 2] = w.nu;
+  }
+  return EMOE_OK;
+}
 
 #ifdef EMOE_PHASE_TRACE
 // Measurement builds only: copy the phase timestamps of the first n_blocks

@@ -124,3 +124,87 @@ def test_cache_argument_errors():
     assert ei.value.status == EMOE_EINVAL
     assert cache.state()[0].tolist() == [-1] * 8    # failed calls change nothing
     cache.close()
+
+
+# ------------------------------------------------------------ fused decode plan
+def _fused_plan(dm, tokens, cap):
+    plan = (ctypes.c_int32 * 9)()
+    work = (ctypes.c_int32 * (3 * 1024))()
+    rc = lib().emoe_debug_fused_plan(ctypes.byref(dm), tokens, cap, plan, work, 1024)
+    if rc != 0:
+        return rc, None, None
+    keys = ("n_router", "n_gate", "n_work", "ppi", "down_r", "tail_r", "lag", "tail_pairs", "gw")
+    p = dict(zip(keys, list(plan)))
+    w = np.frombuffer(work, dtype=np.int32)[:3 * p["n_work"]].reshape(-1, 3)
+    return rc, p, w
+
+
+def _check_fused_assignment(d, f, E, k, T, cap):
+    """Every (pair, output row block) of the down projection is computed by
+    exactly one worker; a worker reads an activation row only from gate/up
+    workers of lower index, and a combining worker (last pair of a token)
+    reads the token's other outputs only from workers of lower index."""
+    dm = api.dims(d, f, E, k)
+    rc, p, w = _fused_plan(dm, T, cap)
+    if rc != 0:
+        assert rc == EMOE_ESHAPE
+        return None
+    P, n_rb = T * k, d // 16
+    chunks = -(-(f // 16) // p["ppi"])
+    assert p["n_gate"] == P * chunks
+    assert p["n_router"] + p["n_work"] <= min(cap, 1024)
+    assert 1 <= p["lag"] <= p["tail_pairs"] <= P
+    producer = {}
+    for wk, (q, rb0, nu) in enumerate(w):
+        blk = p["n_router"] + wk
+        if nu == 0:
+            continue
+        assert 0 <= q < P and 0 <= rb0 and rb0 + nu <= n_rb
+        if wk < p["n_gate"]:
+            assert q == wk // chunks - p["lag"] and q < P - p["tail_pairs"]
+        else:
+            assert q >= P - p["tail_pairs"]
+        # The activation row of pair q comes from gate/up workers of pair q.
+        assert p["n_router"] + (q + 1) * chunks - 1 < blk, (wk, q)
+        for r in range(rb0, rb0 + nu):
+            assert (q, r) not in producer, (q, r)
+            producer[(q, r)] = blk
+    assert len(producer) == P * n_rb
+    for (q, r), blk in producer.items():
+        if q % k == k - 1:
+            for j in range(q - (k - 1), q):
+                assert producer[(j, r)] < blk, (q, j, r)
+    return p
+
+
+@pytest.mark.parametrize("d,f,E,k", [(2048, 1024, 64, 8), (256, 128, 8, 2), (384, 256, 6, 3),
+                                     (256, 384, 1, 1), (128, 128, 200, 8), (2048, 2048, 8, 4),
+                                     (512, 1536, 8, 2), (4096, 4096, 64, 8)])
+@pytest.mark.parametrize("T", [1, 2, 3, 4])
+@pytest.mark.parametrize("cap", [768, 512, 1024, 300])
+def test_fused_decode_work_assignment(d, f, E, k, T, cap):
+    _check_fused_assignment(d, f, E, k, T, cap)
+
+
+def test_fused_decode_plan_at_olmoe_shape():
+    """One token: 64 one-expert router items, 512 one-pair gate/up items, a
+    down lag of two pairs and 192 tail workers for the last three pairs;
+    four tokens: 32 router items, items of four row-block pairs and 128 tail
+    workers for the last two pairs."""
+    p1 = _check_fused_assignment(2048, 1024, 64, 8, 1, 768)
+    assert (p1["n_router"], p1["n_gate"], p1["n_work"], p1["ppi"], p1["down_r"], p1["tail_r"],
+            p1["lag"], p1["tail_pairs"], p1["gw"]) == (64, 512, 704, 1, 2, 2, 2, 3, 2)
+    p4 = _check_fused_assignment(2048, 1024, 64, 8, 4, 768)
+    assert (p4["n_router"], p4["n_gate"], p4["n_work"], p4["ppi"], p4["down_r"], p4["tail_r"],
+            p4["lag"], p4["tail_pairs"]) == (32, 512, 640, 4, 8, 2, 2, 2)
+
+
+def test_fused_decode_plan_rejections():
+    dm = api.dims(2048, 1024, 64, 8)
+    for T in (0, 5):
+        assert _fused_plan(dm, T, 768)[0] == EMOE_ESHAPE
+    assert _fused_plan(dm, 1, 0)[0] == EMOE_EINVAL
+    assert _fused_plan(dm, 1, 100)[0] == EMOE_ESHAPE  # the grid does not fit
+    plan = (ctypes.c_int32 * 9)()
+    assert lib().emoe_debug_fused_plan(ctypes.byref(dm), 1, 768, None, None, 0) == EMOE_EINVAL
+    assert lib().emoe_debug_fused_plan(ctypes.byref(dm), 1, 768, plan, None, 4) == EMOE_EINVAL
