@@ -29,7 +29,10 @@
 //    this wavefront's outstanding loads.
 // Work items (row tile, column tile) are dealt to the XCDs in contiguous
 // eighths, so the column tiles of a row tile and the row tiles of an expert
-// share one L2.
+// share one L2.  The gate/up launch is persistent (each workgroup takes
+// several items of its XCD's eighth in turn); the down launch takes one item
+// per workgroup.
+#include <mutex>
 #include <type_traits>
 
 #include "common.h"
@@ -172,12 +175,13 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
   // tile) order, so the column tiles of a row tile and the row tiles of an
   // expert meet in one L2 and its token rows and weights cross the fabric
   // about once.
+  // Gate/up: the grid holds at most the co-resident workgroups, and
+  // workgroup i takes the items i / 8, i / 8 + gridDim / 8, ... of its XCD's
+  // eighth in turn (no workgroup launch per item); down: one item per
+  // workgroup.
   const int n_items = gv.tile_offsets[n_experts] * n_ctiles;
   const int per_xcd = (n_items + kXcds - 1) / kXcds;
-  const int xj = blockIdx.x / kXcds;
-  if (xj >= per_xcd) return;
-  const int item = (blockIdx.x % kXcds) * per_xcd + xj;
-  if (item >= n_items) return;
+  auto run_item = [&](const int item) __attribute__((always_inline)) {
   const int tile = item / n_ctiles;
   const int ctile = item - tile * n_ctiles;
   // Row tile -> expert (largest e with tile_offsets[e] <= tile).
@@ -492,6 +496,22 @@ __global__ __launch_bounds__(Sh::kThreads, Sh::kBlocksPerCu) void grouped_mfma_k
       }
     }
   }
+  };
+  if constexpr (kGateUp) {
+    const int xstride = (int)gridDim.x / kXcds;
+    for (int xj = blockIdx.x / kXcds; xj < per_xcd; xj += xstride) {
+      const int item = (blockIdx.x % kXcds) * per_xcd + xj;
+      if (item >= n_items) break;
+      run_item(item);
+      barrier();  // the next item's prologue writes the LDS this epilogue reads
+    }
+  } else {
+    const int xj = blockIdx.x / kXcds;
+    if (xj >= per_xcd) return;
+    const int item = (blockIdx.x % kXcds) * per_xcd + xj;
+    if (item >= n_items) return;
+    run_item(item);
+  }
 }
 
 // bias[t][g] = -136 * sum of x[t][128g .. 128g+127] (fp32, fixed order): the
@@ -528,15 +548,39 @@ inline int max_row_tiles(int pairs, int n_experts) {
   return (pairs + kRows - 1) / kRows + e;
 }
 
-// Workgroups for n_ctiles column tiles and up to max_row_tiles row tiles: a
-// multiple of the XCD count, so every XCD gets its eighth of the items.
-inline int mfma_grid(int n_ctiles, int pairs, int n_experts) {
-  const int n = n_ctiles * max_row_tiles(pairs, n_experts);
-  return (n + kXcds - 1) / kXcds * kXcds;
-}
-
 // Launch shape of both projections.
 using MfmaShape = Shape<4>;
+
+// Co-resident workgroups of the gate/up projection on the current device,
+// rounded down to a multiple of the XCD count (0 if unknown).
+int gateup_resident() {
+  static std::mutex mu;
+  static int cap[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  std::lock_guard<std::mutex> lk(mu);
+  if (cap[dev] == 0) {
+    int n = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &n, reinterpret_cast<const void*>(grouped_mfma_kernel<true, MfmaShape>),
+            MfmaShape::kThreads, 0) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    cap[dev] = n * cus / kXcds * kXcds;
+  }
+  return cap[dev];
+}
+
+// Workgroups for n_ctiles column tiles and up to max_row_tiles row tiles: a
+// multiple of the XCD count, so every XCD gets its eighth of the items; at
+// most `limit` (then each takes several items in turn) when limit >= 8.
+inline int mfma_grid(int n_ctiles, int pairs, int n_experts, int limit) {
+  const int n = n_ctiles * max_row_tiles(pairs, n_experts);
+  const int all = (n + kXcds - 1) / kXcds * kXcds;
+  return limit >= kXcds && limit < all ? limit : all;
+}
 
 }  // namespace
 
@@ -554,7 +598,8 @@ hipError_t launch_gateup_mfma(int tokens, int d, int f, int top_k, int n_experts
   if (pairs == 0) return hipSuccess;
   constexpr int kCols = MfmaShape::kCols;
   const int n_ctiles = (2 * f + kCols - 1) / kCols;
-  launch(grouped_mfma_kernel<true, MfmaShape>, dim3(mfma_grid(n_ctiles, pairs, n_experts)),
+  launch(grouped_mfma_kernel<true, MfmaShape>,
+         dim3(mfma_grid(n_ctiles, pairs, n_experts, gateup_resident())),
          dim3(MfmaShape::kThreads), stream, d, f, top_k, n_experts, h,
          (uint32_t)((int64_t)tokens * d * 2), h_bias, pairs,
          gv, wave, slot_bank, record_bytes, n_ctiles, act, act_bias, (uint16_t*)nullptr,
@@ -570,7 +615,7 @@ hipError_t launch_down_mfma(int tokens, int d, int f, int top_k, int n_experts, 
   if (pairs == 0) return hipSuccess;
   constexpr int kCols = MfmaShape::kCols;
   const int n_ctiles = (d + kCols - 1) / kCols;
-  launch(grouped_mfma_kernel<false, MfmaShape>, dim3(mfma_grid(n_ctiles, pairs, n_experts)),
+  launch(grouped_mfma_kernel<false, MfmaShape>, dim3(mfma_grid(n_ctiles, pairs, n_experts, 0)),
          dim3(MfmaShape::kThreads), stream, d, f, top_k, n_experts, act,
          (uint32_t)((int64_t)pairs * f * 2), act_bias, pairs,
          gv, wave, slot_bank, record_bytes, n_ctiles, (uint16_t*)nullptr, (float*)nullptr, pair_out,
